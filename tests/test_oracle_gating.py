@@ -1,0 +1,113 @@
+"""Pins of the gating oracle (Sec. 2.1) against brute force, closed forms and
+hand-worked values; none of these re-types the oracle's own formulas."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_17954_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def brute_force_topk(z, k):
+    """rank(e) = #{e': z_e' > z_e or (z_e' == z_e and e' < e)}; selected iff
+    rank < k; listed by rank."""
+    T, E = z.shape
+    out = np.empty((T, k), dtype=np.int64)
+    for t in range(T):
+        ranks = []
+        for e in range(E):
+            r = 0
+            for e2 in range(E):
+                if z[t, e2] > z[t, e] or (z[t, e2] == z[t, e] and e2 < e):
+                    r += 1
+            ranks.append(r)
+        for e in range(E):
+            if ranks[e] < k:
+                out[t, ranks[e]] = e
+    return out
+
+
+@pytest.mark.parametrize("E,k,levels", [(8, 2, None), (8, 2, 3), (60, 4, 5),
+                                        (64, 6, None), (5, 5, 2), (1, 1, None),
+                                        (16, 1, 2)])
+def test_topk_matches_brute_force_ranking(E, k, levels):
+    z = synth.random_logits(40, E, seed=E * 10 + k, levels=levels).astype(np.float64)
+    assert np.array_equal(oracle.topk_select(z, k), brute_force_topk(z, k))
+
+
+def test_all_equal_logits_pick_lowest_indices():
+    z = np.full((3, 8), 0.25)
+    assert np.array_equal(oracle.topk_select(z, 3), np.tile([0, 1, 2], (3, 1)))
+
+
+def test_signed_zeros_compare_equal():
+    z = np.array([[-0.0, 0.0, -0.0, -1.0]])
+    assert oracle.topk_select(z, 3).tolist() == [[0, 1, 2]]
+
+
+def test_k_equals_E_selects_every_expert():
+    z = synth.random_logits(10, 7, seed=3).astype(np.float64)
+    idx = oracle.topk_select(z, 7)
+    assert (np.sort(idx, axis=1) == np.arange(7)).all()
+    assert (np.diff(np.take_along_axis(z, idx, 1), axis=1) <= 0).all()
+
+
+def test_hand_example():
+    g = json.load(open(os.path.join(GOLDEN, "gating_hand_example.json")))
+    z = np.array(g["logits"])
+    idx = oracle.topk_select(z, g["k"])
+    assert idx.tolist() == g["idx"]
+    assert np.allclose(oracle.gate_weights(z, idx, False), g["w_raw"], rtol=0, atol=1e-15)
+    assert np.allclose(oracle.gate_weights(z, idx, True), g["w_renorm"], rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("E,k", [(8, 2), (60, 4), (64, 6)])
+def test_renormalised_gates_are_softmax_over_selected_logits(E, k):
+    z = synth.random_logits(25, E, seed=7 + E).astype(np.float64) * 3
+    idx = oracle.topk_select(z, k)
+    w = oracle.gate_weights(z, idx, True)
+    for t in range(z.shape[0]):
+        sel = [z[t, e] for e in idx[t]]
+        m = max(sel)
+        den = sum(math.exp(v - m) for v in sel)
+        for j in range(k):
+            assert abs(w[t, j] - math.exp(sel[j] - m) / den) <= 1e-15
+    assert np.allclose(w.sum(axis=1), 1.0, rtol=0, atol=1e-12)
+
+
+def test_raw_gates_are_softmax_scores():
+    z = synth.random_logits(12, 8, seed=11).astype(np.float64)
+    idx = oracle.topk_select(z, 2)
+    w = oracle.gate_weights(z, idx, False)
+    for t in range(12):
+        den = sum(math.exp(v) for v in z[t])
+        for j in range(2):
+            assert abs(w[t, j] - math.exp(z[t, idx[t, j]]) / den) <= 1e-15
+    assert (w.sum(axis=1) < 1).all()
+
+
+def test_single_expert_gets_weight_one():
+    z = synth.random_logits(9, 1, seed=2).astype(np.float64)
+    for renorm in (True, False):
+        w = oracle.gate_weights(z, oracle.topk_select(z, 1), renorm)
+        assert np.array_equal(w, np.ones((9, 1)))
+
+
+def test_router_logits_against_loops():
+    cfg = synth.config(1)
+    inp = synth.layer_inputs(cfg, seed=1, T=6, parts=("x", "router"))
+    x, wr = inp["x"].astype(np.float64), inp["w_router"].astype(np.float64)
+    bias = np.linspace(-1, 1, cfg["E"])
+    z = oracle.router_logits(x, wr, bias)
+    for t in range(6):
+        for e in range(cfg["E"]):
+            s = sum(float(x[t, h]) * float(wr[e, h]) for h in range(cfg["H"]))
+            assert abs(z[t, e] - (s + bias[e])) <= 1e-12
+    tb = np.arange(6 * cfg["E"], dtype=np.float64).reshape(6, cfg["E"])
+    z2 = oracle.router_logits(x, wr, tb)
+    assert abs(z2[4, 3] - (z[4, 3] - bias[3] + tb[4, 3])) <= 1e-12

@@ -1,0 +1,228 @@
+"""Pins of the token-scheduler oracle (Sec. 3.3): the worked example, the
+brute-force optimum of Eq. 2, the integer reading of the similarity, and
+invariants of the balanced two-medoid iteration."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_17954_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bits(routes, E):
+    N, L, k = routes.shape
+    b = np.zeros((N, L * E), dtype=np.int64)
+    for i in range(N):
+        for l in range(L):
+            for j in range(k):
+                b[i, l * E + int(routes[i, l, j])] = 1
+    return b
+
+
+def _eq2_sets(routes, E, batches):
+    """Eq. 2 from its definition: OR the routes of each batch, count ones."""
+    total = 0
+    for members in batches:
+        active = set()
+        for i in members:
+            for l in range(routes.shape[1]):
+                for j in range(routes.shape[2]):
+                    active.add((l, int(routes[i, l, j])))
+        total += len(active)
+    return total
+
+
+def _random_routes(N, L, E, k, seed):
+    return synth.predicted_routes(N, L, E, k, keep=0.5, s=0.8, seed=seed).astype(np.int64)
+
+
+def test_worked_example_from_the_paper():
+    g = json.load(open(os.path.join(GOLDEN, "ts_worked_example.json")))
+    routes = np.array(g["routes"])
+    perm, demand, info = oracle.schedule(routes, g["E"], g["n1"])
+    iters, conv, m1, m2, before, after, used_orig, n1 = info.tolist()
+    assert before == g["obj_before"] and after == g["obj_optimum"]
+    assert (iters, conv, used_orig, n1) == (1, 1, 0, 4)
+    assert sorted(perm[:4].tolist()) == perm[:4].tolist()
+    # every batch holds both tokens of each of its two experts
+    b1 = routes[perm[:4], 0, 0].tolist()
+    assert sorted(b1) in ([0, 0, 2, 2], [0, 0, 1, 1], [0, 0, 3, 3], [1, 1, 2, 2],
+                          [1, 1, 3, 3], [2, 2, 3, 3])
+    assert demand.sum() == 8
+    # the optimum stated in the fixture is the enumerated optimum
+    best = min(_eq2_sets(routes, 4, [c, [i for i in range(8) if i not in c]])
+               for c in itertools.combinations(range(8), 4))
+    assert best == g["obj_optimum"]
+
+
+def test_eq2_objective_matches_definition():
+    routes = _random_routes(20, 3, 6, 2, seed=1)
+    bits = _bits(routes, 6)
+    g = np.random.default_rng(2)
+    for _ in range(10):
+        mask = g.random(20) < 0.5
+        ref = _eq2_sets(routes, 6, [np.nonzero(mask)[0], np.nonzero(~mask)[0]])
+        assert oracle.eq2_objective(bits, mask) == ref
+
+
+def test_route_bits_and_hamming_against_loops():
+    routes = _random_routes(15, 4, 8, 3, seed=3)
+    bits = oracle.route_bits(routes, 8).reshape(15, -1)
+    assert np.array_equal(bits, _bits(routes, 8))
+    for m in (0, 7, 14):
+        d = oracle.hamming_to(bits, m)
+        for i in range(15):
+            assert d[i] == sum(int(a) ^ int(b) for a, b in zip(bits[i], bits[m]))
+
+
+def test_distance_sums_against_pairwise_xor():
+    routes = _random_routes(24, 5, 7, 2, seed=4)
+    bits = _bits(routes, 7)
+    g = np.random.default_rng(5)
+    for _ in range(5):
+        members = np.sort(g.choice(24, size=int(g.integers(1, 24)), replace=False))
+        got = oracle.cluster_distance_sums(bits, members)
+        for a, i in enumerate(members):
+            ref = sum(int(np.bitwise_xor(bits[i], bits[j]).sum()) for j in members)
+            assert got[a] == ref
+
+
+def test_similarity_argmax_is_distance_argmin():
+    """The centroid is the member with the highest mean S_ij = 1 - d_ij/(LE);
+    in integers that is the least summed Hamming distance."""
+    routes = _random_routes(18, 4, 6, 2, seed=6)
+    L, E = 4, 6
+    bits = _bits(routes, E)
+    members = np.arange(0, 18, 2)
+    sims = [np.mean([1.0 - np.bitwise_xor(bits[i], bits[j]).sum() / (L * E)
+                     for j in members]) for i in members]
+    dsum = oracle.cluster_distance_sums(bits, members)
+    best_sim = max(sims)
+    assert {int(members[a]) for a in range(len(members)) if sims[a] == best_sim} == \
+           {int(members[a]) for a in range(len(members)) if dsum[a] == dsum.min()}
+
+
+def test_signature_rank_against_sorted_tuples():
+    routes = _random_routes(60, 4, 5, 2, seed=7)
+    routes[10] = routes[3]              # duplicate signatures tie by index
+    routes[50] = routes[3]
+    keys = [tuple(v for l in range(4) for v in sorted(routes[i, l].tolist())) + (i,)
+            for i in range(60)]
+    order = sorted(range(60), key=lambda i: keys[i])
+    rank = oracle.signature_rank(routes)
+    assert [int(r) for r in rank[order]] == list(range(60))
+    assert rank[3] < rank[10] < rank[50]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_balanced_assignment_is_optimal_for_fixed_centres(seed):
+    routes = _random_routes(10, 3, 4, 1, seed=20 + seed)
+    bits = _bits(routes, 4)
+    m1, m2, n1 = 0, 9, 5
+    d1, d2 = oracle.hamming_to(bits, m1), oracle.hamming_to(bits, m2)
+    sig = oracle.signature_rank(routes)
+    order = np.lexsort((sig, d1 - d2))
+    cost = d1[order[:n1]].sum() + d2[order[n1:]].sum()
+    best = min(d1[list(c)].sum() + d2[[i for i in range(10) if i not in c]].sum()
+               for c in itertools.combinations(range(10), n1))
+    assert cost == best
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_result_against_brute_force_optimum(seed):
+    N, L, E, k = 12, 3, 4, 1
+    routes = _random_routes(N, L, E, k, seed=100 + seed)
+    perm, demand, info = oracle.schedule(routes, E, 6)
+    iters, conv, m1, m2, before, after, used_orig, n1 = info.tolist()
+    b1, b2 = perm[:6], perm[6:]
+    assert sorted(perm.tolist()) == list(range(N))
+    assert after == _eq2_sets(routes, E, [b1, b2])
+    assert before == _eq2_sets(routes, E, [range(6), range(6, 12)])
+    assert after <= before                           # the guard
+    best = min(_eq2_sets(routes, E, [c, [i for i in range(N) if i not in c]])
+               for c in itertools.combinations(range(N), 6))
+    assert best <= after
+    # demand counts the tokens of each batch per (layer, expert)
+    for c, members in enumerate((b1, b2)):
+        ref = np.zeros((L, E), dtype=np.int64)
+        for i in members:
+            for l in range(L):
+                ref[l, routes[i, l, 0]] += 1
+        assert np.array_equal(demand[c], ref)
+
+
+def test_planted_clusters_are_recovered():
+    L, E, k = 6, 8, 2
+    a = np.array([[0, 1]] * L)
+    b = np.array([[4, 5]] * L)
+    routes = np.stack([a] * 9 + [b] * 9)
+    pi = np.random.default_rng(8).permutation(18)
+    routes = routes[pi]
+    perm, demand, info = oracle.schedule(routes, E, 9)
+    assert info[5] == 2 * L * k and info[1] == 1
+    assert len({tuple(routes[i].ravel()) for i in perm[:9]}) == 1
+
+
+def test_identical_routes_keep_the_original_split():
+    routes = np.tile(np.array([[2, 5], [1, 3], [0, 7]]), (11, 1, 1))
+    perm, demand, info = oracle.schedule(routes, 8, 5)
+    assert perm.tolist() == list(range(11))
+    assert info[4] == info[5] == 2 * 3 * 2
+    assert info[7] == 5
+
+
+def test_fixed_point_at_convergence():
+    routes = _random_routes(40, 4, 8, 2, seed=9)
+    bits = _bits(routes, 8)
+    perm, demand, info = oracle.schedule(routes, 8, 20, max_iters=50,
+                                         keep_original_if_worse=False)
+    assert info[1] == 1
+    sig = oracle.signature_rank(routes)
+    for c, members in enumerate((np.sort(perm[:20]), np.sort(perm[20:]))):
+        dsum = oracle.cluster_distance_sums(bits, members)
+        best = members[np.lexsort((sig[members], dsum))[0]]
+        assert best == info[2 + c]
+
+
+def test_iteration_limit_reports_non_convergence():
+    found = False
+    for seed in range(40):
+        routes = _random_routes(64, 4, 8, 2, seed=300 + seed)
+        _, _, full = oracle.schedule(routes, 8, 32, max_iters=50)
+        if full[0] >= 2:
+            _, _, one = oracle.schedule(routes, 8, 32, max_iters=1)
+            assert one[0] == 1 and one[1] == 0
+            found = True
+            break
+    assert found
+
+
+@pytest.mark.parametrize("n1", [0, 7])
+def test_degenerate_batch_sizes(n1):
+    routes = _random_routes(7, 2, 4, 2, seed=10)
+    perm, demand, info = oracle.schedule(routes, 4, n1)
+    assert perm.tolist() == list(range(7))
+    assert info.tolist()[:2] == [0, 1] and info[7] == n1
+    assert demand.sum() == 7 * 2 * 2
+
+
+def test_odd_token_count_and_uneven_split():
+    routes = _random_routes(13, 3, 5, 2, seed=11)
+    perm, demand, info = oracle.schedule(routes, 5, 4)
+    assert sorted(perm.tolist()) == list(range(13))
+    assert demand[0].sum() == 4 * 3 * 2 and demand[1].sum() == 9 * 3 * 2
+
+
+def test_batch_accuracy():
+    routes = _random_routes(30, 4, 8, 2, seed=12)
+    r = oracle.route_bits(routes, 8)
+    assert oracle.batch_accuracy(r, r) == 1.0
+    # hand example: 1 layer, truth {0,1,2,3}, prediction {0,1,6}: recall 2/4
+    t = np.zeros((2, 1, 8)); t[0, 0, [0, 1]] = 1; t[1, 0, [2, 3]] = 1
+    p = np.zeros((1, 1, 8)); p[0, 0, [0, 1, 6]] = 1
+    assert oracle.batch_accuracy(t, p) == 0.5
