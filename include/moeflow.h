@@ -1,0 +1,212 @@
+/*
+ * moeflow.h -- C ABI of libmoeflow.so, the MI355X (gfx950) hot path of the
+ * MoE layer of ExpertFlow (arXiv 2410.17954) executed over route-grouped
+ * token batches:
+ *
+ *   moe_route       softmax top-k gating                        (Sec. 2.1)
+ *   moe_schedule    balanced rebatching of two adjacent batches
+ *                   by predicted routing path                   (Sec. 3.3, Eq. 2)
+ *   moe_permute     expert-major grouping of (token, choice) pairs
+ *   moe_expert_ffn  grouped SwiGLU experts over the resident
+ *                   slots of the expert cache                   (Sec. 2.1, 3.4)
+ *   moe_combine     gate-weighted sum of expert outputs         (Sec. 2.1)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory: every array argument is DEVICE memory owned by the caller, row-major
+ *   and densely packed. The library never allocates, frees or synchronises;
+ *   scratch memory comes from a caller-provided workspace whose size the
+ *   matching *_workspace query returns (0 means none is needed). The
+ *   workspace must be 256-byte aligned. Its contents on entry do not matter.
+ * Ordering: every call only enqueues work on `stream` (a hipStream_t passed as
+ *   void*; NULL = the default stream) and returns; outputs are valid once that
+ *   work completes. Calls on different streams with disjoint outputs and
+ *   workspaces may run concurrently. The library keeps no mutable global
+ *   state apart from a per-device cache of the device's compute-unit count.
+ * Element types: `dtype` selects MOE_BF16 (bfloat16 bit patterns, uint16) or
+ *   MOE_F32 for activations and weights. Logits, biases and gate weights are
+ *   always float32; ids and maps are int32.
+ * Errors: each call returns MOE_OK or a positive moe_status. Arguments are
+ *   validated on the host before anything is enqueued; a failed validation
+ *   enqueues nothing and touches no device state. MOE_ERR_HIP reports a
+ *   launch failure. Nothing throws across the ABI.
+ * Device-side preconditions (ids in range, k distinct experts per route
+ *   layer, finite values) cannot be checked without synchronising. The
+ *   kernels never read or write outside the arrays described here whatever
+ *   those values are, but results are unspecified when they are violated.
+ */
+#ifndef MOEFLOW_H
+#define MOEFLOW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum moe_status {
+  MOE_OK = 0,
+  MOE_ERR_ARG = 1,          /* null required pointer, bad size or flag     */
+  MOE_ERR_UNSUPPORTED = 2,  /* valid request outside what the kernels do   */
+  MOE_ERR_WORKSPACE = 3,    /* workspace missing, too small or misaligned  */
+  MOE_ERR_HIP = 4           /* a HIP launch or query failed                */
+};
+
+enum moe_dtype { MOE_F32 = 0, MOE_BF16 = 1 };
+
+/* Version of this interface; bumped on any incompatible change. */
+#define MOEFLOW_ABI_VERSION 1
+int moe_abi_version(void);
+
+/* Static, human-readable name of a status code. */
+const char* moe_status_str(int status);
+
+/* ------------------------------------------------------------------------
+ * moe_route -- gating (Sec. 2.1: scores softmax(x W_g), the k experts with
+ * the highest scores, each weighted by its score).
+ *
+ *   z[t,e]    = sum_h x[t,h] * w_gate[e,h]  (+ bias)       float32 accumulation
+ *   idx[t,:]  = the k largest z[t,:], descending; equal logits go to the lower
+ *               expert index; -0.0 == +0.0
+ *   w[t,j]    = softmax(z[t,:])[idx[t,j]]               (renormalize = 0)
+ *             = the same divided by sum_j of it, i.e. the softmax over the k
+ *               selected logits                          (renormalize = 1)
+ *
+ * x        [T,H] dtype     hidden states                     (x-mode)
+ * w_gate   [E,H] dtype     router weight, one row per expert (x-mode)
+ * bias     float32, NULL (bias_mode 0), [E] (bias_mode 1) or [T,E] (bias_mode 2)
+ * logits   [T,E] float32   x-mode: optional output (NULL = not written);
+ *                          logits-in mode: required input
+ * topk_idx [T,k] int32     output
+ * topk_w   [T,k] float32   output
+ * Logits-in mode: x == NULL and w_gate == NULL; then bias must be NULL and
+ *   the gate is computed from the given logits (dtype and H are ignored).
+ * Limits: T >= 1, 1 <= k <= E <= 256; x-mode bf16 needs H % 8 == 0, f32 needs
+ *   H >= 1.
+ * ---------------------------------------------------------------------- */
+int moe_route(const void* x, const void* w_gate, int32_t dtype,
+              int64_t T, int64_t H, int32_t E, int32_t k,
+              const float* bias, int32_t bias_mode, int32_t renormalize,
+              float* logits, int32_t* topk_idx, float* topk_w, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_schedule -- the Token Scheduler (Sec. 3.3): split N tokens (two adjacent
+ * batches) into batches of n1 and N - n1 tokens so that few (layer, expert)
+ * pairs are active per batch (Eq. 2), by the balanced two-centroid clustering
+ * under routing-path similarity of Sec. 3.3.2, in exact integer form:
+ *
+ *   routes  [N,L,k] uint8   predicted expert ids per token and layer; the
+ *                           routing path r_i has bit l*E+e set iff e appears
+ *                           in routes[i,l,:]
+ *   sig order   tokens ordered by their per-layer ascending expert ids, layer
+ *               0 first, then by index; every tie below goes to the token
+ *               earlier in this order
+ *   init        m1 = least total Hamming distance to all tokens;
+ *               m2 = farthest from m1
+ *   assign      order tokens by d(i,m1) - d(i,m2); the first n1 are batch 1
+ *   update      m_c = least summed distance to the members of batch c
+ *   stop        centroids unchanged (converged) or max_iters rounds
+ *   guard       keep_original_if_worse = 1: if the result activates more pairs
+ *               than the input split ([0,n1), [n1,N)), return the input split
+ *
+ * perm    [N] int32      batch 1's token ids ascending, then batch 2's
+ * demand  [2,L,E] int32  tokens of each new batch using (l, e); may be NULL
+ * info    [8] int64      {iters, converged, medoid1, medoid2, obj_before,
+ *                         obj_after, used_original, n1}
+ * Limits: N >= 1, 0 <= n1 <= N, L >= 1, 1 <= k <= E <= 256, max_iters >= 1,
+ *   N < 2^26, L*E < 2^24. n1 == 0 or n1 == N returns the identity with iters = 0.
+ * ---------------------------------------------------------------------- */
+size_t moe_schedule_workspace(int64_t N, int32_t L, int32_t E, int32_t k);
+int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t E, int32_t k,
+                 int64_t n1, int32_t max_iters, int32_t keep_original_if_worse,
+                 int32_t* perm, int32_t* demand, int64_t* info,
+                 void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_permute -- group the (token, choice) pairs of one batch by expert so
+ * that every expert sees its tokens as one contiguous block of rows.
+ *
+ * Batch position i (0 <= i < T) is token t_i = token_ids[i] (or i when
+ * token_ids is NULL); pair p = i*k + j is its j-th choice, on expert
+ * e_p = topk_idx[t_i, j].
+ *   expert_offsets[e]  = number of pairs on experts < e    ([E+1] int32 out)
+ *   row_of_pair[p]     = expert_offsets[e_p] + number of pairs p' < p on e_p
+ *                        (stable)                           ([T*k] int32 out)
+ *   pair_of_row[r]     = the inverse map                    ([T*k] int32 out)
+ *   x_perm[row(p), :]  = x[t_i, :] bit for bit              ([T*k,H] out)
+ * x        [n_tokens,H] dtype; x and x_perm may both be NULL (maps only)
+ * topk_idx [n_tokens,k] int32, indexed by token id
+ * Limits: T >= 1, 1 <= k <= E <= 256, token ids < n_tokens, T*k < 2^31,
+ *   bf16 needs H % 8 == 0, f32 needs H % 4 == 0.
+ * ---------------------------------------------------------------------- */
+size_t moe_permute_workspace(int64_t T, int32_t k, int32_t E);
+int moe_permute(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
+                const int32_t* token_ids, int64_t T,
+                const int32_t* topk_idx, int32_t k, int32_t E,
+                int32_t* expert_offsets, int32_t* row_of_pair, int32_t* pair_of_row,
+                void* x_perm, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_expert_ffn -- the experts E_i of Sec. 2.1 in SwiGLU form, over the rows
+ * each expert owns, for experts resident in the expert cache (Sec. 3.4):
+ *
+ *   for e with s = slot_of_expert[e] >= 0, rows r in [offsets[e], offsets[e+1]):
+ *     a[r,:]      = silu(x_perm[r,:] . w_gate[s]^T) * (x_perm[r,:] . w_up[s]^T)
+ *     y_perm[r,:] = a[r,:] . w_down[s]^T
+ *   silu(u) = u / (1 + exp(-u)); float32 accumulation; for bf16 the
+ *   activation a is rounded to bf16 before the down projection and y_perm is
+ *   rounded to bf16. Rows of experts with slot < 0 (cache misses) are left
+ *   untouched.
+ *
+ * x_perm         [max_rows,H] dtype
+ * expert_offsets [E+1] int32 non-decreasing, expert_offsets[E] <= max_rows
+ * slot_of_expert [E] int32, values < S (or -1); NULL means expert e uses slot
+ *                e (then S >= E)
+ * w_gate, w_up   [S,F,H] dtype;  w_down [S,H,F] dtype
+ * y_perm         [max_rows,H] dtype output
+ * Shared (always-on) experts use the same call with E = 1, offsets {0, T},
+ * slot {0} and their weights concatenated along F.
+ * Limits: max_rows >= 1, H >= 1, F >= 1, 1 <= E <= 256, S >= 0; bf16 needs
+ *   H % 8 == 0 and F % 8 == 0.
+ * ---------------------------------------------------------------------- */
+size_t moe_expert_ffn_workspace(int64_t max_rows, int64_t H, int64_t F, int32_t E,
+                                int32_t dtype);
+int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_rows,
+                   int64_t H, int64_t F,
+                   const int32_t* expert_offsets, int32_t E,
+                   const int32_t* slot_of_expert, int32_t S,
+                   const void* w_gate, const void* w_up, const void* w_down,
+                   void* y_perm, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_combine -- the weighted sum of Sec. 2.1, y = sum_j w_j E_{idx_j}(x),
+ * over resident experts, plus always-on shared experts:
+ *
+ *   acc = sum_{j ascending, slot(idx[t_i,j]) >= 0} topk_w[t_i,j] * y_perm[row_of_pair[i*k+j]]
+ *       + y_shared[i]                     (if y_shared != NULL)
+ *       + y[t_i]                          (if accumulate)
+ *   y[t_i] = acc                          (float32 accumulation, one rounding)
+ *   incomplete[i] = 1 if some choice of token t_i is not resident, else 0
+ *
+ * y_perm [rows,H] dtype; y_shared [T,H] dtype by batch position (may be NULL)
+ * topk_idx [n_tokens,k] int32, topk_w [n_tokens,k] float32, by token id
+ * row_of_pair [T*k] int32 (from moe_permute); slot_of_expert [E] or NULL
+ *   (all resident; E is then not needed and may be 0)
+ * y [n_tokens,H] dtype: rows t_i written, other rows untouched
+ * incomplete [T] int32 or NULL
+ * Limits: T >= 1, k >= 1, rows >= 1, token ids < n_tokens; bf16 needs
+ *   H % 8 == 0, f32 needs H % 4 == 0.
+ * ---------------------------------------------------------------------- */
+int moe_combine(const void* y_perm, int32_t dtype, int64_t H, int64_t rows,
+                const int32_t* token_ids, int64_t T, int64_t n_tokens, int32_t k,
+                const int32_t* topk_idx, const float* topk_w,
+                const int32_t* row_of_pair, const int32_t* slot_of_expert, int32_t E,
+                const void* y_shared, int32_t accumulate, void* y,
+                int32_t* incomplete, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOEFLOW_H */

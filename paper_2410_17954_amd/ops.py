@@ -1,0 +1,313 @@
+"""Thin Python binding of libmoeflow.so (include/moeflow.h).
+
+Every function here only marshals arguments: it checks tensor placement,
+dtype and shape, allocates outputs and workspaces with torch (device memory),
+and passes raw pointers and the current HIP stream to the C entry point of the
+same name. All arithmetic of the hot path runs in the library's HIP kernels;
+there is no fallback. If the library has not been built, the first call raises.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+MOE_OK, MOE_ERR_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_F32, MOE_BF16 = 0, 1
+
+_LIB = None
+
+
+class MoeError(RuntimeError):
+    def __init__(self, fn, status, msg):
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+        self.status = status
+
+
+def _c_i64():
+    return ctypes.c_int64
+
+
+def load_library(path=None):
+    """Load libmoeflow.so (once). Raises if it does not exist."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    path = path or _build.library_path()
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build the HIP library first "
+            "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    sig = {
+        "moe_abi_version": (I32, []),
+        "moe_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+        "moe_route": (I32, [P, P, I32, I64, I64, I32, I32, P, I32, I32, P, P, P, P]),
+        "moe_schedule_workspace": (SZ, [I64, I32, I32, I32]),
+        "moe_schedule": (I32, [P, I64, I32, I32, I32, I64, I32, I32, P, P, P, P, SZ, P]),
+        "moe_permute_workspace": (SZ, [I64, I32, I32]),
+        "moe_permute": (I32, [P, I32, I64, I64, P, I64, P, I32, I32, P, P, P, P, P, SZ, P]),
+        "moe_expert_ffn_workspace": (SZ, [I64, I64, I64, I32, I32]),
+        "moe_expert_ffn": (I32, [P, I32, I64, I64, I64, P, I32, P, I32, P, P, P, P, P, SZ, P]),
+        "moe_combine": (I32, [P, I32, I64, I64, P, I64, I64, I32, P, P, P, P, I32, P, I32, P,
+                              P, P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _LIB = lib
+    return lib
+
+
+def exported_symbols():
+    return ["moe_abi_version", "moe_status_str", "moe_route", "moe_schedule_workspace",
+            "moe_schedule", "moe_permute_workspace", "moe_permute",
+            "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine"]
+
+
+def _check(name, status):
+    if status != MOE_OK:
+        msg = load_library().moe_status_str(status).decode()
+        raise MoeError(name, status, msg)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return MOE_BF16
+    if t.dtype == torch.float32:
+        return MOE_F32
+    raise TypeError(f"unsupported dtype {t.dtype}: bfloat16 or float32 expected")
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None:
+            if not t.is_cuda:
+                raise ValueError("every tensor must be on the GPU")
+            if not t.is_contiguous():
+                raise ValueError("every tensor must be contiguous")
+
+
+def _workspace(nbytes, device, workspace):
+    torch = _torch()
+    if nbytes == 0:
+        return None, 0
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError(f"workspace too small: {nbytes} bytes needed")
+        return workspace, workspace.numel() * workspace.element_size()
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    ws = ws[off:off + nbytes]
+    return ws, nbytes
+
+
+def workspace_tensor(nbytes, device):
+    """A 256-byte aligned uint8 device buffer of at least nbytes."""
+    return _workspace(nbytes, device, None)[0]
+
+
+# ----------------------------------------------------------------------- route
+def route(x=None, w_gate=None, k=1, bias=None, renormalize=True, logits=None,
+          want_logits=False, topk_idx=None, topk_w=None, stream=None):
+    """moe_route. x-mode: route(x, w_gate, k, ...). logits-in mode:
+    route(k=k, logits=z). Returns (topk_idx int32 [T,k], topk_w f32 [T,k],
+    logits or None)."""
+    torch = _torch()
+    lib = load_library()
+    if x is None and w_gate is None:
+        if logits is None:
+            raise ValueError("logits-in mode needs logits")
+        _dev(logits)
+        T, E = logits.shape
+        dt, H, bias_mode = MOE_F32, 0, 0
+        dev = logits.device
+    else:
+        _dev(x, w_gate, bias)
+        T, H = x.shape
+        E = w_gate.shape[0]
+        if w_gate.shape[1] != H or w_gate.dtype != x.dtype:
+            raise ValueError("w_gate must be [E, H] with the dtype of x")
+        dt = _dtype_code(x)
+        dev = x.device
+        bias_mode = 0
+        if bias is not None:
+            if bias.dtype != torch.float32:
+                raise TypeError("bias must be float32")
+            bias_mode = 1 if bias.dim() == 1 else 2
+        if logits is None and want_logits:
+            logits = torch.empty((T, E), dtype=torch.float32, device=dev)
+    if topk_idx is None:
+        topk_idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    if topk_w is None:
+        topk_w = torch.empty((T, k), dtype=torch.float32, device=dev)
+    st = lib.moe_route(_ptr(x), _ptr(w_gate), dt, T, H, E, k, _ptr(bias), bias_mode,
+                       1 if renormalize else 0, _ptr(logits), _ptr(topk_idx), _ptr(topk_w),
+                       _stream(stream))
+    _check("moe_route", st)
+    return topk_idx, topk_w, logits
+
+
+# -------------------------------------------------------------------- schedule
+def schedule_workspace(N, L, E, k):
+    return load_library().moe_schedule_workspace(N, L, E, k)
+
+
+def schedule(routes, E, n1=None, max_iters=10, keep_original_if_worse=True,
+             perm=None, demand=None, info=None, workspace=None, want_demand=True,
+             stream=None):
+    """moe_schedule over routes uint8 [N, L, k]. Returns (perm int32 [N],
+    demand int32 [2, L, E] or None, info int64 [8])."""
+    torch = _torch()
+    lib = load_library()
+    _dev(routes)
+    if routes.dtype != torch.uint8 or routes.dim() != 3:
+        raise TypeError("routes must be uint8 [N, L, k]")
+    N, L, k = routes.shape
+    n1 = N // 2 if n1 is None else int(n1)
+    dev = routes.device
+    if perm is None:
+        perm = torch.empty(N, dtype=torch.int32, device=dev)
+    if demand is None and want_demand:
+        demand = torch.empty((2, L, E), dtype=torch.int32, device=dev)
+    if info is None:
+        info = torch.empty(8, dtype=torch.int64, device=dev)
+    ws, nbytes = _workspace(lib.moe_schedule_workspace(N, L, E, k), dev, workspace)
+    st = lib.moe_schedule(_ptr(routes), N, L, E, k, n1, max_iters,
+                          1 if keep_original_if_worse else 0, _ptr(perm), _ptr(demand),
+                          _ptr(info), _ptr(ws), nbytes, _stream(stream))
+    _check("moe_schedule", st)
+    return perm, demand, info
+
+
+# --------------------------------------------------------------------- permute
+def permute_workspace(T, k, E):
+    return load_library().moe_permute_workspace(T, k, E)
+
+
+def permute(x, topk_idx, E, token_ids=None, T=None, expert_offsets=None, row_of_pair=None,
+            pair_of_row=None, x_perm=None, workspace=None, stream=None):
+    """moe_permute. x [n_tokens, H] (or None for maps only), topk_idx
+    [n_tokens, k]; the batch is token_ids (or every row). Returns
+    (expert_offsets [E+1], row_of_pair [T*k], pair_of_row [T*k], x_perm)."""
+    torch = _torch()
+    lib = load_library()
+    _dev(x, topk_idx, token_ids)
+    n_tokens, k = topk_idx.shape
+    if T is None:
+        T = token_ids.shape[0] if token_ids is not None else n_tokens
+    dev = topk_idx.device
+    P = T * k
+    if expert_offsets is None:
+        expert_offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    if row_of_pair is None:
+        row_of_pair = torch.empty(P, dtype=torch.int32, device=dev)
+    if pair_of_row is None:
+        pair_of_row = torch.empty(P, dtype=torch.int32, device=dev)
+    dt, H = MOE_F32, 0
+    if x is not None:
+        dt, H = _dtype_code(x), x.shape[1]
+        if x_perm is None:
+            x_perm = torch.empty((P, H), dtype=x.dtype, device=dev)
+    ws, nbytes = _workspace(lib.moe_permute_workspace(T, k, E), dev, workspace)
+    st = lib.moe_permute(_ptr(x), dt, H, x.shape[0] if x is not None else n_tokens,
+                         _ptr(token_ids), T, _ptr(topk_idx), k, E, _ptr(expert_offsets),
+                         _ptr(row_of_pair), _ptr(pair_of_row), _ptr(x_perm), _ptr(ws), nbytes,
+                         _stream(stream))
+    _check("moe_permute", st)
+    return expert_offsets, row_of_pair, pair_of_row, x_perm
+
+
+# ------------------------------------------------------------------ expert ffn
+def expert_ffn_workspace(max_rows, H, F, E, dtype_code=MOE_BF16):
+    return load_library().moe_expert_ffn_workspace(max_rows, H, F, E, dtype_code)
+
+
+def expert_ffn(x_perm, expert_offsets, w_gate, w_up, w_down, slot_of_expert=None,
+               y_perm=None, workspace=None, stream=None):
+    """moe_expert_ffn. x_perm [max_rows, H]; w_gate/w_up [S, F, H]; w_down
+    [S, H, F]; expert_offsets [E+1]. Rows of non-resident experts of y_perm are
+    left as they were. Returns y_perm."""
+    torch = _torch()
+    lib = load_library()
+    _dev(x_perm, expert_offsets, w_gate, w_up, w_down, slot_of_expert)
+    max_rows, H = x_perm.shape
+    S, F, H2 = w_gate.shape
+    if H2 != H or tuple(w_up.shape) != (S, F, H) or tuple(w_down.shape) != (S, H, F):
+        raise ValueError("weights must be w_gate/w_up [S,F,H] and w_down [S,H,F]")
+    if not (w_gate.dtype == w_up.dtype == w_down.dtype == x_perm.dtype):
+        raise TypeError("weights and activations must share one dtype")
+    E = expert_offsets.shape[0] - 1
+    dt = _dtype_code(x_perm)
+    if y_perm is None:
+        y_perm = torch.empty_like(x_perm)
+    ws, nbytes = _workspace(lib.moe_expert_ffn_workspace(max_rows, H, F, E, dt),
+                            x_perm.device, workspace)
+    st = lib.moe_expert_ffn(_ptr(x_perm), dt, max_rows, H, F, _ptr(expert_offsets), E,
+                            _ptr(slot_of_expert), S, _ptr(w_gate), _ptr(w_up), _ptr(w_down),
+                            _ptr(y_perm), _ptr(ws), nbytes, _stream(stream))
+    _check("moe_expert_ffn", st)
+    return y_perm
+
+
+# --------------------------------------------------------------------- combine
+def combine(y_perm, topk_idx, topk_w, row_of_pair, token_ids=None, slot_of_expert=None,
+            y_shared=None, y=None, accumulate=False, want_incomplete=True, incomplete=None,
+            stream=None):
+    """moe_combine. Returns (y [n_tokens, H], incomplete int32 [T] or None)."""
+    torch = _torch()
+    lib = load_library()
+    _dev(y_perm, topk_idx, topk_w, row_of_pair, token_ids, slot_of_expert, y_shared, y)
+    rows, H = y_perm.shape
+    n_tokens, k = topk_idx.shape
+    T = token_ids.shape[0] if token_ids is not None else n_tokens
+    E = slot_of_expert.shape[0] if slot_of_expert is not None else 0
+    dev = y_perm.device
+    if y is None:
+        if accumulate:
+            raise ValueError("accumulate needs an existing y")
+        y = torch.zeros((n_tokens, H), dtype=y_perm.dtype, device=dev)
+    if incomplete is None and want_incomplete:
+        incomplete = torch.empty(T, dtype=torch.int32, device=dev)
+    st = lib.moe_combine(_ptr(y_perm), _dtype_code(y_perm), H, rows, _ptr(token_ids), T,
+                         y.shape[0], k, _ptr(topk_idx), _ptr(topk_w), _ptr(row_of_pair),
+                         _ptr(slot_of_expert), E, _ptr(y_shared), 1 if accumulate else 0,
+                         _ptr(y), _ptr(incomplete), _stream(stream))
+    _check("moe_combine", st)
+    return y, incomplete
+
+
+# ------------------------------------------------------------------ slot table
+def plan_slots(demand, S):
+    """Resident set of one layer from predicted demand (host, the planning step
+    of the expert cache, Sec. 3.4.1): the S experts with the largest demand
+    (equal demand: lower id first) occupy slots 0..S-1 in ascending expert id;
+    slot -1 marks a non-resident expert. demand: int [E]. Returns int32 [E]."""
+    demand = np.asarray(demand).astype(np.int64)
+    E = demand.shape[0]
+    S = max(0, min(int(S), E))
+    # sort key: larger demand first, then lower id
+    keyed = sorted(range(E), key=lambda e: (-int(demand[e]), e))[:S]
+    slot = np.full(E, -1, dtype=np.int32)
+    for s_idx, e in enumerate(sorted(keyed)):
+        slot[e] = s_idx
+    return slot

@@ -1,0 +1,113 @@
+"""CPU checks of the C ABI: the library loads, exports every declared entry
+point, and rejects invalid arguments on the host before touching a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2410_17954_amd import ops
+from paper_2410_17954_amd.build import library_path
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moeflow.h")
+FAKE = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(library_path()):
+        from paper_2410_17954_amd import build
+        build.build(verbose=False)
+    return ops.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(moe_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) == 10, names
+    assert sorted(ops.exported_symbols()) == names
+    for n in names:
+        assert hasattr(lib, n)
+
+
+def test_version_and_status_strings(lib):
+    assert lib.moe_abi_version() == 1
+    for s in range(5):
+        assert lib.moe_status_str(s)
+    assert lib.moe_status_str(99) == b"unknown status"
+
+
+def test_workspace_queries(lib):
+    assert lib.moe_permute_workspace(0, 2, 8) == 0
+    assert lib.moe_permute_workspace(4096, 2, 8) % 256 == 0
+    assert lib.moe_expert_ffn_workspace(8192, 4096, 14336, 8, 1) >= 8192 * 14336 * 2
+    assert lib.moe_schedule_workspace(8192, 32, 8, 2) > 8192 * 4 * 8
+
+
+def test_route_rejects_bad_arguments(lib):
+    S = None
+    # T = 0, k > E, E > 256, missing outputs, bad bias mode, bf16 H % 8 != 0
+    assert lib.moe_route(FAKE, FAKE, 1, 0, 64, 8, 2, S, 0, 1, S, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route(FAKE, FAKE, 1, 4, 64, 2, 3, S, 0, 1, S, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route(FAKE, FAKE, 1, 4, 64, 300, 3, S, 0, 1, S, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route(FAKE, FAKE, 1, 4, 64, 8, 2, S, 0, 1, S, S, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route(FAKE, FAKE, 1, 4, 64, 8, 2, S, 1, 1, S, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route(FAKE, FAKE, 1, 4, 60, 8, 2, S, 0, 1, S, FAKE, FAKE, S) == ops.MOE_ERR_UNSUPPORTED
+    assert lib.moe_route(FAKE, FAKE, 7, 4, 64, 8, 2, S, 0, 1, S, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    # logits-in mode needs logits and no bias
+    assert lib.moe_route(S, S, 1, 4, 0, 8, 2, S, 0, 1, S, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+
+
+def test_schedule_rejects_bad_arguments(lib):
+    S = None
+    ok = (FAKE, 64, 4, 8, 2, 32, 10, 1, FAKE, FAKE, FAKE)
+    bad_n1 = (FAKE, 64, 4, 8, 2, 65, 10, 1, FAKE, FAKE, FAKE)
+    assert lib.moe_schedule(*bad_n1, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_schedule(FAKE, 64, 4, 8, 2, 32, 0, 1, FAKE, FAKE, FAKE, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_schedule(FAKE, 64, 4, 8, 9, 32, 10, 1, FAKE, FAKE, FAKE, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_schedule(*ok, S, 0, S) == ops.MOE_ERR_WORKSPACE
+    assert lib.moe_schedule(*ok, FAKE, 16, S) == ops.MOE_ERR_WORKSPACE
+    assert lib.moe_schedule(*ok, ctypes.c_void_p(0x1001), 1 << 20, S) == ops.MOE_ERR_WORKSPACE
+
+
+def test_permute_rejects_bad_arguments(lib):
+    S = None
+    assert lib.moe_permute(FAKE, 1, 64, 10, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, S, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_permute(FAKE, 1, 60, 10, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, S) == ops.MOE_ERR_UNSUPPORTED
+    assert lib.moe_permute(FAKE, 1, 64, 5, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_permute(FAKE, 1, 64, 10, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, FAKE, FAKE, 8, S) == ops.MOE_ERR_WORKSPACE
+
+
+def test_expert_ffn_rejects_bad_arguments(lib):
+    S = None
+    args = lambda dt, H, F, E, slot, nS, ws, wsb: (FAKE, dt, 128, H, F, FAKE, E, slot, nS, FAKE,
+                                                  FAKE, FAKE, FAKE, ws, wsb, S)
+    big = 1 << 30
+    assert lib.moe_expert_ffn(*args(1, 60, 64, 4, FAKE, 4, FAKE, big)) == ops.MOE_ERR_UNSUPPORTED
+    assert lib.moe_expert_ffn(*args(1, 64, 60, 4, FAKE, 4, FAKE, big)) == ops.MOE_ERR_UNSUPPORTED
+    assert lib.moe_expert_ffn(*args(1, 64, 64, 4, S, 3, FAKE, big)) == ops.MOE_ERR_ARG
+    assert lib.moe_expert_ffn(*args(1, 64, 64, 0, FAKE, 3, FAKE, big)) == ops.MOE_ERR_ARG
+    assert lib.moe_expert_ffn(*args(5, 64, 64, 4, FAKE, 3, FAKE, big)) == ops.MOE_ERR_ARG
+    assert lib.moe_expert_ffn(*args(1, 64, 64, 4, FAKE, 3, FAKE, 100)) == ops.MOE_ERR_WORKSPACE
+
+
+def test_combine_rejects_bad_arguments(lib):
+    S = None
+    assert lib.moe_combine(FAKE, 1, 64, 10, S, 5, 5, 2, FAKE, FAKE, FAKE, S, 0, S, 2, FAKE, S, S) == ops.MOE_ERR_ARG
+    assert lib.moe_combine(FAKE, 1, 60, 10, S, 5, 5, 2, FAKE, FAKE, FAKE, S, 0, S, 0, FAKE, S, S) == ops.MOE_ERR_UNSUPPORTED
+    assert lib.moe_combine(FAKE, 1, 64, 10, S, 5, 5, 2, FAKE, FAKE, FAKE, FAKE, 0, S, 0, FAKE, S, S) == ops.MOE_ERR_ARG
+    assert lib.moe_combine(S, 1, 64, 10, S, 5, 5, 2, FAKE, FAKE, FAKE, S, 0, S, 0, FAKE, S, S) == ops.MOE_ERR_ARG
+
+
+def test_plan_slots_host_rule():
+    import numpy as np
+    slot = ops.plan_slots(np.array([5, 0, 9, 5, 1]), 3)
+    assert slot.tolist() == [0, -1, 1, 2, -1]
+    assert ops.plan_slots(np.array([1, 2]), 0).tolist() == [-1, -1]
+    assert ops.plan_slots(np.array([1, 2]), 5).tolist() == [0, 1]

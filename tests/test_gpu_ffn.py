@@ -1,0 +1,116 @@
+"""GPU parity of moe_expert_ffn against the oracle's SwiGLU experts."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2410_17954_amd import ops, synth
+from gpu_helpers import to_dev, to_host, vals, rel_max_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _weights(S, F, H, seed, dtype="bf16", std=0.02):
+    g = np.random.default_rng(seed)
+    ws = [g.standard_normal(s).astype(np.float32) * np.float32(std)
+          for s in ((S, F, H), (S, F, H), (S, H, F))]
+    return [synth.bf16_bits(w) for w in ws] if dtype == "bf16" else ws
+
+
+def _rows(R, H, seed, dtype="bf16"):
+    x = np.random.default_rng(seed + 1).standard_normal((R, H)).astype(np.float32)
+    return synth.bf16_bits(x) if dtype == "bf16" else x
+
+
+def _run(counts, H, F, slot, S, seed, dtype="bf16", tol=1e-2, extra_rows=0):
+    counts = np.asarray(counts)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    R = int(offsets[-1]) + extra_rows
+    x = _rows(max(R, 1), H, seed, dtype)
+    wg, wu, wd = _weights(S, F, H, seed, dtype)
+    sentinel = 3.0
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    y = torch.full((max(R, 1), H), sentinel, dtype=tdt, device="cuda:0")
+    ops.expert_ffn(to_dev(x), to_dev(offsets), to_dev(wg), to_dev(wu), to_dev(wd),
+                   slot_of_expert=None if slot is None else to_dev(np.asarray(slot, np.int32)),
+                   y_perm=y)
+    torch.cuda.synchronize()
+    got = vals(y)
+    sl = np.arange(len(counts)) if slot is None else np.asarray(slot)
+    ref, computed = oracle.expert_ffn(synth.values(x)[:offsets[-1]], offsets, sl,
+                                      synth.values(wg), synth.values(wu), synth.values(wd))
+    if computed.any():
+        assert rel_max_err(got[:offsets[-1]][computed], ref[computed]) <= tol
+    assert (got[:offsets[-1]][~computed] == sentinel).all()
+    assert (got[offsets[-1]:] == sentinel).all()
+    return got, ref, computed
+
+
+def test_tiny_fp32_config():
+    cfg = synth.config(1)
+    counts = np.bincount(synth.random_topk_idx(64, 8, 2, 1).ravel(), minlength=8)
+    _run(counts, cfg["H"], cfg["F"], None, 8, seed=1, dtype="f32", tol=1e-4)
+
+
+@pytest.mark.parametrize("counts,H,F", [
+    ([0, 300, 17, 513], 256, 512),        # ragged, several row tiles, an empty expert
+    ([1], 64, 64),                         # one row
+    ([256, 256], 128, 192),                # exact tiles, F not a multiple of 64
+    ([700, 3, 0, 1029, 64], 512, 1408),    # Qwen-like F
+])
+def test_bf16_ragged_groups(counts, H, F):
+    _run(counts, H, F, None, len(counts), seed=sum(counts) + H)
+
+
+def test_bf16_resident_subset_and_slot_order():
+    counts = [100, 200, 50, 300, 10, 0]
+    slot = [2, -1, 0, -1, 1, 3]
+    _run(counts, 256, 384, slot, 4, seed=21, extra_rows=33)
+
+
+def test_bf16_nothing_resident():
+    _run([10, 20], 64, 64, [-1, -1], 2, seed=22)
+
+
+def test_shared_experts_as_one_dense_group():
+    # two shared experts of width F concatenated along F == one expert of width 2F
+    T, H, F = 333, 256, 256
+    g = np.random.default_rng(5)
+    x = synth.bf16_bits(g.standard_normal((T, H)).astype(np.float32))
+    wg, wu, wd = _weights(1, 2 * F, H, seed=5)
+    y = ops.expert_ffn(to_dev(x), to_dev(np.array([0, T], np.int32)), to_dev(wg), to_dev(wu),
+                       to_dev(wd))
+    xs, G, Uw, D = synth.values(x), synth.values(wg)[0], synth.values(wu)[0], synth.values(wd)[0]
+    ref = sum(oracle.swiglu(xs, G[s * F:(s + 1) * F], Uw[s * F:(s + 1) * F], D[:, s * F:(s + 1) * F])
+              for s in range(2))
+    assert rel_max_err(vals(y), ref) <= 1e-2
+
+
+@pytest.mark.parametrize("cfg_id", [2, 4])
+def test_full_shape_sampled_rows(cfg_id):
+    """Full expert shapes; the oracle evaluates the first and last row of every
+    expert and a seeded sample of rows one by one."""
+    cfg = synth.config(cfg_id)
+    E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
+    T = 4096 if cfg_id == 2 else 8192
+    idx = synth.random_topk_idx(T, E, k, seed=cfg_id, skew=None if cfg_id == 2 else 1.2)
+    counts = np.bincount(idx.ravel(), minlength=E)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    R = int(offsets[-1])
+    inp = synth.layer_inputs(cfg, cfg_id, T=R, parts=("x", "experts"))
+    x = inp["x"]
+    y = ops.expert_ffn(to_dev(x), to_dev(offsets), to_dev(inp["w_gate"]), to_dev(inp["w_up"]),
+                       to_dev(inp["w_down"]))
+    got = vals(y)
+    g = np.random.default_rng(cfg_id)
+    sample = set(g.choice(R, size=24, replace=False).tolist())
+    for e in range(E):
+        if counts[e]:
+            sample |= {int(offsets[e]), int(offsets[e + 1]) - 1}
+    sample = np.array(sorted(sample))
+    ref = np.empty((len(sample), H))
+    for a, r in enumerate(sample):
+        e = int(np.searchsorted(offsets, r, side="right") - 1)
+        ref[a] = oracle.swiglu(synth.values(x[r:r + 1]), synth.values(inp["w_gate"][e]),
+                               synth.values(inp["w_up"][e]), synth.values(inp["w_down"][e]))[0]
+    assert rel_max_err(got[sample], ref) <= 1e-2

@@ -1,0 +1,86 @@
+"""GPU parity of moe_schedule against the oracle's token scheduler
+(Sec. 3.3): perm, demand and info bit-exact."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_17954_amd import ops, synth
+from gpu_helpers import to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _check(routes, E, n1=None, max_iters=10, keep=True):
+    routes = np.ascontiguousarray(routes, dtype=np.uint8)
+    perm, demand, info = ops.schedule(to_dev(routes), E, n1=n1, max_iters=max_iters,
+                                      keep_original_if_worse=keep)
+    rp, rd, ri = oracle.schedule(routes, E, n1, max_iters, keep)
+    assert to_host(info).tolist() == ri.tolist()
+    assert np.array_equal(to_host(perm), rp)
+    assert np.array_equal(to_host(demand), rd)
+    return ri
+
+
+def test_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "ts_worked_example.json")))
+    info = _check(np.array(g["routes"]), g["E"], g["n1"])
+    assert info[5] == g["obj_optimum"]
+
+
+@pytest.mark.parametrize("N,L,E,k,s", [(64, 4, 8, 2, 1.1), (1000, 8, 16, 2, 1.0),
+                                       (777, 3, 64, 6, 1.0), (4097, 2, 256, 4, 0.5)])
+def test_markov_routes(N, L, E, k, s):
+    routes = synth.predicted_routes(N, L, E, k, 0.7, s, seed=N + L)
+    _check(routes, E)
+
+
+def test_route_grouped_mixtral_unit():
+    cfg = synth.config(3)
+    routes = synth.predicted_routes(cfg["T"], cfg["L"], cfg["E"], cfg["k"], cfg["keep"],
+                                    cfg["zipf"], seed=3)
+    info = _check(routes, cfg["E"])
+    assert info[5] <= info[4]
+
+
+def test_deepseek_unit_26_layers():
+    cfg = synth.config(5)
+    routes = synth.predicted_routes(cfg["T"], cfg["L"], cfg["E"], cfg["k"], cfg["keep"],
+                                    cfg["zipf"], seed=5)
+    _check(routes, cfg["E"])
+
+
+@pytest.mark.parametrize("n1", [0, 1, 5, 13])
+def test_uneven_and_degenerate_splits(n1):
+    routes = synth.predicted_routes(13, 3, 5, 2, 0.5, 0.8, seed=2)
+    _check(routes, 5, n1=n1)
+
+
+def test_single_token():
+    _check(np.array([[[3, 1]]]), 4, n1=1)
+
+
+def test_identical_routes():
+    _check(np.tile(np.array([[2, 5], [1, 3], [0, 7]]), (300, 1, 1)), 8)
+
+
+def test_planted_clusters():
+    a = np.array([[0, 1]] * 6)
+    b = np.array([[4, 5]] * 6)
+    routes = np.stack([a] * 50 + [b] * 50)[np.random.default_rng(8).permutation(100)]
+    info = _check(routes, 8)
+    assert info[5] == 2 * 6 * 2
+
+
+def test_iteration_limit_and_no_guard():
+    routes = synth.predicted_routes(2000, 6, 8, 2, 0.5, 0.8, seed=9)
+    _check(routes, 8, max_iters=1, keep=False)
+    _check(routes, 8, max_iters=2, keep=False)
+
+
+def test_k_equals_E():
+    routes = np.tile(np.arange(4, dtype=np.uint8), (50, 2, 1))
+    _check(routes, 4)
