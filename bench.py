@@ -1,0 +1,253 @@
+"""Throughput of the MoE-layer hot path on one MI355X.
+
+One step = one pass of the whole path over one scheduling unit of the
+Mixtral-8x7B-shaped layer (H 4096, 8 experts of SwiGLU width 14336, top-2):
+two adjacent batches of T = 4096 tokens (8192 tokens) with 32-layer predicted
+routes are rebatched by the token scheduler (moe_schedule), gated in one
+launch (moe_route), and each new batch is grouped by expert (moe_permute), run
+through its resident experts (moe_expert_ffn; all 8 resident) and combined
+(moe_combine). Inputs are seeded synthetic data already resident in HBM; no
+allocation happens inside the timed region.
+
+Prints one JSON line (see the keys below). --gpus N > 1 is refused: this path
+runs on one GPU.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/sec + grouped-FFN MFMA % of peak (bf16, Mixtral-shape)"
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--seed", type=int, default=2)
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="CPU budget of the oracle baseline sample (0 = skip)")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this hot path runs on exactly one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2410_17954_amd import ops, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.config(2)
+    T, H, E, F, k, L = cfg["T"], cfg["H"], cfg["E"], cfg["F"], cfg["k"], cfg["L"]
+    N = 2 * T                        # one scheduling unit = two adjacent batches
+    n1 = N // 2
+
+    t_gen = time.time()
+    inp = synth.layer_inputs(cfg, args.seed, T=N, parts=("x", "router", "experts"))
+    routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], args.seed)
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    x = up(inp["x"])
+    wr = up(inp["w_router"])
+    wg, wu, wd = up(inp["w_gate"]), up(inp["w_up"]), up(inp["w_down"])
+    routes_d = up(routes)
+    gen_s = time.time() - t_gen
+
+    # Outputs and workspaces, allocated once.
+    perm = torch.empty(N, dtype=torch.int32, device=dev)
+    demand = torch.empty((2, L, E), dtype=torch.int32, device=dev)
+    info = torch.empty(8, dtype=torch.int64, device=dev)
+    ws_sched = ops.workspace_tensor(ops.schedule_workspace(N, L, E, k), dev)
+    idx = torch.empty((N, k), dtype=torch.int32, device=dev)
+    gw = torch.empty((N, k), dtype=torch.float32, device=dev)
+    R = T * k
+    offs = [torch.empty(E + 1, dtype=torch.int32, device=dev) for _ in range(2)]
+    rops = [torch.empty(R, dtype=torch.int32, device=dev) for _ in range(2)]
+    pors = [torch.empty(R, dtype=torch.int32, device=dev) for _ in range(2)]
+    xps = [torch.empty((R, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    yps = [torch.empty((R, H), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    incs = [torch.empty(T, dtype=torch.int32, device=dev) for _ in range(2)]
+    ws_perm = ops.workspace_tensor(ops.permute_workspace(T, k, E), dev)
+    ws_ffn = ops.workspace_tensor(ops.expert_ffn_workspace(R, H, F, E), dev)
+    y = torch.zeros((N, H), dtype=torch.bfloat16, device=dev)
+    # Resident set (expert-cache planning from predicted demand): with as many
+    # slots as experts every expert is resident, whatever the demand.
+    S = cfg["S"]
+    assert S >= E
+    slot = torch.arange(E, dtype=torch.int32, device=dev)
+    batches = [perm[:n1], perm[n1:]]
+
+    stage_names = ["schedule", "route", "permute", "expert_ffn", "combine"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        ops.schedule(routes_d, E, n1=n1, perm=perm, demand=demand, info=info,
+                     workspace=ws_sched)
+        mark(1)
+        ops.route(x, wr, k, topk_idx=idx, topk_w=gw)
+        mark(2)
+        j = 3
+        for b in range(2):
+            tok = batches[b]
+            ops.permute(x, idx, E, token_ids=tok, expert_offsets=offs[b], row_of_pair=rops[b],
+                        pair_of_row=pors[b], x_perm=xps[b], workspace=ws_perm)
+            mark(j)
+            ops.expert_ffn(xps[b], offs[b], wg, wu, wd, slot_of_expert=slot, y_perm=yps[b],
+                           workspace=ws_ffn)
+            mark(j + 1)
+            ops.combine(yps[b], idx, gw, rops[b], token_ids=tok, slot_of_expert=slot, y=y,
+                        incomplete=incs[b])
+            mark(j + 2)
+            j += 3
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(K):
+        step(events[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / K
+
+    def span(ev, a, b):
+        return ev[a].elapsed_time(ev[b])
+
+    st = {n: 0.0 for n in stage_names}
+    ffn_launch_ms = []
+    for ev in events:
+        st["schedule"] += span(ev, 0, 1)
+        st["route"] += span(ev, 1, 2)
+        prev = 2
+        for b in range(2):
+            base = 3 + 3 * b
+            st["permute"] += span(ev, prev, base)
+            d = span(ev, base, base + 1)
+            st["expert_ffn"] += d
+            ffn_launch_ms.append(d)
+            st["combine"] += span(ev, base + 1, base + 2)
+            prev = base + 2
+    st = {n: v / K for n, v in st.items()}
+
+    info_h = info.cpu().numpy()
+    inc_h = torch.cat(incs).cpu().numpy()
+    assert inc_h.sum() == 0 and torch.isfinite(y.float()).all().item()
+
+    # Algorithmic work.
+    ffn_flops = 6.0 * H * F * R                     # per moe_expert_ffn launch
+    ffn_ms = float(np.mean(ffn_launch_ms))
+    achieved = ffn_flops / (ffn_ms * 1e-3) / 1e12
+    bytes_route = N * H * 2 + E * H * 2 + N * k * 8
+    bytes_perm = 2 * (T * H * 2 + R * H * 2 + T * k * 4 + R * 8)
+    bytes_comb = 2 * (R * H * 2 + T * H * 2 + T * k * 12)
+    stages = {
+        "schedule": {"ms": st["schedule"], "obj_before": int(info_h[4]),
+                     "obj_after": int(info_h[5]), "iters": int(info_h[0])},
+        "route": {"ms": st["route"], "GB/s": bytes_route / st["route"] / 1e6,
+                  "hbm_frac": bytes_route / st["route"] / 1e6 / PEAK_HBM_GBS},
+        "permute": {"ms": st["permute"], "GB/s": bytes_perm / st["permute"] / 1e6,
+                    "hbm_frac": bytes_perm / st["permute"] / 1e6 / PEAK_HBM_GBS},
+        "expert_ffn": {"ms": st["expert_ffn"], "TFLOP/s": achieved,
+                       "mfma_frac": achieved / PEAK_BF16_TFLOPS},
+        "combine": {"ms": st["combine"], "GB/s": bytes_comb / st["combine"] / 1e6,
+                    "hbm_frac": bytes_comb / st["combine"] / 1e6 / PEAK_HBM_GBS},
+    }
+
+    out = {
+        "metric": METRIC,
+        "value": N / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations, N(0,0.02) weights, Markov predicted routes)",
+        "config": {
+            "workload": ("Mixtral-8x7B-shaped MoE layer, one scheduling unit of two adjacent "
+                         "T=4096 batches (8192 tokens), H=4096, E=8, F=14336, top-2 renormalised, "
+                         "all 8 experts resident, 32-layer predicted routes (keep 0.7, Zipf 1.1)"),
+            "tokens_per_step": N, "T": T, "H": H, "E": E, "F": F, "k": k, "L": L,
+            "resident": S, "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "mfma", "kernel": "moe_expert_ffn (grouped SwiGLU: up+gate GEMM, down GEMM)",
+            "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+            "flop_per_launch": ffn_flops, "launch_ms": ffn_ms,
+        },
+        "stages": stages,
+        "setup_s": gen_s,
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(inp, routes, cfg, args.cpu_seconds)
+    print(json.dumps(out))
+
+
+def cpu_baseline(inp, routes, cfg, budget_s):
+    """The CPU oracle, unmodified, on a bounded sample of the same workload:
+    the scheduler over the whole 8192-token unit, then the MoE layer on
+    128-token chunks of the first new batch until the budget is spent. The
+    rate is per token: 1 / (schedule time / N + layer time / sampled tokens)."""
+    import oracle
+    from paper_2410_17954_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max(int(i.get("num_threads", 1)) for i in threadpool_info()) \
+            if threadpool_info() else 1
+    except Exception:
+        blas_threads = 1
+    E, k = cfg["E"], cfg["k"]
+    N = routes.shape[0]
+    x = synth.values(inp["x"])
+    wr = synth.values(inp["w_router"])
+    wg, wu, wd = (synth.values(inp[n]) for n in ("w_gate", "w_up", "w_down"))
+    t0 = time.perf_counter()
+    perm, demand, info = oracle.schedule(routes, E)
+    t_sched = time.perf_counter() - t0
+    chunk = 128
+    done = 0
+    t_layer = 0.0
+    while done < N and (t_layer + t_sched) < budget_s:
+        tok = perm[done:done + chunk]
+        t1 = time.perf_counter()
+        oracle.moe_layer(x[tok], wr, k, wg, wu, wd)
+        t_layer += time.perf_counter() - t1
+        done += len(tok)
+    per_token = t_sched / N + t_layer / max(done, 1)
+    return {"value": 1.0 / per_token, "unit": "tokens/s", "cores": blas_threads,
+            "kind": "oracle",
+            "sample": (f"scheduler over all {N} tokens ({t_sched:.2f} s) + MoE layer on "
+                       f"{done} tokens in {chunk}-token chunks ({t_layer:.2f} s), float64"),
+            "affinity_cores": len(os.sched_getaffinity(0))}
+
+
+if __name__ == "__main__":
+    main()

@@ -9,7 +9,9 @@ SeedSequence(seed), one child per named tensor, so each tensor is independent
 of the sizes of the others):
   * hidden states x ~ N(0, 1); router and expert weights ~ N(0, 0.02);
     drawn in float32, then rounded to bfloat16 (round to nearest even) for the
-    bf16 workloads. bf16 tensors are returned as uint16 bit patterns.
+    bf16 workloads. bf16 tensors are returned as uint16 bit patterns. Large
+    tensors are drawn in blocks along their first axis (1024 rows of x, one
+    expert of a weight stack), block b from the stream (seed, tensor, b).
   * Zipf-skewed router bias (Qwen- and DeepSeek-shaped layers): expert e gets
     b_e = ln(rho_e^-s / sum_e' rho_e'^-s), rho = 1 + a seeded permutation of
     0..E-1, so the softmax odds of expert e are scaled by its Zipf mass.
@@ -23,6 +25,9 @@ of the sizes of the others):
 These stand in for the paper's models (Table 1) and datasets, which are not
 available; the shapes follow Table 1's Mixtral, Qwen1.5-MoE and DeepSeek rows.
 """
+import concurrent.futures
+import os
+
 import numpy as np
 
 # Workload shapes. T = tokens in one layer call, H hidden, E routed experts,
@@ -56,18 +61,28 @@ def config(n):
     return dict(CONFIGS[n], id=n)
 
 
-def rng_for(seed, name):
-    ss = np.random.SeedSequence(int(seed))
-    child = ss.spawn(len(_STREAM))[_STREAM[name]]
-    return np.random.Generator(np.random.PCG64(child))
+def rng_for(seed, name, block=None):
+    """Generator of the named tensor (and of one block of it along axis 0)."""
+    key = [int(seed), _STREAM[name]] + ([] if block is None else [int(block)])
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(key)))
 
 
 def bf16_bits(a):
-    """float32 array -> uint16 bfloat16 bit patterns, round to nearest even."""
+    """float32 array -> uint16 bfloat16 bit patterns, round to nearest even
+    (finite inputs)."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return rounded.astype(np.uint16)
+    out = np.empty(a.shape, dtype=np.uint16)
+    flat_in = a.reshape(-1).view(np.uint32)
+    flat_out = out.reshape(-1)
+    step = 1 << 22
+    for lo in range(0, flat_in.size, step):
+        u = flat_in[lo:lo + step]
+        r = (u >> 16) & 1
+        r += 0x7FFF
+        r += u
+        r >>= 16
+        flat_out[lo:lo + step] = r
+    return out
 
 
 def bf16_to_f32(bits):
@@ -82,12 +97,32 @@ def values(arr):
     return np.asarray(arr, dtype=np.float64)
 
 
-def _normal(seed, name, shape, std, dtype):
-    g = rng_for(seed, name)
-    a = g.standard_normal(size=shape, dtype=np.float32)
-    if std != 1.0:
-        a *= np.float32(std)
-    return bf16_bits(a) if dtype == "bf16" else a
+_POOL_THREADS = min(16, os.cpu_count() or 1)
+
+
+def _normal(seed, name, shape, std, dtype, rows_per_block=1):
+    """N(0, std^2) draws of `shape`, in blocks of `rows_per_block` along axis 0,
+    block b drawn from its own stream (seed, name, b); threads only change
+    the speed, never the values."""
+    n0 = shape[0]
+    inner = shape[1:]
+    out = np.empty(shape, dtype=np.uint16 if dtype == "bf16" else np.float32)
+    blocks = list(range(0, n0, rows_per_block))
+
+    def fill(lo):
+        g = rng_for(seed, name, lo // rows_per_block)
+        hi = min(n0, lo + rows_per_block)
+        a = g.standard_normal(size=(hi - lo,) + tuple(inner), dtype=np.float32)
+        if std != 1.0:
+            a *= np.float32(std)
+        out[lo:hi] = bf16_bits(a) if dtype == "bf16" else a
+
+    if len(blocks) == 1:
+        fill(0)
+    else:
+        with concurrent.futures.ThreadPoolExecutor(_POOL_THREADS) as ex:
+            list(ex.map(fill, blocks))
+    return out
 
 
 def layer_inputs(cfg, seed, T=None, parts=("x", "router", "experts", "shared", "bias")):
@@ -98,18 +133,18 @@ def layer_inputs(cfg, seed, T=None, parts=("x", "router", "experts", "shared", "
     H, E, F, dt = cfg["H"], cfg["E"], cfg["F"], cfg["dtype"]
     out = {}
     if "x" in parts:
-        out["x"] = _normal(seed, "x", (T, H), 1.0, dt)
+        out["x"] = _normal(seed, "x", (T, H), 1.0, dt, rows_per_block=1024)
     if "router" in parts:
-        out["w_router"] = _normal(seed, "router", (E, H), 0.02, dt)
+        out["w_router"] = _normal(seed, "router", (E, H), 0.02, dt, rows_per_block=E)
     if "experts" in parts:
         out["w_gate"] = _normal(seed, "w_gate", (E, F, H), 0.02, dt)
         out["w_up"] = _normal(seed, "w_up", (E, F, H), 0.02, dt)
         out["w_down"] = _normal(seed, "w_down", (E, H, F), 0.02, dt)
     if "shared" in parts and cfg.get("n_shared", 0) > 0:
         Fs = cfg["n_shared"] * F
-        out["shared_gate"] = _normal(seed, "shared_gate", (Fs, H), 0.02, dt)
-        out["shared_up"] = _normal(seed, "shared_up", (Fs, H), 0.02, dt)
-        out["shared_down"] = _normal(seed, "shared_down", (H, Fs), 0.02, dt)
+        out["shared_gate"] = _normal(seed, "shared_gate", (Fs, H), 0.02, dt, rows_per_block=F)
+        out["shared_up"] = _normal(seed, "shared_up", (Fs, H), 0.02, dt, rows_per_block=F)
+        out["shared_down"] = _normal(seed, "shared_down", (H, Fs), 0.02, dt, rows_per_block=H)
     if "bias" in parts and cfg.get("zipf_bias") is not None:
         out["bias"] = zipf_bias(E, cfg["zipf_bias"], popularity_order(seed, E, 1)[0])
     return out

@@ -51,15 +51,15 @@ def _x_mode_case(cfg_id, T, seed, bias_kind=None, renorm=True):
     bound = logit_bound(x, wr, z_ref, bias)
     assert (np.abs(z - z_ref) <= bound).all(), np.max(np.abs(z - z_ref) / bound)
     near = check_topk_against_bound(idx, z_ref, bound, k)
-    ok = (idx == oracle.topk_select(z_ref, k)).all(axis=1)
+    # decisions are taken on float64 logits on both sides: exact on every token
+    assert np.array_equal(idx, oracle.topk_select(z_ref, k))
     ref_w = oracle.gate_weights(z_ref, idx, renorm)
     assert np.max(np.abs(w - ref_w)) <= bound.max() + 1e-6
-    return near, ok.mean()
+    return near
 
 
 def test_x_mode_tiny_fp32():
-    near, agree = _x_mode_case(1, 64, 1)
-    assert agree == 1.0
+    _x_mode_case(1, 64, 1)
 
 
 @pytest.mark.parametrize("T", [1, 17, 300])
@@ -68,8 +68,10 @@ def test_x_mode_ragged_token_counts(T):
 
 
 def test_x_mode_mixtral_full_size():
-    near, agree = _x_mode_case(2, 4096, 2)
-    assert near <= 4
+    near = _x_mode_case(2, 8192, 2)
+    # a sizeable share of tokens is not decided by the float32 error bound
+    # alone; those go through the float64 refinement
+    assert near > 0
 
 
 def test_x_mode_qwen_expert_bias():
@@ -89,3 +91,22 @@ def test_x_mode_wide_expert_count():
     bound = logit_bound(x, wr, z_ref)
     assert (np.abs(to_host(z) - z_ref) <= bound).all()
     check_topk_against_bound(to_host(idx), z_ref, bound, 8)
+
+
+def test_x_mode_crafted_exact_and_near_ties():
+    """Router rows that tie exactly, or differ by one bf16 ulp in one
+    element, so float32 cannot separate them: the decision must still match
+    the float64 oracle, exact ties going to the lower expert id."""
+    g = np.random.default_rng(17)
+    H, E, T, k = 512, 8, 64, 3
+    w = synth.bf16_bits((g.standard_normal((E, H)) * 0.02).astype(np.float32))
+    w[3] = w[1]                               # exact tie
+    w[5] = w[1]
+    w[5, 7] ^= 1                              # one ulp apart in one element
+    w[6] = w[2]
+    w[6, 100] += 1
+    x = synth.bf16_bits(g.standard_normal((T, H)).astype(np.float32))
+    x[:, 7] = synth.bf16_bits(np.full(T, 3.0, np.float32))
+    idx, _, _ = ops.route(to_dev(x), to_dev(w), k)
+    z_ref = oracle.router_logits(synth.values(x), synth.values(w))
+    assert np.array_equal(to_host(idx), oracle.topk_select(z_ref, k))
