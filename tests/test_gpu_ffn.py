@@ -57,6 +57,8 @@ def test_tiny_fp32_config():
     ([1], 64, 64),                         # one row
     ([256, 256], 128, 192),                # exact tiles, F not a multiple of 64
     ([700, 3, 0, 1029, 64], 512, 1408),    # Qwen-like F
+    ([300, 5, 260], 136, 200),             # H, F not multiples of 32: general path
+    ([40, 300], 264, 96),                  # general path, K tail inside a 64-deep step
 ])
 def test_bf16_ragged_groups(counts, H, F):
     _run(counts, H, F, None, len(counts), seed=sum(counts) + H)

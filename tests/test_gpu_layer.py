@@ -1,0 +1,188 @@
+"""End-to-end GPU parity of the MoE-layer hot path (gating, scheduling,
+resident-set planning, grouping, experts, combine) against the oracle, at
+the workload shapes. Full-size cases check every integer output exactly and
+the layer output on a seeded sample of tokens, which the oracle evaluates as
+its own batch (tokens are independent through the layer)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2410_17954_amd import ops, synth
+from gpu_helpers import to_dev, to_host, vals, rel_max_err, DEV
+
+pytestmark = pytest.mark.gpu
+
+
+class SlotView:
+    """Expert weights seen through a slot table, converted to float64 on
+    access (plumbing for the oracle; no arithmetic)."""
+
+    def __init__(self, arr, experts):
+        self.arr, self.experts = arr, list(experts)
+
+    def __getitem__(self, s):
+        return synth.values(self.arr[self.experts[s]])
+
+
+def _gpu_weights(inp, names=("w_gate", "w_up", "w_down")):
+    return {n: to_dev(inp[n]) for n in names}
+
+
+def _layer_batch(x_d, idx_d, w_d, W, E, tok_d, slot_np, y_d, shared=None):
+    """One batch through permute -> resident experts -> combine on the GPU."""
+    res = [e for e in range(E) if slot_np[e] >= 0]
+    sel = torch.tensor(res, dtype=torch.long, device=DEV)
+    wg, wu, wd = (W[n].index_select(0, sel).contiguous() for n in ("w_gate", "w_up", "w_down"))
+    slot_d = to_dev(slot_np.astype(np.int32))
+    off, rop, por, xp = ops.permute(x_d, idx_d, E, token_ids=tok_d)
+    yp = ops.expert_ffn(xp, off, wg, wu, wd, slot_of_expert=slot_d)
+    ys = None
+    if shared is not None:
+        o1, r1, _, xs = ops.permute(x_d, torch.zeros((x_d.shape[0], 1), dtype=torch.int32,
+                                                      device=DEV), 1, token_ids=tok_d)
+        ys = ops.expert_ffn(xs, o1, *shared)
+    _, inc = ops.combine(yp, idx_d, w_d, rop, token_ids=tok_d, slot_of_expert=slot_d,
+                         y_shared=ys, y=y_d)
+    return off, inc
+
+
+def _oracle_sample(inp, cfg, sample, slot_np, bias=None, renorm=True):
+    E = cfg["E"]
+    res = [e for e in range(E) if slot_np[e] >= 0]
+    shared = None
+    if cfg.get("n_shared", 0):
+        shared = tuple(synth.values(inp[n]) for n in ("shared_gate", "shared_up", "shared_down"))
+    b = None if bias is None else (bias if np.ndim(bias) == 1 else bias[sample])
+    return oracle.moe_layer(synth.values(inp["x"][sample]), synth.values(inp["w_router"]),
+                            cfg["k"], SlotView(inp["w_gate"], res), SlotView(inp["w_up"], res),
+                            SlotView(inp["w_down"], res), bias=b, renormalize=renorm,
+                            slot_of_expert=slot_np, shared=shared)
+
+
+def test_tiny_fp32_layer_full():
+    cfg = synth.config(1)
+    inp = synth.layer_inputs(cfg, 1)
+    E, k = cfg["E"], cfg["k"]
+    x_d = to_dev(inp["x"])
+    W = _gpu_weights(inp)
+    idx, w, _ = ops.route(x_d, to_dev(inp["w_router"]), k)
+    y = torch.zeros_like(x_d)
+    _layer_batch(x_d, idx, w, W, E, None, np.arange(E), y)
+    ref = oracle.moe_layer(synth.values(inp["x"]), synth.values(inp["w_router"]), k,
+                           inp["w_gate"], inp["w_up"], inp["w_down"])
+    assert np.array_equal(to_host(idx), ref["idx"])
+    assert rel_max_err(to_host(y), ref["y"]) <= 1e-4
+
+
+def test_mixtral_layer_full_size_sampled():
+    cfg = synth.config(2)
+    T, E, k = cfg["T"], cfg["E"], cfg["k"]
+    inp = synth.layer_inputs(cfg, 2)
+    x_d = to_dev(inp["x"])
+    W = _gpu_weights(inp)
+    idx, w, _ = ops.route(x_d, to_dev(inp["w_router"]), k)
+    y = torch.zeros_like(x_d)
+    off, inc = _layer_batch(x_d, idx, w, W, E, None, np.arange(E), y)
+    z = oracle.router_logits(synth.values(inp["x"]), synth.values(inp["w_router"]))
+    ridx = oracle.topk_select(z, k)
+    assert np.array_equal(to_host(idx), ridx)
+    assert np.array_equal(to_host(off), np.concatenate([[0], np.cumsum(np.bincount(ridx.ravel(), minlength=E))]))
+    assert to_host(inc).sum() == 0
+    sample = np.sort(np.random.default_rng(2).choice(T, 48, replace=False))
+    ref = _oracle_sample(inp, cfg, sample, np.arange(E))
+    assert rel_max_err(vals(y)[sample], ref["y"]) <= 1e-2
+
+
+def _scheduled_unit(cfg_id, n_sample=48):
+    """Route-grouped workload: schedule N tokens by predicted route, plan each
+    batch's resident set from the predicted demand of layer 0, run layer 0
+    batch by batch with misses flagged."""
+    cfg = synth.config(cfg_id)
+    N, E, k, L, S = cfg["T"], cfg["E"], cfg["k"], cfg["L"], cfg["S"]
+    inp = synth.layer_inputs(cfg, cfg_id, T=N)
+    routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], cfg_id)
+    bias = synth.route_boost_bias(routes, 0, E, cfg["boost"], inp.get("bias"))
+    perm, demand, info = ops.schedule(to_dev(routes), E)
+    r_perm, r_demand, r_info = oracle.schedule(routes, E)
+    assert to_host(info).tolist() == r_info.tolist()
+    assert np.array_equal(to_host(perm), r_perm)
+    assert np.array_equal(to_host(demand), r_demand)
+    x_d = to_dev(inp["x"])
+    W = _gpu_weights(inp)
+    shared = None
+    if cfg["n_shared"]:
+        shared = tuple(to_dev(inp[n][None]) for n in ("shared_gate", "shared_up", "shared_down"))
+    idx, w, _ = ops.route(x_d, to_dev(inp["w_router"]), k, bias=to_dev(bias))
+    z = oracle.router_logits(synth.values(inp["x"]), synth.values(inp["w_router"]), bias)
+    assert np.array_equal(to_host(idx), oracle.topk_select(z, k))
+    y = torch.zeros_like(x_d)
+    n1 = int(r_info[7])
+    g = np.random.default_rng(cfg_id)
+    d_host = to_host(demand)
+    for b, tok in enumerate((r_perm[:n1], r_perm[n1:])):
+        slot = ops.plan_slots(d_host[b, 0], S)
+        assert np.array_equal(slot, oracle.plan_slots(r_demand[b, 0], S))
+        tok_d = perm[:n1] if b == 0 else perm[n1:]
+        _, inc = _layer_batch(x_d, idx, w, W, E, tok_d, slot, y, shared)
+        r_idx = oracle.topk_select(z[tok], k)
+        assert np.array_equal(to_host(inc), (slot[r_idx] < 0).any(axis=1).astype(np.int32))
+        sample = np.sort(g.choice(tok, n_sample, replace=False))
+        ref = _oracle_sample(inp, cfg, sample, slot, bias=bias)
+        assert rel_max_err(vals(y)[sample], ref["y"]) <= 1e-2
+    return r_info
+
+
+def test_route_grouped_mixtral_unit_with_misses():
+    _scheduled_unit(3)
+
+
+def test_deepseek_unit_scheduled_shared_experts():
+    _scheduled_unit(5)
+
+
+def test_qwen_layer_zipf_bias_shared_experts():
+    cfg = synth.config(4)
+    T, E, k, S = cfg["T"], cfg["E"], cfg["k"], cfg["S"]
+    inp = synth.layer_inputs(cfg, 4)
+    x_d = to_dev(inp["x"])
+    W = _gpu_weights(inp)
+    shared = tuple(to_dev(inp[n][None]) for n in ("shared_gate", "shared_up", "shared_down"))
+    idx, w, _ = ops.route(x_d, to_dev(inp["w_router"]), k, bias=to_dev(inp["bias"]))
+    z = oracle.router_logits(synth.values(inp["x"]), synth.values(inp["w_router"]), inp["bias"])
+    ridx = oracle.topk_select(z, k)
+    assert np.array_equal(to_host(idx), ridx)
+    # resident set = the S most-routed experts of the batch (a perfect predictor)
+    slot = ops.plan_slots(np.bincount(ridx.ravel(), minlength=E), S)
+    y = torch.zeros_like(x_d)
+    _, inc = _layer_batch(x_d, idx, w, W, E, None, slot, y, shared)
+    assert np.array_equal(to_host(inc), (slot[ridx] < 0).any(axis=1).astype(np.int32))
+    sample = np.sort(np.random.default_rng(4).choice(T, 48, replace=False))
+    ref = _oracle_sample(inp, cfg, sample, slot, bias=inp["bias"])
+    assert rel_max_err(vals(y)[sample], ref["y"]) <= 1e-2
+
+
+def test_missed_experts_second_pass_completes_the_output():
+    """Real-time correction: run the resident experts, then the missed ones
+    with accumulate=1; the sum equals the all-resident layer."""
+    cfg = dict(synth.config(2), T=512, H=512, F=1024)
+    E, k = cfg["E"], cfg["k"]
+    inp = synth.layer_inputs(cfg, 7)
+    x_d = to_dev(inp["x"])
+    W = _gpu_weights(inp)
+    idx, w, _ = ops.route(x_d, to_dev(inp["w_router"]), k)
+    resident = np.array([0, -1, 1, -1, 2, 3, -1, 4], dtype=np.int32)
+    missed = np.where(resident < 0, np.cumsum(resident < 0) - 1, -1).astype(np.int32)
+    y = torch.zeros_like(x_d)
+    _layer_batch(x_d, idx, w, W, E, None, resident, y)
+    res_m = [e for e in range(E) if missed[e] >= 0]
+    sel = torch.tensor(res_m, dtype=torch.long, device=DEV)
+    off, rop, _, xp = ops.permute(x_d, idx, E)
+    yp = ops.expert_ffn(xp, off, *(W[n].index_select(0, sel).contiguous()
+                                   for n in ("w_gate", "w_up", "w_down")),
+                        slot_of_expert=to_dev(missed))
+    ops.combine(yp, idx, w, rop, slot_of_expert=to_dev(missed), y=y, accumulate=True)
+    full = oracle.moe_layer(synth.values(inp["x"]), synth.values(inp["w_router"]), k,
+                            synth.values(inp["w_gate"]), synth.values(inp["w_up"]),
+                            synth.values(inp["w_down"]))
+    assert rel_max_err(vals(y), full["y"]) <= 2e-2
