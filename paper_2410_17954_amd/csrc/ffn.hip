@@ -35,11 +35,15 @@ constexpr int BK = 64;
 constexpr int kThreads = 256;
 constexpr int kChunks = BK / 8;           // 16-byte K-chunks per tile row
 
-// Per-expert row-tile prefix of resident experts.
+// Per-expert row-tile prefix of resident experts; also clears the per-XCD
+// tile-claim counters of the two GEMMs (kClaimWords ints after prefix[E]).
+constexpr int kClaimWords = 16;
 __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
                                  const int32_t* __restrict__ slot, int E, int S,
                                  int64_t max_rows, int bm, int32_t* __restrict__ prefix) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  if (blockIdx.x != 0) return;
+  if (threadIdx.x < kClaimWords) prefix[E + 1 + threadIdx.x] = 0;
+  if (threadIdx.x != 0) return;
   int32_t run = 0;
   for (int e = 0; e < E; ++e) {
     prefix[e] = run;
@@ -273,7 +277,7 @@ ffn_gemm_bf16_v2(const uint16_t* __restrict__ A, int64_t K,
                  int64_t F, int64_t H,
                  const int32_t* __restrict__ offsets, const int32_t* __restrict__ slot,
                  int E, int64_t max_rows, const int32_t* __restrict__ prefix,
-                 uint16_t* __restrict__ C) {
+                 int32_t* __restrict__ claim, uint16_t* __restrict__ C) {
   constexpr int BM = v2::BM, BN = v2::BN;
   constexpr int CPR = BK / 8;                  // 16-byte chunks per tile row
   constexpr int RPW = 128 / BK;                // rows per 256-byte bank window
@@ -303,16 +307,25 @@ ffn_gemm_bf16_v2(const uint16_t* __restrict__ A, int64_t K,
   const int wm = wave >> 2, wn = wave & 3;    // 2 x 4 waves
 
   const int64_t total = (int64_t)prefix[E] * n_tiles;
-  const int64_t G = gridDim.x;
-  const int64_t per_xcd = G / 8;
-  const int64_t first = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int64_t per_xcd = gridDim.x / 8;        // blocks per XCD = tiles per chunk
+  const int xcd = blockIdx.x % 8;
   const int64_t ktiles = K / BK;
+  __shared__ int64_t s_claim;
 
   const int lrow = lane / CPR;                // row within a DMA piece
   const int lpch = lane % CPR;                // physical chunk this lane fills
   auto swz = [](int r, int c) { return c ^ ((r / RPW) % CPR); };
 
-  for (int64_t t = first; t < total; t += G) {
+  // Tiles are claimed dynamically from a per-XCD counter: the j-th claim on
+  // XCD x takes tile ((j / C) * 8 + x) * C + j % C (C = blocks per XCD), so
+  // each XCD walks its own chunks of C consecutive tiles, and blocks that
+  // drew cheap (partly empty) tiles simply claim more.
+  for (;;) {
+    if (tid == 0) s_claim = atomicAdd(&claim[xcd], 1);
+    __syncthreads();
+    const int64_t j = s_claim;
+    const int64_t t = ((j / per_xcd) * 8 + xcd) * per_xcd + (j % per_xcd);
+    if (t >= total) break;
     int e = 0;
     while (e + 1 < E && (int64_t)prefix[e + 1] * n_tiles <= t) ++e;
     const int64_t local = t - (int64_t)prefix[e] * n_tiles;
@@ -327,6 +340,10 @@ ffn_gemm_bf16_v2(const uint16_t* __restrict__ A, int64_t K,
     const int64_t row0 = lo + mt * BM;
     const int64_t row_end = min(row0 + (int64_t)BM, hi);
     const int64_t n0 = nt * kOutN;
+    // A wave whose 128-row half holds no row of the expert skips its LDS reads
+    // and MFMAs (it still takes part in loads and barriers), so a tile with at
+    // most 128 rows costs about half.
+    const bool active = __builtin_amdgcn_readfirstlane((int)(row_end - row0 > wm * 128)) != 0;
 
     // Per-lane source pointers (the K offset is added per step). Rows past the
     // end of the expert (or of the weight) read a valid row; their results are
@@ -404,28 +421,30 @@ ffn_gemm_bf16_v2(const uint16_t* __restrict__ A, int64_t K,
       // MFMAs, so LDS latency overlaps the matrix work.
       constexpr int KS = BK / 16;
       bf16x8_t af[KS][4], bfr[KS][2];
+      if (active) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int ch = ks * 2 + fk;
+        for (int ks = 0; ks < KS; ++ks) {
+          const int ch = ks * 2 + fk;
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi) {
-          const int r = wm * 128 + mi * 32 + frow;
-          af[ks][mi] = *reinterpret_cast<const bf16x8_t*>(&as[r * BK + swz(r, ch) * 8]);
+          for (int mi = 0; mi < 4; ++mi) {
+            const int r = wm * 128 + mi * 32 + frow;
+            af[ks][mi] = *reinterpret_cast<const bf16x8_t*>(&as[r * BK + swz(r, ch) * 8]);
+          }
+#pragma unroll
+          for (int ni = 0; ni < 2; ++ni) {
+            const int r = wn * 64 + ni * 32 + frow;
+            bfr[ks][ni] = *reinterpret_cast<const bf16x8_t*>(&bs[r * BK + swz(r, ch) * 8]);
+          }
         }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-          const int r = wn * 64 + ni * 32 + frow;
-          bfr[ks][ni] = *reinterpret_cast<const bf16x8_t*>(&bs[r * BK + swz(r, ch) * 8]);
-        }
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+              acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][mi], bfr[ks][ni], acc[mi][ni], 0, 0, 0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-          for (int ni = 0; ni < 2; ++ni)
-            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][mi], bfr[ks][ni], acc[mi][ni], 0, 0, 0);
       // Wait for the loads of step kt+1 only; later steps stay in flight.
       const int64_t later = min(kt + STAGES - 1, ktiles - 1) - (kt + 1);
       if (later >= 2) wait_vmcnt<2 * 2 * PPW>();
@@ -534,7 +553,7 @@ extern "C" size_t moe_expert_ffn_workspace(int64_t max_rows, int64_t H, int64_t 
   if (max_rows < 1 || F < 1 || E < 1 || !moe::valid_dtype(dtype)) return 0;
   const size_t elt = dtype == MOE_BF16 ? 2 : 4;
   size_t bytes = moe::align_up((size_t)max_rows * (size_t)F * elt, 256);
-  bytes += moe::align_up((size_t)(E + 1) * sizeof(int32_t), 256);
+  bytes += moe::align_up((size_t)(E + 1 + 16) * sizeof(int32_t), 256);
   return bytes;
 }
 
@@ -590,10 +609,12 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
   auto* yb = static_cast<uint16_t*>(y_perm);
   if (fast) {
     ffn_gemm_bf16_v2<0, v2::FAST_BK, v2::FAST_STAGES><<<dim3(grid), dim3(v2::kThreads), 0, st>>>(
-        xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix, ab);
+        xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
+        prefix + E + 1, ab);
     MOE_CHECK_LAUNCH();
     ffn_gemm_bf16_v2<1, v2::FAST_BK, v2::FAST_STAGES><<<dim3(grid), dim3(v2::kThreads), 0, st>>>(
-        ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix, yb);
+        ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
+        prefix + E + 1 + 8, yb);
     MOE_CHECK_LAUNCH();
     return MOE_OK;
   }
