@@ -23,6 +23,8 @@
 // (12 + 5 * max_iters launches); nothing is read back to the host.
 #include "common.h"
 
+#include <algorithm>
+
 namespace moe {
 namespace {
 
@@ -100,9 +102,11 @@ __device__ __forceinline__ uint64_t lowbit(uint64_t d) { return d & (0ull - d); 
 // ---------------------------------------------------------------- kernels
 __global__ void __launch_bounds__(kT)
 sch_pack(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
-         uint64_t* __restrict__ bits, int32_t* __restrict__ ones) {
+         uint64_t* __restrict__ bits, uint64_t* __restrict__ bits_t, int32_t* __restrict__ ones,
+         int32_t* __restrict__ rank) {
   const int i = blockIdx.x * kT + threadIdx.x;
   if (i >= N) return;
+  rank[i] = 0;
   uint64_t* b = bits + (int64_t)i * W;
   for (int w = 0; w < W; ++w) b[w] = 0;
   const uint8_t* r = routes + (int64_t)i * L * k;
@@ -115,7 +119,10 @@ sch_pack(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
       }
     }
   int c = 0;
-  for (int w = 0; w < W; ++w) c += __popcll(b[w]);
+  for (int w = 0; w < W; ++w) {
+    c += __popcll(b[w]);
+    bits_t[(int64_t)w * N + i] = b[w];          // word-major copy: coalesced per word
+  }
   ones[i] = c;
 }
 
@@ -353,6 +360,7 @@ __global__ void __launch_bounds__(kSel)
 sch_finish(int N, int n1, int L, int E, int keep_if_worse, int trivial,
            const int32_t* __restrict__ in1, const int32_t* __restrict__ cnt,
            const int32_t* __restrict__ cnt_orig, const int64_t* __restrict__ state,
+           const int32_t* __restrict__ err,
            int32_t* __restrict__ perm, int32_t* __restrict__ demand, int64_t* __restrict__ info) {
   const int LE = L * E;
   int a = 0, b = 0;
@@ -382,7 +390,8 @@ sch_finish(int N, int n1, int L, int E, int keep_if_worse, int trivial,
   if (demand)
     for (int q = threadIdx.x; q < 2 * LE; q += kSel) demand[q] = src[q];
   if (threadIdx.x == 0) {
-    info[0] = trivial ? 0 : state[ST_ITERS];
+    // a bounded wait that timed out in the cooperative loop marks the result
+    info[0] = (*err) ? -1 : (trivial ? 0 : state[ST_ITERS]);
     info[1] = trivial ? 1 : state[ST_CONV];
     info[2] = trivial ? -1 : state[ST_AM1];
     info[3] = trivial ? -1 : state[ST_AM2];
@@ -393,8 +402,361 @@ sch_finish(int N, int n1, int L, int E, int keep_if_worse, int trivial,
   }
 }
 
+// ------------------------------------------------ rank with keys in LDS
+// Same count as sch_rank, with the whole key of every token of the j-tile
+// staged in LDS and token i's key in registers (W <= WMAX words), so equal
+// leading words never go back to global memory.
+template <int WMAX>
+__global__ void __launch_bounds__(kT)
+sch_rank_keys(const uint64_t* __restrict__ bits, int N, int W, int tile,
+              int32_t* __restrict__ rank) {
+  extern __shared__ uint64_t s_keys[];          // [tile][W]
+  const int j0 = blockIdx.y * tile;
+  const int jn = min(tile, N - j0);
+  for (int q = threadIdx.x; q < jn * W; q += kT) s_keys[q] = bits[(int64_t)j0 * W + q];
+  __syncthreads();
+  const int i = blockIdx.x * kT + threadIdx.x;
+  if (i >= N) return;
+  uint64_t ki[WMAX];
+#pragma unroll
+  for (int w = 0; w < WMAX; ++w) ki[w] = (w < W) ? bits[(int64_t)i * W + w] : 0ull;
+  // Most pairs differ in their first word; the remaining words are compared
+  // only on a tie there (all still in LDS / registers).
+  auto before = [&](int q) -> int {
+    const uint64_t* kj = s_keys + q * W;
+    const uint64_t a0 = kj[0];
+    const uint64_t d0 = a0 ^ ki[0];
+    if (d0) return (a0 & lowbit(d0)) != 0;
+#pragma unroll
+    for (int w = 1; w < WMAX; ++w) {
+      if (w < W) {
+        const uint64_t a = kj[w];
+        const uint64_t d = a ^ ki[w];
+        if (d) return (a & lowbit(d)) != 0;
+      }
+    }
+    return (j0 + q) < i;                          // equal keys: index order; j == i adds 0
+  };
+  int cnt = 0;
+  int q = 0;
+  for (; q + 4 <= jn; q += 4) cnt += before(q) + before(q + 1) + before(q + 2) + before(q + 3);
+  for (; q < jn; ++q) cnt += before(q);
+  atomicAdd(&rank[i], cnt);
+}
+
+// ------------------------------------------------ cooperative round loop
+// All rounds in one cooperative launch (every block resident): block b owns
+// a contiguous range of token indices and the same range of signature ranks.
+// Data that crosses blocks inside the launch is read and written with
+// device-scope atomics, and phases are separated by a grid barrier on a
+// monotonic arrival counter: every thread issues an agent-scope release fence
+// before its block arrives (the XCD L2s are not coherent with each other, and
+// a workgroup barrier does not wait for the other waves' memory operations)
+// and an acquire fence after the wait. Every barrier wait is
+// bounded: past the bound the block records an error and goes on, so the
+// launch always terminates (the result is then flagged, never trusted).
+// Candidates are packed as (value << 24 | signature rank) and reduced with a
+// 64-bit atomicMin, which keeps the lower-rank tie rule.
+constexpr int kCoopT = 256;
+constexpr int kCoopMaxLE = 8192;
+constexpr unsigned kSpinBound = 1u << 20;
+
+// Shared data within the launch: reads as an atomic add of zero, writes as an
+// atomic exchange, the same path the accumulating atomics take.
+__device__ __forceinline__ int ld_coh(const int32_t* p) {
+  return atomicAdd(const_cast<int32_t*>(p), 0);
+}
+__device__ __forceinline__ void st_coh(int32_t* p, int32_t v) { atomicExch(p, v); }
+__device__ __forceinline__ unsigned long long ld_coh64(const unsigned long long* p) {
+  return atomicAdd(const_cast<unsigned long long*>(p), 0ull);
+}
+__device__ __forceinline__ void st_coh64(unsigned long long* p, unsigned long long v) {
+  atomicExch(p, v);
+}
+
+__device__ void grid_sync(unsigned* bar, unsigned nblk, int32_t* err) {
+  // Release: every wave waits for its own stores and atomics and writes the
+  // XCD's L2 back, so the arrival below is ordered after all of them (a
+  // workgroup barrier alone does not wait for other waves' memory traffic).
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned arrived = atomicAdd(bar, 1u) + 1u;
+    const unsigned target = (arrived + nblk - 1u) / nblk * nblk;
+    unsigned spins = 0;
+    while (atomicAdd(bar, 0u) < target) {
+      __builtin_amdgcn_s_sleep(1);
+      if (++spins == kSpinBound) {
+        atomicExch(err, 1);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+  __threadfence();                               // acquire: drop stale cached lines
+}
+
+__device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long w = __shfl_xor(v, o, kWave);
+    v = w < v ? w : v;
+  }
+  return v;
+}
+
+struct CoopArgs {
+  const uint64_t* bits_t;   // [W][N] word-major paths
+  const int32_t* ones;
+  const int32_t* rank;
+  const int32_t* order;
+  int N, W, LE, n1, nbins, off, max_iters, trivial, twoLk;
+  int32_t* delta;           // [N]
+  int32_t* in1;             // [N]
+  int32_t* hist;            // [nbins]
+  int32_t* cnt;             // [2][LE]
+  int32_t* cnt_orig;        // [2][LE]
+  unsigned long long* tot;  // [4]: batch sums, then input-split sums
+  unsigned long long* cand; // [2]
+  int32_t* tiecnt;          // [nblk]
+  unsigned* bar;
+  int32_t* err;
+  int64_t* state;
+};
+
+__global__ void __launch_bounds__(kCoopT)
+sch_coop(CoopArgs a) {
+  __shared__ int32_t s_c[2 * kCoopMaxLE];        // local column counts / copy of cnt
+  __shared__ uint64_t s_med[2][kCoopMaxLE / 64];
+  __shared__ unsigned long long s_red[kCoopT / kWave];
+  __shared__ int s_thr, s_q;
+  __shared__ unsigned long long s_tot[2];
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const unsigned nblk = gridDim.x;
+  const int N = a.N, W = a.W, LE = a.LE;
+  const int per = (N + (int)nblk - 1) / (int)nblk;
+  const int t0 = min(N, (int)blockIdx.x * per), t1 = min(N, t0 + per);
+
+  auto word = [&](int i, int w) { return a.bits_t[(int64_t)w * N + i]; };
+
+  auto block_min_u64 = [&](unsigned long long v) {
+    v = wave_min_u64(v);
+    if (lane == 0) s_red[tid / kWave] = v;
+    __syncthreads();
+    unsigned long long r = s_red[0];
+    for (int w = 1; w < kCoopT / kWave; ++w) r = s_red[w] < r ? s_red[w] : r;
+    __syncthreads();
+    return r;
+  };
+
+  // Column counts of this block's tokens into global cnt (batch of token i
+  // from `batch_of`), plus |r| sums into tot[2 * which + batch].
+  auto count = [&](auto batch_of, int32_t* dst, int which) {
+    for (int q = tid; q < 2 * LE; q += kCoopT) s_c[q] = 0;
+    if (tid < 2) s_tot[tid] = 0;
+    __syncthreads();
+    for (int i = t0 + tid; i < t1; i += kCoopT) {
+      const int c = batch_of(i);
+      for (int w = 0; w < W; ++w) {
+        uint64_t x = word(i, w);
+        while (x) {
+          atomicAdd(&s_c[c * LE + w * 64 + __builtin_ctzll(x)], 1);
+          x &= x - 1;
+        }
+      }
+      atomicAdd(&s_tot[c], (unsigned long long)a.ones[i]);
+    }
+    __syncthreads();
+    for (int q = tid; q < 2 * LE; q += kCoopT)
+      if (s_c[q]) atomicAdd(&dst[q], s_c[q]);
+    if (tid < 2 && s_tot[tid]) atomicAdd(&a.tot[2 * which + tid], s_tot[tid]);
+  };
+
+  // Candidate key of token i under the batch sums copied into s_c / s_tot.
+  auto dist_key = [&](int i, int c, int64_t size) -> unsigned long long {
+    const int32_t* cc = s_c + c * LE;
+    int64_t g = 0;
+    for (int w = 0; w < W; ++w) {
+      uint64_t x = word(i, w);
+      while (x) {
+        g += cc[w * 64 + __builtin_ctzll(x)];
+        x &= x - 1;
+      }
+    }
+    const int64_t D = size * a.ones[i] + (int64_t)s_tot[c] - 2 * g;
+    return ((unsigned long long)D << 24) | (unsigned long long)a.rank[i];
+  };
+
+  // ---- input split: column counts (Eq. 2 before, demand of the original)
+  count([&](int i) { return i < a.n1 ? 0 : 1; }, a.cnt_orig, 1);
+  if (a.trivial) return;                          // uniform over the grid
+  grid_sync(a.bar, nblk, a.err);
+
+  // ---- m1: least total distance; counts over everyone = both input batches
+  for (int q = tid; q < LE; q += kCoopT) s_c[q] = ld_coh(a.cnt_orig + q) + ld_coh(a.cnt_orig + LE + q);
+  if (tid == 0) s_tot[0] = ld_coh64(a.tot + 2) + ld_coh64(a.tot + 3);
+  __syncthreads();
+  {
+    unsigned long long best = ~0ull;
+    for (int i = t0 + tid; i < t1; i += kCoopT) {
+      const unsigned long long k = dist_key(i, 0, N);
+      best = k < best ? k : best;
+    }
+    best = block_min_u64(best);
+    if (tid == 0) atomicMin(&a.cand[0], best);
+  }
+  grid_sync(a.bar, nblk, a.err);
+  auto decode = [&](unsigned long long key) {
+    const int r = (int)(key & 0xFFFFFF);
+    return r < N ? a.order[r] : 0;               // empty batch only after a barrier error
+  };
+  int m1 = decode(ld_coh64(a.cand));
+  for (int w = tid; w < W; w += kCoopT) s_med[0][w] = word(m1, w);
+  __syncthreads();
+  // ---- m2: farthest from m1, as a minimum of (2Lk - d, rank)
+  {
+    unsigned long long best = ~0ull;
+    for (int i = t0 + tid; i < t1; i += kCoopT) {
+      if (i == m1) continue;
+      int d = 0;
+      for (int w = 0; w < W; ++w) d += __popcll(word(i, w) ^ s_med[0][w]);
+      const unsigned long long k = ((unsigned long long)(a.twoLk - d) << 24) | (unsigned long long)a.rank[i];
+      best = k < best ? k : best;
+    }
+    best = block_min_u64(best);
+    if (tid == 0) atomicMin(&a.cand[1], best);
+  }
+  grid_sync(a.bar, nblk, a.err);
+  int m2 = decode(ld_coh64(a.cand + 1));
+
+  int iters = 0, conv = 0, am1 = -1, am2 = -1;
+  for (int it = 1; it <= a.max_iters; ++it) {
+    // A: delta_i = d(i, m1) - d(i, m2) for own tokens, histogram
+    for (int w = tid; w < W; w += kCoopT) {
+      s_med[0][w] = word(m1, w);
+      s_med[1][w] = word(m2, w);
+    }
+    __syncthreads();
+    for (int i = t0 + tid; i < t1; i += kCoopT) {
+      int d = 0;
+      for (int w = 0; w < W; ++w) {
+        const uint64_t x = word(i, w);
+        d += __popcll(x ^ s_med[0][w]) - __popcll(x ^ s_med[1][w]);
+      }
+      st_coh(a.delta + i, d);
+      atomicAdd(&a.hist[d + a.off], 1);
+    }
+    grid_sync(a.bar, nblk, a.err);
+    // B: threshold (every block alike), ties of own rank range; resets
+    {
+      const int pb = (a.nbins + kCoopT - 1) / kCoopT;
+      const int v0 = min(a.nbins, tid * pb), v1 = min(a.nbins, v0 + pb);
+      int local = 0;
+      for (int v = v0; v < v1; ++v) local += ld_coh(a.hist + v);
+      int total;
+      int cum = block_excl_scan<kCoopT>(local, &total);
+      for (int v = v0; v < v1; ++v) {
+        const int h = ld_coh(a.hist + v);
+        if (cum < a.n1 && cum + h >= a.n1) {
+          s_thr = v - a.off;
+          s_q = a.n1 - cum;
+        }
+        cum += h;
+      }
+    }
+    __syncthreads();
+    const int thr = s_thr, q = s_q;
+    const int sub = (t1 - t0 + kCoopT - 1) / kCoopT;      // ranks per thread
+    const int r0 = min(t1, t0 + tid * sub), r1 = min(t1, r0 + sub);
+    int ties = 0;
+    for (int r = r0; r < r1; ++r) ties += ld_coh(a.delta + a.order[r]) == thr;
+    int btot;
+    int pre_in_block = block_excl_scan<kCoopT>(ties, &btot);
+    if (tid == 0) st_coh(a.tiecnt + blockIdx.x, btot);
+    if (blockIdx.x == 0) {
+      if (tid < 2) st_coh64(a.cand + tid, ~0ull);
+      if (tid < 2) st_coh64(a.tot + tid, 0ull);
+    }
+    for (int qq = blockIdx.x * kCoopT + tid; qq < 2 * LE; qq += (int)nblk * kCoopT) st_coh(a.cnt + qq, 0);
+    grid_sync(a.bar, nblk, a.err);
+    // C: the first n1 in (delta, rank) order go to batch 1; hist reset
+    {
+      int before = 0;
+      for (unsigned b = 0; b < blockIdx.x; ++b) before += ld_coh(a.tiecnt + b);
+      int pre = before + pre_in_block;
+      for (int r = r0; r < r1; ++r) {
+        const int i = a.order[r];
+        const int d = ld_coh(a.delta + i);
+        st_coh(a.in1 + i, d < thr ? 1 : (d > thr ? 0 : (pre++ < q ? 1 : 0)));
+      }
+    }
+    for (int v = blockIdx.x * kCoopT + tid; v < a.nbins; v += (int)nblk * kCoopT) st_coh(a.hist + v, 0);
+    am1 = m1;
+    am2 = m2;
+    iters = it;
+    grid_sync(a.bar, nblk, a.err);
+    // D: batch column counts
+    count([&](int i) { return ld_coh(a.in1 + i) ? 0 : 1; }, a.cnt, 0);
+    grid_sync(a.bar, nblk, a.err);
+    // E: centroid candidates per batch
+    for (int qq = tid; qq < 2 * LE; qq += kCoopT) s_c[qq] = ld_coh(a.cnt + qq);
+    if (tid < 2) s_tot[tid] = ld_coh64(a.tot + tid);
+    __syncthreads();
+    {
+      unsigned long long b0 = ~0ull, b1 = ~0ull;
+      for (int i = t0 + tid; i < t1; i += kCoopT) {
+        const int c = ld_coh(a.in1 + i) ? 0 : 1;
+        const unsigned long long k = dist_key(i, c, c == 0 ? a.n1 : N - a.n1);
+        if (c == 0) b0 = k < b0 ? k : b0;
+        else b1 = k < b1 ? k : b1;
+      }
+      b0 = block_min_u64(b0);
+      b1 = block_min_u64(b1);
+      if (tid == 0) {
+        atomicMin(&a.cand[0], b0);
+        atomicMin(&a.cand[1], b1);
+      }
+    }
+    grid_sync(a.bar, nblk, a.err);
+    // F: new centroids; stop when they repeat (same decision in every block)
+    const int n1c = decode(ld_coh64(a.cand));
+    const int n2c = decode(ld_coh64(a.cand + 1));
+    if (n1c == m1 && n2c == m2) {
+      conv = 1;
+      break;
+    }
+    m1 = n1c;
+    m2 = n2c;
+  }
+  if (blockIdx.x == 0 && tid == 0) {
+    a.state[ST_ITERS] = iters;
+    a.state[ST_CONV] = conv;
+    a.state[ST_AM1] = am1;
+    a.state[ST_AM2] = am2;
+  }
+}
+
+// Clears the small scratch of one call (a kernel rather than memset nodes,
+// so that the sequence can be captured in a graph).
+__global__ void __launch_bounds__(kT)
+sch_init(int32_t* __restrict__ hist, int nbins, int32_t* __restrict__ cnt_orig, int LE2,
+         unsigned long long* __restrict__ tot, unsigned long long* __restrict__ cand,
+         unsigned* __restrict__ bar, int32_t* __restrict__ err, int64_t* __restrict__ state) {
+  const int g = blockIdx.x * kT + threadIdx.x, stride = gridDim.x * kT;
+  for (int q = g; q < nbins; q += stride) hist[q] = 0;
+  for (int q = g; q < LE2; q += stride) cnt_orig[q] = 0;
+  if (g < 4) tot[g] = 0;
+  if (g < 2) cand[g] = ~0ull;
+  if (g < ST_NWORDS) state[g] = 0;
+  if (g == 0) {
+    *bar = 0;
+    *err = 0;
+  }
+}
+
 struct SchLayout {
-  size_t bits, ones, rank, order, delta, in1, cnt, cnt_orig, hist, tot, state, cand, total;
+  size_t bits, bits_t, ones, rank, order, delta, in1, cnt, cnt_orig, hist, tot, state, cand,
+      cand2, tiecnt, bar, total;
 };
 
 SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
@@ -410,6 +772,7 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
     return at;
   };
   s.bits = take(N * W * 8);
+  s.bits_t = take(N * W * 8);
   s.ones = take(N * 4);
   s.rank = take(N * 4);
   s.order = take(N * 4);
@@ -418,9 +781,12 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
   s.cnt = take(2 * LE * 4);
   s.cnt_orig = take(2 * LE * 4);
   s.hist = take(nbins * 4);
-  s.tot = take(2 * 8);
+  s.tot = take(4 * 8);
   s.state = take(ST_NWORDS * 8);
   s.cand = take(nblk * 2 * sizeof(Cand));
+  s.cand2 = take(2 * 8);
+  s.tiecnt = take(nblk * 4);
+  s.bar = take(2 * 4);                    // arrival counter, error flag
   s.total = o;
   return s;
 }
@@ -450,6 +816,7 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
     return MOE_ERR_WORKSPACE;
   char* ws = static_cast<char*>(workspace);
   auto* bits = reinterpret_cast<uint64_t*>(ws + lay.bits);
+  auto* bits_t = reinterpret_cast<uint64_t*>(ws + lay.bits_t);
   auto* ones = reinterpret_cast<int32_t*>(ws + lay.ones);
   auto* rank = reinterpret_cast<int32_t*>(ws + lay.rank);
   auto* order = reinterpret_cast<int32_t*>(ws + lay.order);
@@ -461,6 +828,10 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   auto* tot = reinterpret_cast<unsigned long long*>(ws + lay.tot);
   auto* state = reinterpret_cast<int64_t*>(ws + lay.state);
   auto* cand = reinterpret_cast<Cand*>(ws + lay.cand);
+  auto* cand2 = reinterpret_cast<unsigned long long*>(ws + lay.cand2);
+  auto* tiecnt = reinterpret_cast<int32_t*>(ws + lay.tiecnt);
+  auto* bar = reinterpret_cast<unsigned*>(ws + lay.bar);
+  auto* err = reinterpret_cast<int32_t*>(ws + lay.bar + 4);
 
   const int n = (int)N, W = (L * E + 63) / 64, LE = L * E;
   const int nbins = 4 * L * k + 1, off = 2 * L * k;
@@ -471,60 +842,98 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
 #define MOE_TRY(expr) \
   do { if ((expr) != hipSuccess) return MOE_ERR_HIP; } while (0)
 
-  MOE_TRY(fill_i64(state, 0, ST_NWORDS, st));
-  MOE_TRY(fill_i32(cnt, 0, 2 * (int64_t)LE, st));
-  MOE_TRY(fill_i32(cnt_orig, 0, 2 * (int64_t)LE, st));
-  MOE_TRY(fill_i64(reinterpret_cast<int64_t*>(tot), 0, 2, st));
-  sch_pack<<<grid, blk, 0, st>>>(routes, n, L, E, k, W, bits, ones);
-  MOE_CHECK_LAUNCH();
-  // Eq. 2 of the input split; the column counts of [0,n1) and [n1,N).
-  unsigned long long* tot_scratch = tot;  // reset by sch_select before reuse
-  sch_colcount<<<grid, blk, cc_lds, st>>>(bits, ones, n, W, LE, 1, (int)n1, in1, cnt_orig,
-                                         tot_scratch, state);
-  MOE_CHECK_LAUNCH();
   const bool trivial = (n1 == 0 || n1 == N);
-  if (!trivial) {
-    MOE_TRY(fill_i32(rank, 0, N, st));
-    MOE_TRY(fill_i32(hist, 0, nbins, st));
-    MOE_TRY(fill_i64(reinterpret_cast<int64_t*>(tot), 0, 2, st));
-    sch_rank<<<dim3(nblk, (unsigned)ceil_div(N, kRankTile)), blk, 0, st>>>(bits, n, W, rank);
-    MOE_CHECK_LAUNCH();
+
+  sch_init<<<dim3((unsigned)std::min<int64_t>(64, ceil_div(std::max(nbins, 2 * LE), kT))), blk, 0,
+             st>>>(hist, nbins, cnt_orig, 2 * LE, tot, cand2, bar, err, state);
+  MOE_CHECK_LAUNCH();
+  sch_pack<<<grid, blk, 0, st>>>(routes, n, L, E, k, W, bits, bits_t, ones, rank);
+  MOE_CHECK_LAUNCH();
+  auto launch_rank = [&]() -> int {
+    if (W <= 32) {
+      const int tile = std::min(256, 65536 / (8 * W));
+      const dim3 g2(nblk, (unsigned)ceil_div(N, tile));
+      const size_t lds = (size_t)tile * W * sizeof(uint64_t);
+      if (W <= 4) sch_rank_keys<4><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
+      else if (W <= 8) sch_rank_keys<8><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
+      else if (W <= 16) sch_rank_keys<16><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
+      else sch_rank_keys<32><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
+    } else {
+      sch_rank<<<dim3(nblk, (unsigned)ceil_div(N, kRankTile)), blk, 0, st>>>(bits, n, W, rank);
+    }
+    if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
     sch_order<<<grid, blk, 0, st>>>(rank, n, order);
+    return hipGetLastError() != hipSuccess ? MOE_ERR_HIP : MOE_OK;
+  };
+
+  bool done = false;
+  const bool coop_fits = LE <= kCoopMaxLE && N < (1 << 24) && 2 * (int64_t)L * k < (1 << 15);
+  if (!trivial && coop_fits) {
+    const int rc = launch_rank();
+    if (rc != MOE_OK) return rc;
+    const int cus = device_cu_count();
+    const int nb = (int)std::max<int64_t>(1, std::min<int64_t>(cus, ceil_div(N, kCoopT)));
+    CoopArgs ca{bits_t, ones, rank, order, n, W, LE, (int)n1, nbins, off, max_iters, 0,
+                2 * L * k, delta, in1, hist, cnt, cnt_orig, tot, cand2, tiecnt, bar, err, state};
+    void* args[] = {&ca};
+    if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&sch_coop), dim3(nb),
+                                   dim3(kCoopT), args, 0, st) == hipSuccess) {
+      done = true;
+    } else {
+      (void)hipGetLastError();                 // fall back to one launch per phase
+      MOE_TRY(fill_i64(state, 0, ST_NWORDS, st));
+      MOE_TRY(fill_i32(cnt_orig, 0, 2 * (int64_t)LE, st));
+      MOE_TRY(fill_i32(hist, 0, nbins, st));
+    }
+  }
+  if (!done) {
+    MOE_TRY(fill_i32(cnt, 0, 2 * (int64_t)LE, st));
+    MOE_TRY(fill_i64(reinterpret_cast<int64_t*>(tot), 0, 2, st));
+    // Eq. 2 of the input split; the column counts of [0,n1) and [n1,N).
+    sch_colcount<<<grid, blk, cc_lds, st>>>(bits, ones, n, W, LE, 1, (int)n1, in1, cnt_orig,
+                                           tot, state);
     MOE_CHECK_LAUNCH();
-    // m1: least total distance to every token
-    sch_colcount<<<grid, blk, cc_lds, st>>>(bits, ones, n, W, LE, 0, (int)n1, in1, cnt, tot,
-                                           state);
-    MOE_CHECK_LAUNCH();
-    sch_cand<<<grid, blk, 0, st>>>(bits, ones, rank, n, W, LE, 0, (int)n1, in1, cnt, tot, state,
-                                   cand);
-    MOE_CHECK_LAUNCH();
-    sch_pick<<<dim3(1), dim3(kSel), 0, st>>>(cand, nblk, 0, state);
-    MOE_CHECK_LAUNCH();
-    // m2: farthest from m1
-    sch_cand<<<grid, blk, 0, st>>>(bits, ones, rank, n, W, LE, 1, (int)n1, in1, cnt, tot, state,
-                                   cand);
-    MOE_CHECK_LAUNCH();
-    sch_pick<<<dim3(1), dim3(kSel), 0, st>>>(cand, nblk, 1, state);
-    MOE_CHECK_LAUNCH();
-    for (int it = 0; it < max_iters; ++it) {
-      sch_delta<<<grid, blk, 0, st>>>(bits, n, W, off, delta, hist, state);
-      MOE_CHECK_LAUNCH();
-      sch_select<<<dim3(1), dim3(kSel), 0, st>>>(n, (int)n1, nbins, off, delta, order, hist, in1,
-                                                cnt, LE, tot, state);
-      MOE_CHECK_LAUNCH();
-      sch_colcount<<<grid, blk, cc_lds, st>>>(bits, ones, n, W, LE, 2, (int)n1, in1, cnt, tot,
+    if (!trivial) {
+      MOE_TRY(fill_i64(reinterpret_cast<int64_t*>(tot), 0, 2, st));
+      if (!coop_fits) {
+        const int rc = launch_rank();
+        if (rc != MOE_OK) return rc;
+      }
+      // m1: least total distance to every token
+      sch_colcount<<<grid, blk, cc_lds, st>>>(bits, ones, n, W, LE, 0, (int)n1, in1, cnt, tot,
                                              state);
       MOE_CHECK_LAUNCH();
-      sch_cand<<<grid, blk, 0, st>>>(bits, ones, rank, n, W, LE, 2, (int)n1, in1, cnt, tot,
+      sch_cand<<<grid, blk, 0, st>>>(bits, ones, rank, n, W, LE, 0, (int)n1, in1, cnt, tot,
                                      state, cand);
       MOE_CHECK_LAUNCH();
-      sch_pick<<<dim3(1), dim3(kSel), 0, st>>>(cand, nblk, 2, state);
+      sch_pick<<<dim3(1), dim3(kSel), 0, st>>>(cand, nblk, 0, state);
       MOE_CHECK_LAUNCH();
+      // m2: farthest from m1
+      sch_cand<<<grid, blk, 0, st>>>(bits, ones, rank, n, W, LE, 1, (int)n1, in1, cnt, tot,
+                                     state, cand);
+      MOE_CHECK_LAUNCH();
+      sch_pick<<<dim3(1), dim3(kSel), 0, st>>>(cand, nblk, 1, state);
+      MOE_CHECK_LAUNCH();
+      for (int it = 0; it < max_iters; ++it) {
+        sch_delta<<<grid, blk, 0, st>>>(bits, n, W, off, delta, hist, state);
+        MOE_CHECK_LAUNCH();
+        sch_select<<<dim3(1), dim3(kSel), 0, st>>>(n, (int)n1, nbins, off, delta, order, hist,
+                                                  in1, cnt, LE, tot, state);
+        MOE_CHECK_LAUNCH();
+        sch_colcount<<<grid, blk, cc_lds, st>>>(bits, ones, n, W, LE, 2, (int)n1, in1, cnt, tot,
+                                               state);
+        MOE_CHECK_LAUNCH();
+        sch_cand<<<grid, blk, 0, st>>>(bits, ones, rank, n, W, LE, 2, (int)n1, in1, cnt, tot,
+                                       state, cand);
+        MOE_CHECK_LAUNCH();
+        sch_pick<<<dim3(1), dim3(kSel), 0, st>>>(cand, nblk, 2, state);
+        MOE_CHECK_LAUNCH();
+      }
     }
   }
   sch_finish<<<dim3(1), dim3(kSel), 0, st>>>(n, (int)n1, L, E, keep_original_if_worse,
-                                            trivial ? 1 : 0, in1, cnt, cnt_orig, state, perm,
-                                            demand, info);
+                                            trivial ? 1 : 0, in1, cnt, cnt_orig, state, err,
+                                            perm, demand, info);
   MOE_CHECK_LAUNCH();
 #undef MOE_TRY
   return MOE_OK;
