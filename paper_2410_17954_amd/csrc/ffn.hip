@@ -14,8 +14,9 @@
 // together and share it through that XCD's L2. A small prologue kernel turns
 // expert_offsets and the slot table into a prefix of row tiles per resident
 // expert; everything stays on the device.
-// Fast path (H and F multiples of 32): `ffn_gemm_bf16_v2`, 256 x 256 x 32
-// tiles, 8 waves, a four-stage LDS ring filled by direct global->LDS DMA.
+// Fast path (H and F multiples of 32): `ffn_gemm_bf16_fast`, 256 x 256 x 32
+// tiles, 4 waves of 128 x 128, a four-stage LDS ring filled by direct
+// global->LDS DMA.
 // General path (H, F multiples of 8): `ffn_gemm_bf16`, 256 x 128 x 64 tiles,
 // 4 waves, register-staged LDS double buffer with zero-filled K tails.
 //
@@ -240,22 +241,7 @@ ffn_gemm_bf16(const uint16_t* __restrict__ A, int64_t K,
   }
 }
 
-// ------------------------------------------------------- bf16 fast path
-// 256 x 256 tiles, 8 waves (2 per SIMD) in a 2 (M) x 4 (N) arrangement, each
-// wave 128 x 64 of the output (4 x 2 MFMA 32x32x16 tiles). Operands move from
-// global memory straight into LDS (global_load_lds_dwordx4: each lane deposits
-// 16 bytes at M0 + 16 * lane), so no registers are spent on staging; the XOR
-// swizzle is applied on the load side by choosing which K-chunk each lane
-// fetches. A ring of STAGES LDS stages of BK-deep tiles keeps STAGES-1 steps
-// of loads in flight while one step is multiplied; at the end of a step each
-// wave waits only for the loads of the next step, then one barrier.
-// Needs K % BK == 0.
-namespace v2 {
-constexpr int BM = 256, BN = 256;
-constexpr int kWaves = 8, kThreads = kWaves * 64;
-constexpr int FAST_BK = 32, FAST_STAGES = 4;
-}  // namespace v2
-
+// ------------------------------------------------------- LDS DMA helpers
 typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ void lds_dma16(const void* g, void* lds_wave_base) {
@@ -270,56 +256,89 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int EPI, int BK, int STAGES>
-__global__ void __launch_bounds__(v2::kThreads, 1)
-ffn_gemm_bf16_v2(const uint16_t* __restrict__ A, int64_t K,
+// ------------------------------------------------------- bf16 fast path
+// 256 x 256 block tiles, K in steps of 32, 4 waves (one per SIMD), each
+// owning a 128 x 128 quarter of the output: 16 MFMA 32x32x16 accumulators,
+// 256 registers, held in the accumulation registers. Per K-step a wave reads
+// 128 + 128 rows of fragments from LDS for 2 x 128 x 128 x 32 flop, which
+// keeps LDS traffic (fragment reads plus DMA writes) under the LDS bandwidth.
+// Operands move from global memory straight into LDS
+// (global_load_lds_dwordx4: each lane deposits 16 bytes at M0 + 16 * lane),
+// with an XOR swizzle applied on the load side by choosing which K-chunk each
+// lane fetches. A ring of four LDS stages keeps three K-steps of loads in
+// flight. Within a step the second half-step's fragments are read while the
+// first half's MFMAs run, then one barrier, then the next step's first
+// fragments are read while the second half's MFMAs run; the A loads of a
+// later step are spread over the first half and its B loads over the second,
+// so the memory pipe never stalls MFMA issue for long.
+// A tile whose expert has at most 128 rows left is computed by all 4 waves
+// side by side (each 32, 64 or 128 rows x 64 columns), so a ragged last row
+// tile costs in proportion to its rows, on every SIMD.
+// Needs K % 32 == 0.
+namespace fast {
+constexpr int BM = 256, BN = 256, BK = 32, STAGES = 4;
+constexpr int kWaves = 4, kThreads = kWaves * 64;
+constexpr int CPR = BK / 8;                 // 16-byte chunks per tile row
+constexpr int RPW = 128 / BK;               // rows per 256-byte bank window
+constexpr int ROWS_PER_PIECE = 512 / BK;    // rows per 1 KB DMA piece
+constexpr int PIECES = BM * BK / 512;       // 1 KB pieces per operand stage
+constexpr int PPW = PIECES / kWaves;        // pieces per wave per operand
+constexpr int kStage = BM * BK;             // elements per operand stage
+static_assert(BM == BN, "A and B stages share the piece layout");
+static_assert(STAGES * 2 * kStage * 2 <= 160 * 1024, "LDS");
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / RPW) % CPR); }
+}  // namespace fast
+
+// Workgroup barrier for the K loop: this wave's LDS reads have returned
+// (a stage is refilled by DMA only after every wave passed the barrier that
+// follows its last reads) and its DMA of the awaited step was waited for
+// beforehand; no memory fence, which would drain every DMA in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0) only
+  __builtin_amdgcn_s_barrier();
+}
+
+template <int EPI>
+__global__ void __launch_bounds__(fast::kThreads, 1)
+ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
                  const uint16_t* __restrict__ B0, const uint16_t* __restrict__ B1,
                  int64_t F, int64_t H,
                  const int32_t* __restrict__ offsets, const int32_t* __restrict__ slot,
                  int E, int64_t max_rows, const int32_t* __restrict__ prefix,
                  int32_t* __restrict__ claim, uint16_t* __restrict__ C) {
-  constexpr int BM = v2::BM, BN = v2::BN;
-  constexpr int CPR = BK / 8;                  // 16-byte chunks per tile row
-  constexpr int RPW = 128 / BK;                // rows per 256-byte bank window
-  constexpr int ROWS_PER_PIECE = 512 / BK;     // rows per 1 KB DMA piece
-  constexpr int PIECES = BM * BK / 512;        // 1 KB pieces per operand stage
-  constexpr int PPW = PIECES / v2::kWaves;     // pieces per wave per operand
-  constexpr int kStageA = BM * BK, kStageB = BN * BK;   // elements
+  constexpr int BM = fast::BM, BN = fast::BN, BK = fast::BK, STAGES = fast::STAGES;
+  constexpr int CPR = fast::CPR, ROWS_PER_PIECE = fast::ROWS_PER_PIECE, PPW = fast::PPW;
+  constexpr int kStage = fast::kStage;
+  auto swz = [](int r, int c) { return fast::swz(r, c); };
   constexpr int kOutN = EPI == 0 ? BN / 2 : BN;
-  static_assert(PPW * v2::kWaves == PIECES, "piece split");
-  static_assert((STAGES * (kStageA + kStageB) * 2) <= 160 * 1024, "LDS");
-
   const int64_t N_out = EPI == 0 ? F : H;
   const int64_t ldc = N_out;
   const int64_t n_tiles = (N_out + kOutN - 1) / kOutN;
 
-  // One LDS object per stage: the compiler then proves that a DMA into one
-  // stage cannot alias reads of another and inserts no blanket vmcnt(0).
-  static_assert(STAGES == 4, "four LDS stages");
-  __shared__ __attribute__((aligned(1024))) uint16_t As0[kStageA], As1[kStageA], As2[kStageA], As3[kStageA];
-  __shared__ __attribute__((aligned(1024))) uint16_t Bs0[kStageB], Bs1[kStageB], Bs2[kStageB], Bs3[kStageB];
+  __shared__ __attribute__((aligned(1024))) uint16_t As0[kStage], As1[kStage], As2[kStage], As3[kStage];
+  __shared__ __attribute__((aligned(1024))) uint16_t Bs0[kStage], Bs1[kStage], Bs2[kStage], Bs3[kStage];
   uint16_t* const As[4] = {As0, As1, As2, As3};
   uint16_t* const Bs[4] = {Bs0, Bs1, Bs2, Bs3};
+  __shared__ int64_t s_claim;
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wave = tid / kWave;
-  const int wm = wave >> 2, wn = wave & 3;    // 2 x 4 waves
-
-  const int64_t total = (int64_t)prefix[E] * n_tiles;
-  const int64_t per_xcd = gridDim.x / 8;        // blocks per XCD = tiles per chunk
-  const int xcd = blockIdx.x % 8;
-  const int64_t ktiles = K / BK;
-  __shared__ int64_t s_claim;
-
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int frow = lane & 31;                 // fragment row within a 32-row MFMA tile
+  const int fk = lane >> 5;                   // which 8-wide half of a 16-wide K step
   const int lrow = lane / CPR;                // row within a DMA piece
   const int lpch = lane % CPR;                // physical chunk this lane fills
-  auto swz = [](int r, int c) { return c ^ ((r / RPW) % CPR); };
 
-  // Tiles are claimed dynamically from a per-XCD counter: the j-th claim on
-  // XCD x takes tile ((j / C) * 8 + x) * C + j % C (C = blocks per XCD), so
-  // each XCD walks its own chunks of C consecutive tiles, and blocks that
-  // drew cheap (partly empty) tiles simply claim more.
+  const int64_t total = (int64_t)prefix[E] * n_tiles;
+  const int64_t per_xcd = gridDim.x / 8;
+  const int xcd = blockIdx.x % 8;
+  const int64_t ksteps = K / BK;
+
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+
   for (;;) {
     if (tid == 0) s_claim = atomicAdd(&claim[xcd], 1);
     __syncthreads();
@@ -340,154 +359,224 @@ ffn_gemm_bf16_v2(const uint16_t* __restrict__ A, int64_t K,
     const int64_t row0 = lo + mt * BM;
     const int64_t row_end = min(row0 + (int64_t)BM, hi);
     const int64_t n0 = nt * kOutN;
-    // A wave whose 128-row half holds no row of the expert skips its LDS reads
-    // and MFMAs (it still takes part in loads and barriers), so a tile with at
-    // most 128 rows costs about half.
-    const bool active = __builtin_amdgcn_readfirstlane((int)(row_end - row0 > wm * 128)) != 0;
+    const int nrows = (int)(row_end - row0);
 
-    // Per-lane source pointers (the K offset is added per step). Rows past the
-    // end of the expert (or of the weight) read a valid row; their results are
+    // DMA sources: a wave-uniform base per piece plus a 32-bit byte offset
+    // per lane (the K offset is added to the base per step). Rows past the
+    // end of the expert or of the weight read a valid row; their results are
     // never stored.
-    const uint16_t* a_src[PPW];
-    const uint16_t* b_src[PPW];
+    const char* const a_base = reinterpret_cast<const char*>(A + row0 * K);
+    const char* b_base[PPW];
+    uint32_t a_off[PPW], b_off[PPW];
 #pragma unroll
     for (int i = 0; i < PPW; ++i) {
-      const int r = (wave * PPW + i) * ROWS_PER_PIECE + lrow;   // tile row
-      const int lch = swz(r, lpch);                              // logical chunk
-      int64_t ar = row0 + r;
-      if (ar >= row_end) ar = row0;
-      a_src[i] = A + ar * K + lch * 8;
+      const int piece = wave * PPW + i;
+      const int r = piece * ROWS_PER_PIECE + lrow;
+      const int lch = swz(r, lpch);
+      a_off[i] = (uint32_t)(((r < nrows ? r : 0) * K + lch * 8) * 2);
       int64_t wrow;
-      const uint16_t* base;
       if (EPI == 0) {
-        const int grp = r >> 5;                  // 32-row groups: gate, up, gate, up, ...
+        const int grp = piece >> 1;              // 32-row groups: gate, up, gate, up, ...
         int64_t f = n0 + (grp >> 1) * 32 + (r & 31);
         if (f >= F) f = 0;
-        base = ((grp & 1) ? B1 : B0) + (int64_t)s * F * H;
+        b_base[i] = reinterpret_cast<const char*>(((grp & 1) ? B1 : B0) + (int64_t)s * F * H);
         wrow = f;
       } else {
         int64_t h = n0 + r;
         if (h >= H) h = 0;
-        base = B0 + (int64_t)s * H * F;
+        b_base[i] = reinterpret_cast<const char*>(B0 + (int64_t)s * H * F);
         wrow = h;
       }
-      b_src[i] = base + wrow * K + lch * 8;
+      b_off[i] = (uint32_t)((wrow * K + lch * 8) * 2);
     }
     auto issue = [&](auto stage_c, int64_t step) {
       constexpr int stage = decltype(stage_c)::value;
-      const int64_t k0 = step * BK;
+      const int64_t kb = step * BK * 2;
 #pragma unroll
       for (int i = 0; i < PPW; ++i) {
-        lds_dma16(a_src[i] + k0, As[stage] + (wave * PPW + i) * 512);
-        lds_dma16(b_src[i] + k0, Bs[stage] + (wave * PPW + i) * 512);
+        lds_dma16(a_base + kb + a_off[i], As[stage] + (wave * PPW + i) * 512);
+        lds_dma16(b_base[i] + kb + b_off[i], Bs[stage] + (wave * PPW + i) * 512);
       }
     };
+    auto issue_a = [&](auto stage_c, int64_t step) {
+      constexpr int stage = decltype(stage_c)::value;
+      const int64_t kb = step * BK * 2;
+#pragma unroll
+      for (int i = 0; i < PPW; ++i) lds_dma16(a_base + kb + a_off[i], As[stage] + (wave * PPW + i) * 512);
+    };
+    auto issue_b = [&](auto stage_c, int64_t step) {
+      constexpr int stage = decltype(stage_c)::value;
+      const int64_t kb = step * BK * 2;
+#pragma unroll
+      for (int i = 0; i < PPW; ++i) lds_dma16(b_base[i] + kb + b_off[i], Bs[stage] + (wave * PPW + i) * 512);
+    };
 
-    f32x16_t acc[4][2];
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) acc[mi][ni][q] = 0.f;
+    // MODE 0: 2 x 2 waves of 128 x 128; MODE m in {1, 2, 4}: 4 waves side by
+    // side, each m x 32 rows by 64 columns.
+    auto run = [&](auto mode_c) {
+      constexpr int MODE = decltype(mode_c)::value;
+      constexpr bool FULL = MODE == 0;
+      constexpr int MI = FULL ? 4 : MODE;
+      constexpr int NI = FULL ? 4 : 2;
+      const int rbase = FULL ? (wave >> 1) * 128 : 0;
+      const int cbase = FULL ? (wave & 1) * 128 : wave * 64;
 
-    // prologue: STAGES-1 steps in flight, the first one complete
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    using I3 = std::integral_constant<int, 3>;
-    if (0 < ktiles) issue(I0{}, 0);
-    if (1 < ktiles) issue(I1{}, 1);
-    if (2 < ktiles) issue(I2{}, 2);
-    {
-      const int64_t inflight = min((int64_t)STAGES - 1, ktiles) - 1;   // beyond step 0
-      if (inflight >= 2) wait_vmcnt<2 * 2 * PPW>();
-      else if (inflight == 1) wait_vmcnt<2 * PPW>();
-      else wait_vmcnt<0>();
-    }
-    __syncthreads();
+      f32x16_t acc[MI][NI];
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+          for (int q = 0; q < 16; ++q) acc[mi][ni][q] = 0.f;
+      bf16x8_t fa0[MI], fb0[NI], fa1[MI], fb1[NI];
 
-    const int frow = lane & 31;
-    const int fk = lane >> 5;
-    // One K-step on stage J: start the loads of step kt+3 into stage J+3
-    // (mod 4), multiply stage J, wait for step kt+1, barrier.
-    auto step = [&](auto j_c, int64_t kt) {
-      constexpr int J = decltype(j_c)::value;
-      if (kt + STAGES - 1 < ktiles)
-        issue(std::integral_constant<int, (J + STAGES - 1) % STAGES>{}, kt + STAGES - 1);
-      const uint16_t* as = As[J];
-      const uint16_t* bs = Bs[J];
-      // All fragments of the step first (BK/16 substeps x 6 reads), then the
-      // MFMAs, so LDS latency overlaps the matrix work.
-      constexpr int KS = BK / 16;
-      bf16x8_t af[KS][4], bfr[KS][2];
-      if (active) {
+      auto rd = [&](auto stage_c, int ks, bf16x8_t (&fa)[MI], bf16x8_t (&fb)[NI]) {
+        constexpr int J = decltype(stage_c)::value;
+        const uint16_t* as = As[J];
+        const uint16_t* bs = Bs[J];
+        const int ch = ks * 2 + fk;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const int ch = ks * 2 + fk;
-#pragma unroll
-          for (int mi = 0; mi < 4; ++mi) {
-            const int r = wm * 128 + mi * 32 + frow;
-            af[ks][mi] = *reinterpret_cast<const bf16x8_t*>(&as[r * BK + swz(r, ch) * 8]);
-          }
-#pragma unroll
-          for (int ni = 0; ni < 2; ++ni) {
-            const int r = wn * 64 + ni * 32 + frow;
-            bfr[ks][ni] = *reinterpret_cast<const bf16x8_t*>(&bs[r * BK + swz(r, ch) * 8]);
-          }
+        for (int mi = 0; mi < MI; ++mi) {
+          const int r = rbase + mi * 32 + frow;
+          fa[mi] = *reinterpret_cast<const bf16x8_t*>(&as[r * BK + swz(r, ch) * 8]);
         }
-        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
+        for (int ni = 0; ni < NI; ++ni) {
+          const int r = cbase + ni * 32 + frow;
+          fb[ni] = *reinterpret_cast<const bf16x8_t*>(&bs[r * BK + swz(r, ch) * 8]);
+        }
+      };
+      auto mm = [&](const bf16x8_t (&fa)[MI], const bf16x8_t (&fb)[NI]) {
 #pragma unroll
-          for (int mi = 0; mi < 4; ++mi)
+        for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-            for (int ni = 0; ni < 2; ++ni)
-              acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks][mi], bfr[ks][ni], acc[mi][ni], 0, 0, 0);
+          for (int ni = 0; ni < NI; ++ni)
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[ni], acc[mi][ni], 0, 0, 0);
+      };
+      // One K-step on stage J: DMA of step kt+3 into stage J+3 (mod 4); the
+      // second half-step's fragments are read while the first half's MFMAs
+      // run; wait for step kt+1; barrier; the next step's first fragments are
+      // read while this step's second half runs.
+      auto step = [&](auto j_c, int64_t kt) {
+        constexpr int J = decltype(j_c)::value;
+        if (kt + STAGES - 1 < ksteps)
+          issue(std::integral_constant<int, (J + STAGES - 1) % STAGES>{}, kt + STAGES - 1);
+        rd(j_c, 1, fa1, fb1);
+        mm(fa0, fb0);
+        const int64_t later = min(kt + STAGES - 1, ksteps - 1) - (kt + 1);
+        if (later >= 2) wait_vmcnt<2 * 2 * PPW>();
+        else if (later == 1) wait_vmcnt<2 * PPW>();
+        else wait_vmcnt<0>();
+        lds_barrier();
+        if (kt + 1 < ksteps) rd(std::integral_constant<int, (J + 1) % STAGES>{}, 0, fa0, fb0);
+        mm(fa1, fb1);
+      };
+
+      // Steady state (steps kt + 3 < ksteps): the same step with every
+      // condition known, so the waits are fixed and exact.
+      auto step_ss = [&](auto j_c, int64_t kt) {
+        constexpr int J = decltype(j_c)::value;
+        constexpr int JN = (J + STAGES - 1) % STAGES;
+        issue_a(std::integral_constant<int, JN>{}, kt + STAGES - 1);
+        rd(j_c, 1, fa1, fb1);
+        mm(fa0, fb0);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+        // outstanding after step kt+1: A,B of kt+2 and A of kt+3
+        wait_vmcnt<3 * PPW>();
+        lds_barrier();
+        issue_b(std::integral_constant<int, JN>{}, kt + STAGES - 1);
+        rd(std::integral_constant<int, (J + 1) % STAGES>{}, 0, fa0, fb0);
+        mm(fa1, fb1);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+        }
+      };
+
+      if (0 < ksteps) issue(I0{}, 0);
+      if (1 < ksteps) issue(I1{}, 1);
+      if (2 < ksteps) issue(I2{}, 2);
+      {
+        const int64_t inflight = min((int64_t)STAGES - 1, ksteps) - 1;
+        if (inflight >= 2) wait_vmcnt<2 * 2 * PPW>();
+        else if (inflight == 1) wait_vmcnt<2 * PPW>();
+        else wait_vmcnt<0>();
       }
-      // Wait for the loads of step kt+1 only; later steps stay in flight.
-      const int64_t later = min(kt + STAGES - 1, ktiles - 1) - (kt + 1);
-      if (later >= 2) wait_vmcnt<2 * 2 * PPW>();
-      else if (later == 1) wait_vmcnt<2 * PPW>();
-      else wait_vmcnt<0>();
       __syncthreads();
-    };
-    int64_t kt = 0;
-    for (; kt + STAGES <= ktiles; kt += STAGES) {
-      step(I0{}, kt);
-      step(I1{}, kt + 1);
-      step(I2{}, kt + 2);
-      step(I3{}, kt + 3);
-    }
-    if (kt < ktiles) step(I0{}, kt);
-    if (kt + 1 < ktiles) step(I1{}, kt + 1);
-    if (kt + 2 < ktiles) step(I2{}, kt + 2);
+      rd(I0{}, 0, fa0, fb0);
+      int64_t kt = 0;
+      for (; kt + STAGES + STAGES - 1 <= ksteps; kt += STAGES) {
+        step_ss(I0{}, kt);
+        step_ss(I1{}, kt + 1);
+        step_ss(I2{}, kt + 2);
+        step_ss(I3{}, kt + 3);
+      }
+      for (; kt + STAGES <= ksteps; kt += STAGES) {
+        step(I0{}, kt);
+        step(I1{}, kt + 1);
+        step(I2{}, kt + 2);
+        step(I3{}, kt + 3);
+      }
+      if (kt < ksteps) step(I0{}, kt);
+      if (kt + 1 < ksteps) step(I1{}, kt + 1);
+      if (kt + 2 < ksteps) step(I2{}, kt + 2);
 
-    // Epilogue (32x32 C layout: column lane % 32, rows 8*(q/4) + 4*(lane/32) + q%4).
-    const int ccol = lane & 31;
-    const int crow = (lane >> 5) * 4;
+      // Epilogue (32x32 C layout: column lane % 32, rows 8*(q/4) + 4*(lane/32) + q%4).
+      // The row stride is made opaque per tile so that the 16 * MI row
+      // offsets are formed where they are used rather than hoisted out of
+      // the tile loop into registers.
+      int64_t ld = ldc;
+      asm volatile("" : "+s"(ld));
+      const int ccol = lane & 31;
+      const int crow = (lane >> 5) * 4;
+      const int r_lane = rbase + crow;                       // tile row of q = 0, mi = 0
+      uint16_t* const c_lane = C + (row0 + r_lane) * ld + n0 + ccol;
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
+      for (int mi = 0; mi < MI; ++mi) {
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int64_t r = row0 + wm * 128 + mi * 32 + 8 * (q >> 2) + crow + (q & 3);
-        if (r >= row_end) continue;
-        if (EPI == 0) {
-          const int64_t f = n0 + wn * 32 + ccol;
-          if (f < F) {
-            const float g = acc[mi][0][q];
-            const float u = acc[mi][1][q];
-            C[r * ldc + f] = f32_to_bf16(g / (1.f + expf(-g)) * u);
-          }
-        } else {
+        for (int q = 0; q < 16; ++q) {
+          const int dr = mi * 32 + 8 * (q >> 2) + (q & 3);
+          if (r_lane + dr >= nrows) continue;
+          uint16_t* const c_row = c_lane + dr * ld;
+          if (EPI == 0) {
 #pragma unroll
-          for (int ni = 0; ni < 2; ++ni) {
-            const int64_t h = n0 + wn * 64 + ni * 32 + ccol;
-            if (h < H) C[r * ldc + h] = f32_to_bf16(acc[mi][ni][q]);
+            for (int p = 0; p < NI / 2; ++p) {
+              const int fc = cbase / 2 + p * 32;
+              if (n0 + fc + ccol < F) {
+                const float g = acc[mi][2 * p][q];
+                const float u = acc[mi][2 * p + 1][q];
+                c_row[fc] = f32_to_bf16(g / (1.f + expf(-g)) * u);
+              }
+            }
+          } else {
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni) {
+              const int hc = cbase + ni * 32;
+              if (n0 + hc + ccol < H) c_row[hc] = f32_to_bf16(acc[mi][ni][q]);
+            }
           }
         }
       }
-    }
+    };
+    if (nrows > 128) run(std::integral_constant<int, 0>{});
+    else if (nrows > 64) run(std::integral_constant<int, 4>{});
+    else if (nrows > 32) run(std::integral_constant<int, 2>{});
+    else run(std::integral_constant<int, 1>{});
   }
 }
 
@@ -594,8 +683,10 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
     return MOE_OK;
   }
 
-  const bool fast = (H % v2::FAST_BK == 0) && (F % v2::FAST_BK == 0);
-  const int bm = fast ? v2::BM : BM;
+  // The fast path addresses one expert's weight matrix, and 256 rows of an
+  // activation, with 32-bit byte offsets.
+  const bool fast = (H % fast::BK == 0) && (F % fast::BK == 0) && F * H < ((int64_t)1 << 31);
+  const int bm = fast ? fast::BM : BM;
   ffn_tiles_kernel<<<dim3(1), dim3(64), 0, st>>>(expert_offsets, slot_of_expert, E, S, max_rows,
                                                  bm, prefix);
   MOE_CHECK_LAUNCH();
@@ -608,11 +699,11 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
   const auto* wdb = static_cast<const uint16_t*>(w_down);
   auto* yb = static_cast<uint16_t*>(y_perm);
   if (fast) {
-    ffn_gemm_bf16_v2<0, v2::FAST_BK, v2::FAST_STAGES><<<dim3(grid), dim3(v2::kThreads), 0, st>>>(
+    ffn_gemm_bf16_fast<0><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
         xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
         prefix + E + 1, ab);
     MOE_CHECK_LAUNCH();
-    ffn_gemm_bf16_v2<1, v2::FAST_BK, v2::FAST_STAGES><<<dim3(grid), dim3(v2::kThreads), 0, st>>>(
+    ffn_gemm_bf16_fast<1><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
         ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
         prefix + E + 1 + 8, yb);
     MOE_CHECK_LAUNCH();
