@@ -167,6 +167,12 @@ int moe_permute(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
  * y_perm         [max_rows,H] dtype output
  * Shared (always-on) experts use the same call with E = 1, offsets {0, T},
  * slot {0} and their weights concatenated along F.
+ * workspace      moe_expert_ffn_workspace(max_rows, H, F, E, dtype) bytes,
+ *                256-byte aligned, caller-owned: the activation a, tile
+ *                counters and (bf16 with H, F multiples of 32) fp32 partial
+ *                tiles of the last round of tiles, which is split along K;
+ *                pieces are summed in a fixed order, so results do not depend
+ *                on scheduling. Calls that share a workspace must not overlap.
  * Limits: max_rows >= 1, H >= 1, F >= 1, 1 <= E <= 256, S >= 0; bf16 needs
  *   H % 8 == 0 and F % 8 == 0.
  * ---------------------------------------------------------------------- */

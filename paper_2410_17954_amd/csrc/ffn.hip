@@ -25,6 +25,7 @@
 
 #include <math.h>
 
+#include <algorithm>
 #include <type_traits>
 
 namespace moe {
@@ -36,14 +37,20 @@ constexpr int BK = 64;
 constexpr int kThreads = 256;
 constexpr int kChunks = BK / 8;           // 16-byte K-chunks per tile row
 
-// Per-expert row-tile prefix of resident experts; also clears the per-XCD
-// tile-claim counters of the two GEMMs (kClaimWords ints after prefix[E]).
+// Counters after prefix[E]: 16 per-XCD tile claims (8 per GEMM), then per
+// GEMM one claim counter for the split tail and kMaxTailTiles arrival
+// counters (one per tail tile).
 constexpr int kClaimWords = 16;
+constexpr int kMaxTailTiles = 1024;
+constexpr int kTailWords = 1 + kMaxTailTiles;
+constexpr int kCounterWords = kClaimWords + 2 * kTailWords;
+
+// Per-expert row-tile prefix of resident experts; also clears the counters.
 __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
                                  const int32_t* __restrict__ slot, int E, int S,
                                  int64_t max_rows, int bm, int32_t* __restrict__ prefix) {
   if (blockIdx.x != 0) return;
-  if (threadIdx.x < kClaimWords) prefix[E + 1 + threadIdx.x] = 0;
+  for (int q = threadIdx.x; q < kCounterWords; q += blockDim.x) prefix[E + 1 + q] = 0;
   if (threadIdx.x != 0) return;
   int32_t run = 0;
   for (int e = 0; e < E; ++e) {
@@ -284,10 +291,30 @@ constexpr int ROWS_PER_PIECE = 512 / BK;    // rows per 1 KB DMA piece
 constexpr int PIECES = BM * BK / 512;       // 1 KB pieces per operand stage
 constexpr int PPW = PIECES / kWaves;        // pieces per wave per operand
 constexpr int kStage = BM * BK;             // elements per operand stage
+// Split-K of the last, partial round of tiles: at most kMaxSplit pieces per
+// tile, each at least kMinSplitSteps K-steps; a piece's fp32 partial tile is
+// 256 threads x 64 float4 (256 KB) in the workspace.
+constexpr int kMaxSplit = 8, kMinSplitSteps = 16;
+constexpr int kMaxPieces = 512;
+constexpr size_t kPieceBytes = 256 * 64 * 16;
 static_assert(BM == BN, "A and B stages share the piece layout");
 static_assert(STAGES * 2 * kStage * 2 <= 160 * 1024, "LDS");
 __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / RPW) % CPR); }
 }  // namespace fast
+
+// The fast path addresses one expert's weight matrix, and 256 rows of an
+// activation, with 32-bit byte offsets.
+inline bool fast_path(int64_t H, int64_t F) {
+  return H % fast::BK == 0 && F % fast::BK == 0 && F * H < ((int64_t)1 << 31);
+}
+
+// Partial tiles the workspace holds for the split tail of either GEMM.
+inline int64_t max_split_pieces(int64_t max_rows, int64_t H, int64_t F, int E) {
+  const int64_t row_tiles = ceil_div(max_rows, fast::BM) + E;
+  const int64_t col_tiles = std::max(ceil_div(F, fast::BN / 2), ceil_div(H, fast::BN));
+  return std::min<int64_t>(fast::kMaxPieces,
+                           fast::kMaxSplit * std::min<int64_t>(row_tiles * col_tiles, kMaxTailTiles));
+}
 
 // Workgroup barrier for the K loop: this wave's LDS reads have returned
 // (a stage is refilled by DMA only after every wave passed the barrier that
@@ -305,7 +332,8 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
                  int64_t F, int64_t H,
                  const int32_t* __restrict__ offsets, const int32_t* __restrict__ slot,
                  int E, int64_t max_rows, const int32_t* __restrict__ prefix,
-                 int32_t* __restrict__ claim, uint16_t* __restrict__ C) {
+                 int32_t* __restrict__ claim, int32_t* __restrict__ tail,
+                 float* __restrict__ partial, int max_pieces, uint16_t* __restrict__ C) {
   constexpr int BM = fast::BM, BN = fast::BN, BK = fast::BK, STAGES = fast::STAGES;
   constexpr int CPR = fast::CPR, ROWS_PER_PIECE = fast::ROWS_PER_PIECE, PPW = fast::PPW;
   constexpr int kStage = fast::kStage;
@@ -320,6 +348,7 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   uint16_t* const As[4] = {As0, As1, As2, As3};
   uint16_t* const Bs[4] = {Bs0, Bs1, Bs2, Bs3};
   __shared__ int64_t s_claim;
+  __shared__ int s_piece, s_last;
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -330,21 +359,57 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   const int lpch = lane % CPR;                // physical chunk this lane fills
 
   const int64_t total = (int64_t)prefix[E] * n_tiles;
-  const int64_t per_xcd = gridDim.x / 8;
+  const int64_t G = gridDim.x;                 // persistent grid, a multiple of 8
+  const int64_t per_xcd = G / 8;
   const int xcd = blockIdx.x % 8;
   const int64_t ksteps = K / BK;
+
+  // Whole rounds of G tiles are claimed per XCD (each XCD walks its own
+  // chunks of per_xcd consecutive tiles, so the row tiles that share a weight
+  // tile run together on one L2). The last, partial round of rem tiles is
+  // split along K into `split` pieces claimed from one global counter,
+  // chosen to minimise ceil(rem * split / G) / split rounds.
+  const int64_t full = total / G * G;
+  const int64_t rem = total - full;
+  int64_t split = 1;
+  for (int64_t sp = 2; sp <= fast::kMaxSplit; ++sp) {
+    if (ksteps / sp < fast::kMinSplitSteps || rem * sp > max_pieces) break;
+    if (((rem * sp + G - 1) / G) * split < ((rem * split + G - 1) / G) * sp) split = sp;
+  }
 
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
 
+  bool in_tail = false;                        // thread 0 only
   for (;;) {
-    if (tid == 0) s_claim = atomicAdd(&claim[xcd], 1);
+    if (tid == 0) {
+      int64_t tt = -1;
+      int pc = 0;
+      if (!in_tail) {
+        const int64_t j = atomicAdd(&claim[xcd], 1);
+        const int64_t c = ((j / per_xcd) * 8 + xcd) * per_xcd + (j % per_xcd);
+        if (c < full) tt = c;
+        else in_tail = true;
+      }
+      if (in_tail) {
+        const int64_t u = atomicAdd(&tail[0], 1);
+        if (u < rem * split) {
+          tt = full + u / split;
+          pc = (int)(u % split);
+        }
+      }
+      s_claim = tt;
+      s_piece = pc;
+    }
     __syncthreads();
-    const int64_t j = s_claim;
-    const int64_t t = ((j / per_xcd) * 8 + xcd) * per_xcd + (j % per_xcd);
-    if (t >= total) break;
+    const int64_t t = s_claim;
+    const int piece = s_piece;
+    if (t < 0) break;
+    const bool split_tile = t >= full && split > 1;
+    const int64_t kbeg = split_tile ? piece * ksteps / split : 0;
+    const int64_t nks = split_tile ? (piece + 1) * ksteps / split - kbeg : ksteps;
     int e = 0;
     while (e + 1 < E && (int64_t)prefix[e + 1] * n_tiles <= t) ++e;
     const int64_t local = t - (int64_t)prefix[e] * n_tiles;
@@ -391,7 +456,7 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
     }
     auto issue = [&](auto stage_c, int64_t step) {
       constexpr int stage = decltype(stage_c)::value;
-      const int64_t kb = step * BK * 2;
+      const int64_t kb = (kbeg + step) * BK * 2;
 #pragma unroll
       for (int i = 0; i < PPW; ++i) {
         lds_dma16(a_base + kb + a_off[i], As[stage] + (wave * PPW + i) * 512);
@@ -400,13 +465,13 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
     };
     auto issue_a = [&](auto stage_c, int64_t step) {
       constexpr int stage = decltype(stage_c)::value;
-      const int64_t kb = step * BK * 2;
+      const int64_t kb = (kbeg + step) * BK * 2;
 #pragma unroll
       for (int i = 0; i < PPW; ++i) lds_dma16(a_base + kb + a_off[i], As[stage] + (wave * PPW + i) * 512);
     };
     auto issue_b = [&](auto stage_c, int64_t step) {
       constexpr int stage = decltype(stage_c)::value;
-      const int64_t kb = step * BK * 2;
+      const int64_t kb = (kbeg + step) * BK * 2;
 #pragma unroll
       for (int i = 0; i < PPW; ++i) lds_dma16(b_base[i] + kb + b_off[i], Bs[stage] + (wave * PPW + i) * 512);
     };
@@ -459,20 +524,20 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
       // read while this step's second half runs.
       auto step = [&](auto j_c, int64_t kt) {
         constexpr int J = decltype(j_c)::value;
-        if (kt + STAGES - 1 < ksteps)
+        if (kt + STAGES - 1 < nks)
           issue(std::integral_constant<int, (J + STAGES - 1) % STAGES>{}, kt + STAGES - 1);
         rd(j_c, 1, fa1, fb1);
         mm(fa0, fb0);
-        const int64_t later = min(kt + STAGES - 1, ksteps - 1) - (kt + 1);
+        const int64_t later = min(kt + STAGES - 1, nks - 1) - (kt + 1);
         if (later >= 2) wait_vmcnt<2 * 2 * PPW>();
         else if (later == 1) wait_vmcnt<2 * PPW>();
         else wait_vmcnt<0>();
         lds_barrier();
-        if (kt + 1 < ksteps) rd(std::integral_constant<int, (J + 1) % STAGES>{}, 0, fa0, fb0);
+        if (kt + 1 < nks) rd(std::integral_constant<int, (J + 1) % STAGES>{}, 0, fa0, fb0);
         mm(fa1, fb1);
       };
 
-      // Steady state (steps kt + 3 < ksteps): the same step with every
+      // Steady state (steps kt + 3 < nks): the same step with every
       // condition known, so the waits are fixed and exact.
       auto step_ss = [&](auto j_c, int64_t kt) {
         constexpr int J = decltype(j_c)::value;
@@ -508,11 +573,11 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
         }
       };
 
-      if (0 < ksteps) issue(I0{}, 0);
-      if (1 < ksteps) issue(I1{}, 1);
-      if (2 < ksteps) issue(I2{}, 2);
+      if (0 < nks) issue(I0{}, 0);
+      if (1 < nks) issue(I1{}, 1);
+      if (2 < nks) issue(I2{}, 2);
       {
-        const int64_t inflight = min((int64_t)STAGES - 1, ksteps) - 1;
+        const int64_t inflight = min((int64_t)STAGES - 1, nks) - 1;
         if (inflight >= 2) wait_vmcnt<2 * 2 * PPW>();
         else if (inflight == 1) wait_vmcnt<2 * PPW>();
         else wait_vmcnt<0>();
@@ -520,21 +585,73 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
       __syncthreads();
       rd(I0{}, 0, fa0, fb0);
       int64_t kt = 0;
-      for (; kt + STAGES + STAGES - 1 <= ksteps; kt += STAGES) {
+      for (; kt + STAGES + STAGES - 1 <= nks; kt += STAGES) {
         step_ss(I0{}, kt);
         step_ss(I1{}, kt + 1);
         step_ss(I2{}, kt + 2);
         step_ss(I3{}, kt + 3);
       }
-      for (; kt + STAGES <= ksteps; kt += STAGES) {
+      for (; kt + STAGES <= nks; kt += STAGES) {
         step(I0{}, kt);
         step(I1{}, kt + 1);
         step(I2{}, kt + 2);
         step(I3{}, kt + 3);
       }
-      if (kt < ksteps) step(I0{}, kt);
-      if (kt + 1 < ksteps) step(I1{}, kt + 1);
-      if (kt + 2 < ksteps) step(I2{}, kt + 2);
+      if (kt < nks) step(I0{}, kt);
+      if (kt + 1 < nks) step(I1{}, kt + 1);
+      if (kt + 2 < nks) step(I2{}, kt + 2);
+
+      // A K-piece stores its fp32 partial tile; the piece that arrives last
+      // (a device-scope counter per tail tile, ordered by release and acquire
+      // fences) adds all pieces in piece order, so the sum does not depend on
+      // arrival order, and writes the output.
+      if (split_tile) {
+        constexpr int kF4 = fast::kPieceBytes / 16 / 256;       // float4 per thread
+        static_assert(MI * NI * 4 <= kF4, "partial tile layout");
+        const int64_t tile_slot = t - full;
+        f32x4_t* const P = reinterpret_cast<f32x4_t*>(partial);
+        f32x4_t* const mine = P + (tile_slot * split + piece) * (int64_t)kF4 * 256;
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+              f32x4_t v;
+              v[0] = acc[mi][ni][4 * q4];
+              v[1] = acc[mi][ni][4 * q4 + 1];
+              v[2] = acc[mi][ni][4 * q4 + 2];
+              v[3] = acc[mi][ni][4 * q4 + 3];
+              mine[((mi * NI + ni) * 4 + q4) * 256 + tid] = v;
+            }
+        __threadfence();
+        __syncthreads();
+        if (tid == 0) s_last = atomicAdd(&tail[1 + tile_slot], 1) == (int)split - 1;
+        __syncthreads();
+        if (!s_last) return;
+        __threadfence();
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[mi][ni][q] = 0.f;
+        for (int64_t pc = 0; pc < split; ++pc) {
+          const f32x4_t* const src = P + (tile_slot * split + pc) * (int64_t)kF4 * 256;
+#pragma unroll
+          for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+              for (int q4 = 0; q4 < 4; ++q4) {
+                const f32x4_t v = src[((mi * NI + ni) * 4 + q4) * 256 + tid];
+                acc[mi][ni][4 * q4] += v[0];
+                acc[mi][ni][4 * q4 + 1] += v[1];
+                acc[mi][ni][4 * q4 + 2] += v[2];
+                acc[mi][ni][4 * q4 + 3] += v[3];
+              }
+        }
+      }
 
       // Epilogue (32x32 C layout: column lane % 32, rows 8*(q/4) + 4*(lane/32) + q%4).
       // The row stride is made opaque per tile so that the 16 * MI row
@@ -638,11 +755,13 @@ __global__ void ffn_f32_down(const float* __restrict__ act, int64_t H, int64_t F
 
 extern "C" size_t moe_expert_ffn_workspace(int64_t max_rows, int64_t H, int64_t F, int32_t E,
                                            int32_t dtype) {
-  (void)H;
-  if (max_rows < 1 || F < 1 || E < 1 || !moe::valid_dtype(dtype)) return 0;
+  using namespace moe;
+  if (max_rows < 1 || H < 1 || F < 1 || E < 1 || !valid_dtype(dtype)) return 0;
   const size_t elt = dtype == MOE_BF16 ? 2 : 4;
-  size_t bytes = moe::align_up((size_t)max_rows * (size_t)F * elt, 256);
-  bytes += moe::align_up((size_t)(E + 1 + 16) * sizeof(int32_t), 256);
+  size_t bytes = align_up((size_t)max_rows * (size_t)F * elt, 256);
+  bytes += align_up((size_t)(E + 1 + kCounterWords) * sizeof(int32_t), 256);
+  if (dtype == MOE_BF16 && fast_path(H, F))
+    bytes += (size_t)max_split_pieces(max_rows, H, F, E) * fast::kPieceBytes;
   return bytes;
 }
 
@@ -683,15 +802,13 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
     return MOE_OK;
   }
 
-  // The fast path addresses one expert's weight matrix, and 256 rows of an
-  // activation, with 32-bit byte offsets.
-  const bool fast = (H % fast::BK == 0) && (F % fast::BK == 0) && F * H < ((int64_t)1 << 31);
+  const bool fast = fast_path(H, F);
   const int bm = fast ? fast::BM : BM;
   ffn_tiles_kernel<<<dim3(1), dim3(64), 0, st>>>(expert_offsets, slot_of_expert, E, S, max_rows,
                                                  bm, prefix);
   MOE_CHECK_LAUNCH();
   int grid = device_cu_count();
-  grid = (grid + 7) / 8 * 8;
+  grid = std::min((grid + 7) / 8 * 8, kMaxTailTiles);     // a tail round has < grid tiles
   const auto* xb = static_cast<const uint16_t*>(x_perm);
   auto* ab = static_cast<uint16_t*>(act);
   const auto* wgb = static_cast<const uint16_t*>(w_gate);
@@ -699,13 +816,18 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
   const auto* wdb = static_cast<const uint16_t*>(w_down);
   auto* yb = static_cast<uint16_t*>(y_perm);
   if (fast) {
+    int32_t* const claim = prefix + E + 1;
+    int32_t* const tail = claim + kClaimWords;
+    float* const partial = reinterpret_cast<float*>(
+        reinterpret_cast<char*>(prefix) + align_up((size_t)(E + 1 + kCounterWords) * 4, 256));
+    const int pieces = (int)max_split_pieces(max_rows, H, F, E);
     ffn_gemm_bf16_fast<0><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
         xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
-        prefix + E + 1, ab);
+        claim, tail, partial, pieces, ab);
     MOE_CHECK_LAUNCH();
     ffn_gemm_bf16_fast<1><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
         ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
-        prefix + E + 1 + 8, yb);
+        claim + 8, tail + kTailWords, partial, pieces, yb);
     MOE_CHECK_LAUNCH();
     return MOE_OK;
   }

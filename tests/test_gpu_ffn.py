@@ -64,6 +64,19 @@ def test_bf16_ragged_groups(counts, H, F):
     _run(counts, H, F, None, len(counts), seed=sum(counts) + H)
 
 
+@pytest.mark.parametrize("counts,H,F", [
+    ([300, 40, 200], 1024, 4096),      # both GEMMs split their only, partial round along K
+    ([9, 1100, 257, 31], 512, 2048),   # split down projection over ragged tiles of every size
+])
+def test_bf16_split_k_tail(counts, H, F):
+    # Fewer tiles than compute units: the last round is split into K-pieces
+    # whose fp32 partials are summed in a fixed order, so a second call gives
+    # identical bits.
+    got, _, _ = _run(counts, H, F, None, len(counts), seed=sum(counts) + F)
+    again, _, _ = _run(counts, H, F, None, len(counts), seed=sum(counts) + F)
+    np.testing.assert_array_equal(got, again)
+
+
 def test_bf16_resident_subset_and_slot_order():
     counts = [100, 200, 50, 300, 10, 0]
     slot = [2, -1, 0, -1, 1, 3]
