@@ -36,11 +36,71 @@ def parse():
     p.add_argument("--seed", type=int, default=2)
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="CPU budget of the oracle baseline sample (0 = skip)")
+    p.add_argument("--copy-probe-mib", type=int, default=0,
+                   help="after timing, run one plain device copy of this many MiB "
+                        "(the calibration kernel of a counter run)")
+    p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="summarise two rocprofv3 counter_collection.csv files (FETCH_SIZE, "
+                        "WRITE_SIZE) of a --copy-probe-mib run into the traffic file, then exit")
     return p.parse_args()
+
+
+# HBM traffic of moe_expert_ffn, measured by counters on this workload; used
+# only while the FFN source is the one the counters were taken on.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "expert_ffn_mixtral_T4096_traffic.txt")
+FFN_SOURCE = os.path.join(ROOT, "paper_2410_17954_amd", "csrc", "ffn.hip")
+FFN_KERNELS = ("ffn_tiles_kernel", "ffn_gemm_bf16_fast<0>", "ffn_gemm_bf16_fast<1>")
+
+
+def ffn_source_digest():
+    import hashlib
+    with open(FFN_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def pmc_summary(fetch_csv, write_csv, copy_mib):
+    """Per-launch HBM bytes of moe_expert_ffn from FETCH_SIZE and WRITE_SIZE
+    (KiB per dispatch), each scaled by the ratio of true bytes to counter for
+    the plain copy of copy_mib MiB in the same run."""
+    import csv
+    copy_bytes = copy_mib * 2**20
+
+    def per_kernel(path, counter):
+        acc = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            acc.setdefault(name, []).append(float(r["Counter_Value"]) * 1024.0)
+        return acc
+
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        acc = per_kernel(path, counter)
+        copies = [max(v) for n, v in acc.items() if "copyBuffer" in n]
+        probe = max(copies)
+        factor = copy_bytes / probe
+        ffn = 0.0
+        for k in FFN_KERNELS:
+            vals = [v for n, v in acc.items() if k in n]
+            if not vals:
+                raise SystemExit(f"no {k} dispatch in {path}")
+            ffn += float(np.mean(vals[0])) * factor
+        out[counter] = {"bytes_per_launch": ffn, "copy_probe_counter_bytes": probe,
+                        "factor": factor}
+    return out
+
 
 
 def main():
     args = parse()
+    if args.pmc_summary:
+        summ = pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_probe_mib)
+        rec = {"ffn_source_sha256": ffn_source_digest(),
+               "traffic_bytes_per_launch": summ["FETCH_SIZE"]["bytes_per_launch"]
+               + summ["WRITE_SIZE"]["bytes_per_launch"], **summ}
+        print(json.dumps(rec))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this hot path runs on exactly one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
@@ -153,6 +213,12 @@ def main():
             prev = base + 2
     st = {n: v / K for n, v in st.items()}
 
+    if args.copy_probe_mib > 0:
+        src = torch.empty(args.copy_probe_mib * 2**20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
     info_h = info.cpu().numpy()
     inc_h = torch.cat(incs).cpu().numpy()
     assert inc_h.sum() == 0 and torch.isfinite(y.float()).all().item()
@@ -198,9 +264,10 @@ def main():
             "resident": S, "parallelism": "single GPU",
         },
         "roofline": {
-            "bound": "mfma", "kernel": "moe_expert_ffn (grouped SwiGLU: up+gate GEMM, down GEMM)",
+            "bound": "mfma",
+            "kernel": "moe_expert_ffn (" + " + ".join(FFN_KERNELS) + ")",
             "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": measured_traffic(),
             "flop_per_launch": ffn_flops, "launch_ms": ffn_ms,
         },
         "stages": stages,
@@ -209,6 +276,19 @@ def main():
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(inp, routes, cfg, args.cpu_seconds)
     print(json.dumps(out))
+
+
+def measured_traffic():
+    """HBM bytes per moe_expert_ffn launch from the counter summary, or None
+    when there is none or the FFN source has changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = next(json.loads(l) for l in f if l.startswith("{"))
+    except (OSError, StopIteration, ValueError):
+        return None
+    if rec.get("ffn_source_sha256") != ffn_source_digest():
+        return None
+    return rec["traffic_bytes_per_launch"]
 
 
 def cpu_baseline(inp, routes, cfg, budget_s):
