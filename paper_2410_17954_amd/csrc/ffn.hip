@@ -319,10 +319,11 @@ inline int64_t max_split_pieces(int64_t max_rows, int64_t H, int64_t F, int E) {
 // Workgroup barrier for the K loop: this wave's LDS reads have returned
 // (a stage is refilled by DMA only after every wave passed the barrier that
 // follows its last reads) and its DMA of the awaited step was waited for
-// beforehand; no memory fence, which would drain every DMA in flight.
+// beforehand; no memory fence, which would drain every DMA in flight. The
+// asm's memory clobber keeps the compiler from moving any load or store
+// (LDS reads of the next stage in particular) across it.
 __device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt((15) | (7 << 4) | (0 << 8) | (3 << 14));   // lgkmcnt(0) only
-  __builtin_amdgcn_s_barrier();
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int EPI>

@@ -63,3 +63,13 @@ def test_maps_only_without_rows():
     assert xp is None
     assert np.array_equal(to_host(off), r_off) and np.array_equal(to_host(rop), r_rop)
     assert np.array_equal(to_host(por), r_por)
+
+
+def test_maps_only_many_chunks():
+    # 800K pairs: chunks at the largest size (128 tokens x 8 choices), hundreds
+    # of chunks per expert column scan, every expert id in use.
+    idx = synth.random_topk_idx(100_000, 256, 8, 9)
+    off, rop, por, _ = ops.permute(None, to_dev(idx), 256)
+    r_off, r_rop, r_por, _ = oracle.permute(np.zeros((100_000, 1)), idx, 256)
+    assert np.array_equal(to_host(off), r_off) and np.array_equal(to_host(rop), r_rop)
+    assert np.array_equal(to_host(por), r_por)
