@@ -64,6 +64,14 @@ __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
   prefix[E] = run;
 }
 
+// silu(g) * u with the hardware exp2 and reciprocal (about 2 ulp of float32,
+// far below the bf16 rounding of the result); exp2 overflows to +inf for very
+// negative g, giving g * 0 * u = -0 as the exact expression does.
+__device__ __forceinline__ float swiglu(float g, float u) {
+  const float e = __builtin_amdgcn_exp2f(-g * 1.4426950408889634f);
+  return g * __builtin_amdgcn_rcpf(1.f + e) * u;
+}
+
 __device__ __forceinline__ int swz(int row, int chunk) {
   return chunk ^ ((row >> 1) & 7);
 }
@@ -233,7 +241,7 @@ ffn_gemm_bf16(const uint16_t* __restrict__ A, int64_t K,
           if (f < F) {
             const float g = acc[mi][0][q];
             const float u = acc[mi][1][q];
-            const float act = g / (1.f + expf(-g)) * u;
+            const float act = swiglu(g, u);
             C[r * ldc + f] = f32_to_bf16(act);
           }
         } else {
@@ -654,41 +662,87 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
         }
       }
 
-      // Epilogue (32x32 C layout: column lane % 32, rows 8*(q/4) + 4*(lane/32) + q%4).
-      // The row stride is made opaque per tile so that the 16 * MI row
-      // offsets are formed where they are used rather than hoisted out of
-      // the tile loop into registers.
-      int64_t ld = ldc;
-      asm volatile("" : "+s"(ld));
-      const int ccol = lane & 31;
-      const int crow = (lane >> 5) * 4;
-      const int r_lane = rbase + crow;                       // tile row of q = 0, mi = 0
-      uint16_t* const c_lane = C + (row0 + r_lane) * ld + n0 + ccol;
+      // Epilogue, staged through LDS (the stages are free: every wave passed
+      // the last K-step's barrier after its last fragment read). Each wave
+      // writes its bf16 results into the tile, 32 rows per stage array, with
+      // the 16-byte chunks of a row XOR-swizzled by (row mod 8); then the
+      // block stores whole rows with 16-byte coalesced writes.
+      // 32x32 C layout: column lane % 32, rows 8*(q/4) + 4*(lane/32) + q%4.
+      constexpr int NOUT = kOutN;                       // output columns of the tile
+      // Stage array holding rows [32 b, 32 b + 32) of the tile (b compile-time).
+      auto stage_of = [&](auto b_c) -> uint16_t* {
+        constexpr int b = decltype(b_c)::value;
+        if constexpr (b < 4) return As[b];
+        else return Bs[b - 4];
+      };
+      auto off_in = [](int r, int c) {               // r: row within the 32-row block
+        return r * NOUT + ((((c >> 3) ^ (r & 7)) << 3) | (c & 7));
+      };
+      // Lane coordinates are made opaque per tile so that the write addresses
+      // derived from them are formed here, not hoisted out of the tile loop.
+      int ccol = lane & 31;
+      int crow = (lane >> 5) * 4;
+      asm volatile("" : "+v"(ccol), "+v"(crow));
+      // wave's rows: 32-row blocks (rbase / 32) + mi
+      auto write_rows = [&](auto b0_c) {
+        constexpr int B0 = decltype(b0_c)::value;
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi) {
+        for (int mi = 0; mi < MI; ++mi) {
+          uint16_t* const base = mi == 0 ? stage_of(std::integral_constant<int, B0>{})
+                               : mi == 1 ? stage_of(std::integral_constant<int, B0 + 1>{})
+                               : mi == 2 ? stage_of(std::integral_constant<int, (B0 + 2) % 8>{})
+                                         : stage_of(std::integral_constant<int, (B0 + 3) % 8>{});
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const int dr = mi * 32 + 8 * (q >> 2) + (q & 3);
-          if (r_lane + dr >= nrows) continue;
-          uint16_t* const c_row = c_lane + dr * ld;
-          if (EPI == 0) {
+          for (int q = 0; q < 16; ++q) {
+            const int r = 8 * (q >> 2) + crow + (q & 3);
+            if (EPI == 0) {
 #pragma unroll
-            for (int p = 0; p < NI / 2; ++p) {
-              const int fc = cbase / 2 + p * 32;
-              if (n0 + fc + ccol < F) {
+              for (int p = 0; p < NI / 2; ++p) {
                 const float g = acc[mi][2 * p][q];
                 const float u = acc[mi][2 * p + 1][q];
-                c_row[fc] = f32_to_bf16(g / (1.f + expf(-g)) * u);
+                base[off_in(r, cbase / 2 + p * 32 + ccol)] = f32_to_bf16(swiglu(g, u));
               }
-            }
-          } else {
+            } else {
 #pragma unroll
-            for (int ni = 0; ni < NI; ++ni) {
-              const int hc = cbase + ni * 32;
-              if (n0 + hc + ccol < H) c_row[hc] = f32_to_bf16(acc[mi][ni][q]);
+              for (int ni = 0; ni < NI; ++ni)
+                base[off_in(r, cbase + ni * 32 + ccol)] = f32_to_bf16(acc[mi][ni][q]);
             }
           }
         }
+      };
+      if (FULL && (wave >> 1)) write_rows(std::integral_constant<int, 4>{});
+      else write_rows(std::integral_constant<int, 0>{});
+      __syncthreads();
+      // Rows of the tile that hold results: all 256 in a full tile, MI * 32
+      // when the waves sit side by side.
+      constexpr int CPRO = NOUT / 8;                    // 16-byte chunks per output row
+      const int rows_here = min(nrows, FULL ? BM : MI * 32);
+      int64_t ld = ldc;
+      asm volatile("" : "+s"(ld));
+      int tid_o = tid;
+      asm volatile("" : "+v"(tid_o));
+      auto store_block = [&](auto b_c) {
+        constexpr int b = decltype(b_c)::value;
+        const uint16_t* const base = stage_of(b_c);
+#pragma unroll
+        for (int qd0 = 0; qd0 < 32 * CPRO; qd0 += fast::kThreads) {
+          const int qd = qd0 + tid_o;
+          const int r = qd / CPRO, ch = qd - r * CPRO;
+          if (b * 32 + r < rows_here && n0 + ch * 8 < N_out) {
+            const uint4 v = *reinterpret_cast<const uint4*>(base + off_in(r, ch * 8));
+            *reinterpret_cast<uint4*>(C + (row0 + b * 32 + r) * ld + n0 + ch * 8) = v;
+          }
+        }
+      };
+      store_block(std::integral_constant<int, 0>{});
+      store_block(std::integral_constant<int, 1>{});
+      store_block(std::integral_constant<int, 2>{});
+      store_block(std::integral_constant<int, 3>{});
+      if (FULL) {
+        store_block(std::integral_constant<int, 4>{});
+        store_block(std::integral_constant<int, 5>{});
+        store_block(std::integral_constant<int, 6>{});
+        store_block(std::integral_constant<int, 7>{});
       }
     };
     if (nrows > 128) run(std::integral_constant<int, 0>{});
