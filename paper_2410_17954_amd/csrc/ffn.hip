@@ -283,9 +283,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 // lane fetches. A ring of four LDS stages keeps three K-steps of loads in
 // flight. Within a step the second half-step's fragments are read while the
 // first half's MFMAs run, then one barrier, then the next step's first
-// fragments are read while the second half's MFMAs run; the A loads of a
-// later step are spread over the first half and its B loads over the second,
-// so the memory pipe never stalls MFMA issue for long.
+// fragments are read while the second half's MFMAs run. In each half the
+// eight fragment reads go out within the first four MFMAs (so they have
+// landed before the half ends) and the DMA of a later step (A pieces in the
+// first half, B pieces in the second) is spread over the remaining twelve.
 // A tile whose expert has at most 128 rows left is computed by all 4 waves
 // side by side (each 32, 64 or 128 rows x 64 columns), so a ragged last row
 // tile costs in proportion to its rows, on every SIMD.
@@ -557,12 +558,13 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         }
         // outstanding after step kt+1: A,B of kt+2 and A of kt+3
         wait_vmcnt<3 * PPW>();
@@ -573,12 +575,13 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
           __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
         }
       };
 
