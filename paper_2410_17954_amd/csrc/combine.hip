@@ -1,11 +1,16 @@
 // moe_combine: gate-weighted sum of expert outputs per token (Sec. 2.1), over
 // experts resident in the expert cache, plus always-on shared experts.
 //
-// One wavefront per batch token. The token's k (row, weight, resident) triples
-// are staged in LDS; each lane then owns 8 consecutive features at a time
-// (16-byte bf16 vectors) and accumulates in float32 in ascending choice order,
-// adds the shared-expert row and, in accumulate mode, the existing output,
-// and rounds once.
+// One wavefront per batch token; each lane owns 8 consecutive features at a
+// time (16-byte bf16 vectors) and accumulates in float32 in ascending choice
+// order, adds the shared-expert row and, in accumulate mode, the existing
+// output, and rounds once.
+// bf16 with k <= 8 (combine_bf16_kernel): lane j loads choice j's row index
+// first, so the loads of the rows start while the token -> expert -> slot
+// chain that decides residency is still in flight (rows of missed experts
+// are read but not used); each round issues 8 row loads per lane (k choices x
+// 8/k feature groups) before accumulating. Other cases (combine_kernel) stage
+// the choices in LDS and walk the features one group at a time.
 #include "common.h"
 
 namespace moe {
@@ -141,6 +146,85 @@ combine_kernel(CombArgs a) {
   }
 }
 
+template <int KB>
+__global__ void __launch_bounds__(kCombWaves * kWave)
+combine_bf16_kernel(CombArgs a) {
+  constexpr int CU = 8 / KB;                      // feature groups per round
+  const int wave = threadIdx.x / kWave;
+  const int lane = lane_id();
+  const int64_t i = (int64_t)blockIdx.x * kCombWaves + wave;
+  if (i >= a.T) return;                           // whole wave
+  const int k = a.k;
+  const int32_t r_l = lane < k ? a.row_of_pair[i * k + lane] : -1;
+  int64_t t = a.token_ids ? (int64_t)a.token_ids[i] : i;
+  const bool active = t >= 0 && t < a.n_tokens;
+  if (!active) t = 0;
+  int e_l = -1;
+  float w_l = 0.f;
+  bool res_l = false;
+  if (active && lane < k) {
+    e_l = a.idx[t * k + lane];
+    w_l = a.w[t * k + lane];
+    res_l = a.slot ? (e_l >= 0 && e_l < a.E && a.slot[e_l] >= 0) : true;
+  }
+  const bool ok_l = res_l && r_l >= 0 && r_l < a.rows;
+  const bool missing = ballot(active && lane < k && !res_l) != 0;
+  if (active && lane == 0 && a.incomplete) a.incomplete[i] = missing ? 1 : 0;
+  if (!active) return;
+  int32_t rj[KB];
+  float wj[KB];
+  bool okj[KB];
+#pragma unroll
+  for (int j = 0; j < KB; ++j) {
+    rj[j] = __shfl(r_l, j, kWave);
+    wj[j] = __shfl(w_l, j, kWave);
+    okj[j] = j < k && __shfl(ok_l ? 1 : 0, j, kWave) != 0;
+    if (!(j < k && rj[j] >= 0 && rj[j] < a.rows)) rj[j] = -1;
+  }
+  const int64_t H = a.H, G = H / 8;
+  const uint16_t* yp = static_cast<const uint16_t*>(a.y_perm);
+  for (int64_t g0 = 0; g0 < G; g0 += (int64_t)kWave * CU) {
+    uint4 v[KB][CU];
+#pragma unroll
+    for (int j = 0; j < KB; ++j)
+#pragma unroll
+      for (int c = 0; c < CU; ++c) {
+        const int64_t g = g0 + c * kWave + lane;
+        v[j][c] = (rj[j] >= 0 && g < G) ? *reinterpret_cast<const uint4*>(yp + (int64_t)rj[j] * H + g * 8)
+                                        : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+    for (int c = 0; c < CU; ++c) {
+      const int64_t g = g0 + c * kWave + lane;
+      if (g >= G) continue;
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < KB; ++j) {
+        if (!okj[j]) continue;
+        const uint32_t u[4] = {v[j][c].x, v[j][c].y, v[j][c].z, v[j][c].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[2 * q] = fmaf(wj[j], __uint_as_float(u[q] << 16), acc[2 * q]);
+          acc[2 * q + 1] = fmaf(wj[j], __uint_as_float(u[q] & 0xffff0000u), acc[2 * q + 1]);
+        }
+      }
+      if (a.y_shared) {
+        float sv[8];
+        load8<true>(a.y_shared, i * H + g * 8, sv);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] += sv[q];
+      }
+      if (a.accumulate) {
+        float yv[8];
+        load8<true>(a.y, t * H + g * 8, yv);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] += yv[q];
+      }
+      store8<true>(a.y, t * H + g * 8, acc);
+    }
+  }
+}
+
 }  // namespace
 }  // namespace moe
 
@@ -164,7 +248,12 @@ extern "C" int moe_combine(const void* y_perm, int32_t dtype, int64_t H, int64_t
   CombArgs a{y_perm, H, rows, token_ids, T, n_tokens, k, topk_idx, topk_w, row_of_pair,
              slot_of_expert, E, y_shared, accumulate, y, incomplete};
   hipStream_t st = as_stream(stream);
-  if (dtype == MOE_BF16)
+  if (dtype == MOE_BF16 && k <= 8) {
+    const dim3 g((unsigned)blocks), b(kCombWaves * kWave);
+    if (k <= 2) combine_bf16_kernel<2><<<g, b, 0, st>>>(a);
+    else if (k <= 4) combine_bf16_kernel<4><<<g, b, 0, st>>>(a);
+    else combine_bf16_kernel<8><<<g, b, 0, st>>>(a);
+  } else if (dtype == MOE_BF16)
     combine_kernel<true><<<dim3((unsigned)blocks), dim3(kCombWaves * kWave), 0, st>>>(a);
   else
     combine_kernel<false><<<dim3((unsigned)blocks), dim3(kCombWaves * kWave), 0, st>>>(a);

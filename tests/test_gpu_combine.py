@@ -32,7 +32,9 @@ def _elementwise_ok(got, ref, k, w):
     assert rel_max_err(got, ref) <= 1e-2
 
 
-@pytest.mark.parametrize("T,E,k,H", [(1, 4, 1, 8), (77, 8, 2, 128), (2048, 64, 6, 256)])
+@pytest.mark.parametrize("T,E,k,H", [(1, 4, 1, 8), (77, 8, 2, 128), (2048, 64, 6, 256),
+                                     (300, 64, 12, 64),      # k > 8: the general kernel
+                                     (4096, 8, 2, 4096)])    # Mixtral batch
 def test_all_resident(T, E, k, H):
     idx, w, rop, yp, _, _ = _inputs(T, T, E, k, H, seed=T)
     y, inc = ops.combine(to_dev(yp), to_dev(idx), to_dev(w), to_dev(rop))
