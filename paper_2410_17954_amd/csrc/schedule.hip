@@ -8,8 +8,10 @@
 //   order    signature order: ascending per-layer expert ids, layer 0 first,
 //            then token index. For two paths with the same number of ids per
 //            layer, a precedes b iff the lowest bit where they differ is set in
-//            a, so the order is decided word by word on the packed paths. The
-//            rank of each token is counted in parallel over (i, j-tile) pairs.
+//            a, so the order is decided word by word on the packed paths: first
+//            by counting, for every token, the tokens whose (first word, index)
+//            precede its own, then by re-ranking each run of equal first words
+//            on the remaining words.
 //   init     m1 = argmin_i sum_j d_ij over all tokens, m2 = argmax_i d(i, m1)
 //   iterate  delta_i = d(i,m1) - d(i,m2) and its histogram; the threshold
 //            delta* where the count reaches n1; batch 1 = delta < delta* plus
@@ -19,8 +21,8 @@
 //            a device-side flag stops the remaining rounds once they settle
 //   finish   Eq. 2 before/after from the column counts, the optional guard,
 //            perm by stable compaction, demand, info.
-// All ties go to the lower signature rank. The launch sequence is fixed
-// (12 + 5 * max_iters launches); nothing is read back to the host.
+// All ties go to the lower signature rank. The launch sequence depends only
+// on the shapes and max_iters; nothing is read back to the host.
 #include "common.h"
 
 #include <algorithm>
@@ -30,7 +32,6 @@ namespace {
 
 constexpr int kT = 256;          // threads of grid-parallel kernels
 constexpr int kSel = 1024;       // threads of single-block kernels
-constexpr int kRankTile = 1024;  // j-tile of the rank count
 
 // state words
 enum {
@@ -102,63 +103,157 @@ __device__ __forceinline__ uint64_t lowbit(uint64_t d) { return d & (0ull - d); 
 // ---------------------------------------------------------------- kernels
 __global__ void __launch_bounds__(kT)
 sch_pack(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
-         uint64_t* __restrict__ bits, uint64_t* __restrict__ bits_t, int32_t* __restrict__ ones,
-         int32_t* __restrict__ rank) {
+         uint64_t* __restrict__ bits, uint64_t* __restrict__ bits_t, uint64_t* __restrict__ key0,
+         int32_t* __restrict__ ones) {
   const int i = blockIdx.x * kT + threadIdx.x;
   if (i >= N) return;
-  rank[i] = 0;
-  uint64_t* b = bits + (int64_t)i * W;
-  for (int w = 0; w < W; ++w) b[w] = 0;
+  const int LE = L * E;
   const uint8_t* r = routes + (int64_t)i * L * k;
-  for (int l = 0; l < L; ++l)
-    for (int j = 0; j < k; ++j) {
-      const int e = r[l * k + j];
-      if (e < E) {
-        const int64_t bit = (int64_t)l * E + e;
-        b[bit >> 6] |= 1ull << (bit & 63);
-      }
-    }
+  uint64_t* b = bits + (int64_t)i * W;
   int c = 0;
+  // Word w holds bits [64w, 64w + 64): only the layers that overlap it are read.
   for (int w = 0; w < W; ++w) {
-    c += __popcll(b[w]);
-    bits_t[(int64_t)w * N + i] = b[w];          // word-major copy: coalesced per word
+    const int lo = w * 64, hi = min(lo + 64, LE);
+    uint64_t word = 0;
+    for (int l = lo / E; l * E < hi; ++l)
+      for (int j = 0; j < k; ++j) {
+        const int e = r[l * k + j];
+        const int bit = l * E + e - lo;
+        if (e < E && bit >= 0 && bit < 64) word |= 1ull << bit;
+      }
+    b[w] = word;
+    bits_t[(int64_t)w * N + i] = word;          // word-major copy: coalesced per word
+    c += __popcll(word);
+    // Signature order on the first word alone is ascending order of the
+    // complemented bit reversal: the lowest differing bit becomes the highest.
+    if (w == 0) key0[i] = ~__builtin_bitreverse64(word);
   }
   ones[i] = c;
 }
 
-// rank[i] += #{j in this tile : j precedes i in signature order}
+// Signature rank, first level: part[t][i] = #{j in j-tile t : (key0_j, j) <
+// (key0_i, i)}. The j-keys are uniform across the wave (scalar loads), so a
+// pair costs one 64-bit compare and one add with carry; the index tie-break
+// is uniform per tile except on the tile that overlaps the block's own rows.
 __global__ void __launch_bounds__(kT)
-sch_rank(const uint64_t* __restrict__ bits, int N, int W, int32_t* __restrict__ rank) {
-  __shared__ uint64_t s_w0[kRankTile];
-  const int j0 = blockIdx.y * kRankTile;
-  const int jn = min(kRankTile, N - j0);
-  for (int q = threadIdx.x; q < jn; q += kT) s_w0[q] = bits[(int64_t)(j0 + q) * W];
-  __syncthreads();
+sch_rank_first(const uint64_t* __restrict__ key0, int N, int tile, int32_t* __restrict__ part) {
   const int i = blockIdx.x * kT + threadIdx.x;
-  if (i >= N) return;
-  const uint64_t wi = bits[(int64_t)i * W];
+  const int j0 = blockIdx.y * tile;
+  const int jn = min(tile, N - j0);
+  const int ib0 = blockIdx.x * kT, ib1 = min(N, ib0 + kT) - 1;
+  const uint64_t ki = i < N ? key0[i] : 0ull;
+  const uint64_t* kj = key0 + j0;
   int cnt = 0;
-  for (int q = 0; q < jn; ++q) {
-    const uint64_t wj = s_w0[q];
-    const uint64_t d = wi ^ wj;
-    if (d) {
-      cnt += (wj & lowbit(d)) != 0;
-    } else {
-      const int j = j0 + q;
-      if (j == i) continue;
-      int before = j < i;
-      for (int w = 1; w < W; ++w) {
-        const uint64_t a = bits[(int64_t)j * W + w];
-        const uint64_t dd = a ^ bits[(int64_t)i * W + w];
-        if (dd) {
-          before = (a & lowbit(dd)) != 0;
-          break;
-        }
-      }
-      cnt += before;
+  if (j0 + jn - 1 < ib0) {                          // every j < every i: ties count
+    int q = 0;
+    for (; q + 16 <= jn; q += 16)
+#pragma unroll
+      for (int u = 0; u < 16; ++u) cnt += kj[q + u] <= ki;
+    for (; q < jn; ++q) cnt += kj[q] <= ki;
+  } else if (j0 > ib1) {                            // every j > every i: ties do not
+    int q = 0;
+    for (; q + 16 <= jn; q += 16)
+#pragma unroll
+      for (int u = 0; u < 16; ++u) cnt += kj[q + u] < ki;
+    for (; q < jn; ++q) cnt += kj[q] < ki;
+  } else {
+    for (int q = 0; q < jn; ++q) {
+      const uint64_t a = kj[q];
+      cnt += a < ki || (a == ki && j0 + q < i);
     }
   }
-  atomicAdd(&rank[i], cnt);
+  if (i < N) part[(int64_t)blockIdx.y * N + i] = cnt;
+}
+
+// rank[i] = sum of the tile counts; order1[rank[i]] = i.
+__global__ void __launch_bounds__(kT)
+sch_order_first(const int32_t* __restrict__ part, int ntiles, int N, int32_t* __restrict__ rank,
+                int32_t* __restrict__ order1) {
+  const int i = blockIdx.x * kT + threadIdx.x;
+  if (i >= N) return;
+  int r = 0;
+  for (int t = 0; t < ntiles; ++t) r += part[(int64_t)t * N + i];
+  rank[i] = r;
+  order1[r] = i;
+}
+
+// Runs of equal first words in first-level order: gs[p] / ge[p] = first / last
+// position of the run holding position p. One block; each thread walks a
+// contiguous chunk and the chunk boundaries are joined by block scans.
+__global__ void __launch_bounds__(kSel)
+sch_tie_runs(const uint64_t* __restrict__ key0, const int32_t* __restrict__ order1, int N,
+             int32_t* __restrict__ gs, int32_t* __restrict__ ge) {
+  __shared__ int s_a[kSel];
+  const int tid = threadIdx.x;
+  const int per = (N + kSel - 1) / kSel;
+  const int p0 = min(N, tid * per), p1 = min(N, p0 + per);
+  auto key = [&](int p) { return key0[order1[p]]; };
+  // last run start inside the chunk
+  int last = -1;
+  for (int p = p0; p < p1; ++p)
+    if (p == 0 || key(p) != key(p - 1)) last = p;
+  s_a[tid] = last;
+  __syncthreads();
+  for (int o = 1; o < kSel; o <<= 1) {              // inclusive max-scan
+    const int v = tid >= o ? s_a[tid - o] : -1;
+    __syncthreads();
+    s_a[tid] = max(s_a[tid], v);
+    __syncthreads();
+  }
+  int cur = tid > 0 ? s_a[tid - 1] : -1;
+  for (int p = p0; p < p1; ++p) {
+    if (p == 0 || key(p) != key(p - 1)) cur = p;
+    gs[p] = cur;
+  }
+  __syncthreads();
+  // first run end inside the chunk
+  int first = N;
+  for (int p = p1 - 1; p >= p0; --p)
+    if (p == N - 1 || key(p) != key(p + 1)) first = p;
+  s_a[tid] = first;
+  __syncthreads();
+  for (int o = 1; o < kSel; o <<= 1) {              // inclusive min-scan from the right
+    const int v = tid + o < kSel ? s_a[tid + o] : N;
+    __syncthreads();
+    s_a[tid] = min(s_a[tid], v);
+    __syncthreads();
+  }
+  cur = tid + 1 < kSel ? s_a[tid + 1] : N;
+  for (int p = p1 - 1; p >= p0; --p) {
+    if (p == N - 1 || key(p) != key(p + 1)) cur = p;
+    ge[p] = cur;
+  }
+}
+
+// Second level: inside a run of equal first words the remaining words (then
+// the token index) decide; rank[i] = run start + #{run members before i}.
+__global__ void __launch_bounds__(kT)
+sch_rank_ties(const uint64_t* __restrict__ bits, int N, int W, const int32_t* __restrict__ order1,
+              const int32_t* __restrict__ gs, const int32_t* __restrict__ ge,
+              int32_t* __restrict__ rank) {
+  const int p = blockIdx.x * kT + threadIdx.x;
+  if (p >= N) return;
+  const int s = gs[p], e = ge[p];
+  if (s == e) return;
+  const int i = order1[p];
+  const uint64_t* bi = bits + (int64_t)i * W;
+  int cnt = 0;
+  for (int m = s; m <= e; ++m) {
+    if (m == p) continue;
+    const int j = order1[m];
+    const uint64_t* bj = bits + (int64_t)j * W;
+    int before = j < i;
+    for (int w = 1; w < W; ++w) {
+      const uint64_t a = bj[w];
+      const uint64_t d = a ^ bi[w];
+      if (d) {
+        before = (a & lowbit(d)) != 0;
+        break;
+      }
+    }
+    cnt += before;
+  }
+  rank[i] = s + cnt;
 }
 
 __global__ void __launch_bounds__(kT)
@@ -400,48 +495,6 @@ sch_finish(int N, int n1, int L, int E, int keep_if_worse, int trivial,
     info[6] = (!trivial && use_orig) ? 1 : 0;
     info[7] = n1;
   }
-}
-
-// ------------------------------------------------ rank with keys in LDS
-// Same count as sch_rank, with the whole key of every token of the j-tile
-// staged in LDS and token i's key in registers (W <= WMAX words), so equal
-// leading words never go back to global memory.
-template <int WMAX>
-__global__ void __launch_bounds__(kT)
-sch_rank_keys(const uint64_t* __restrict__ bits, int N, int W, int tile,
-              int32_t* __restrict__ rank) {
-  extern __shared__ uint64_t s_keys[];          // [tile][W]
-  const int j0 = blockIdx.y * tile;
-  const int jn = min(tile, N - j0);
-  for (int q = threadIdx.x; q < jn * W; q += kT) s_keys[q] = bits[(int64_t)j0 * W + q];
-  __syncthreads();
-  const int i = blockIdx.x * kT + threadIdx.x;
-  if (i >= N) return;
-  uint64_t ki[WMAX];
-#pragma unroll
-  for (int w = 0; w < WMAX; ++w) ki[w] = (w < W) ? bits[(int64_t)i * W + w] : 0ull;
-  // Most pairs differ in their first word; the remaining words are compared
-  // only on a tie there (all still in LDS / registers).
-  auto before = [&](int q) -> int {
-    const uint64_t* kj = s_keys + q * W;
-    const uint64_t a0 = kj[0];
-    const uint64_t d0 = a0 ^ ki[0];
-    if (d0) return (a0 & lowbit(d0)) != 0;
-#pragma unroll
-    for (int w = 1; w < WMAX; ++w) {
-      if (w < W) {
-        const uint64_t a = kj[w];
-        const uint64_t d = a ^ ki[w];
-        if (d) return (a & lowbit(d)) != 0;
-      }
-    }
-    return (j0 + q) < i;                          // equal keys: index order; j == i adds 0
-  };
-  int cnt = 0;
-  int q = 0;
-  for (; q + 4 <= jn; q += 4) cnt += before(q) + before(q + 1) + before(q + 2) + before(q + 3);
-  for (; q < jn; ++q) cnt += before(q);
-  atomicAdd(&rank[i], cnt);
 }
 
 // ------------------------------------------------ cooperative round loop
@@ -755,9 +808,22 @@ sch_init(int32_t* __restrict__ hist, int nbins, int32_t* __restrict__ cnt_orig, 
 }
 
 struct SchLayout {
-  size_t bits, bits_t, ones, rank, order, delta, in1, cnt, cnt_orig, hist, tot, state, cand,
-      cand2, tiecnt, bar, total;
+  size_t bits, bits_t, key0, ones, rank, part, order1, runs, order, delta, in1, cnt, cnt_orig,
+      hist, tot, state, cand, cand2, tiecnt, bar, total;
 };
+
+// j-tiling of the first-level rank: about 2048 blocks in all, tiles of a
+// multiple of 64 tokens.
+struct RankTiles {
+  int tile, ntiles;
+};
+
+RankTiles rank_tiles(int64_t N) {
+  const int64_t nbi = ceil_div(N, kT);
+  const int64_t want = std::max<int64_t>(1, std::min<int64_t>(64, 2048 / nbi));
+  const int64_t tile = align_up(ceil_div(N, want), 64);
+  return RankTiles{(int)tile, (int)ceil_div(N, tile)};
+}
 
 SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
   const int64_t W = ((int64_t)L * E + 63) / 64;
@@ -773,8 +839,12 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
   };
   s.bits = take(N * W * 8);
   s.bits_t = take(N * W * 8);
+  s.key0 = take(N * 8);
   s.ones = take(N * 4);
   s.rank = take(N * 4);
+  s.part = take((size_t)rank_tiles(N).ntiles * N * 4);
+  s.order1 = take(N * 4);
+  s.runs = take(2 * N * 4);
   s.order = take(N * 4);
   s.delta = take(N * 4);
   s.in1 = take(N * 4);
@@ -817,6 +887,11 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   char* ws = static_cast<char*>(workspace);
   auto* bits = reinterpret_cast<uint64_t*>(ws + lay.bits);
   auto* bits_t = reinterpret_cast<uint64_t*>(ws + lay.bits_t);
+  auto* key0 = reinterpret_cast<uint64_t*>(ws + lay.key0);
+  auto* part = reinterpret_cast<int32_t*>(ws + lay.part);
+  auto* order1 = reinterpret_cast<int32_t*>(ws + lay.order1);
+  auto* run_s = reinterpret_cast<int32_t*>(ws + lay.runs);
+  auto* run_e = run_s + N;
   auto* ones = reinterpret_cast<int32_t*>(ws + lay.ones);
   auto* rank = reinterpret_cast<int32_t*>(ws + lay.rank);
   auto* order = reinterpret_cast<int32_t*>(ws + lay.order);
@@ -847,23 +922,25 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   sch_init<<<dim3((unsigned)std::min<int64_t>(64, ceil_div(std::max(nbins, 2 * LE), kT))), blk, 0,
              st>>>(hist, nbins, cnt_orig, 2 * LE, tot, cand2, bar, err, state);
   MOE_CHECK_LAUNCH();
-  sch_pack<<<grid, blk, 0, st>>>(routes, n, L, E, k, W, bits, bits_t, ones, rank);
+  sch_pack<<<grid, blk, 0, st>>>(routes, n, L, E, k, W, bits, bits_t, key0, ones);
   MOE_CHECK_LAUNCH();
+  // Signature order: (first word, index) by counting, then runs of equal
+  // first words re-ranked on the remaining words.
   auto launch_rank = [&]() -> int {
-    if (W <= 32) {
-      const int tile = std::min(256, 65536 / (8 * W));
-      const dim3 g2(nblk, (unsigned)ceil_div(N, tile));
-      const size_t lds = (size_t)tile * W * sizeof(uint64_t);
-      if (W <= 4) sch_rank_keys<4><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
-      else if (W <= 8) sch_rank_keys<8><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
-      else if (W <= 16) sch_rank_keys<16><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
-      else sch_rank_keys<32><<<g2, blk, lds, st>>>(bits, n, W, tile, rank);
-    } else {
-      sch_rank<<<dim3(nblk, (unsigned)ceil_div(N, kRankTile)), blk, 0, st>>>(bits, n, W, rank);
-    }
+    const RankTiles rt = rank_tiles(N);
+    sch_rank_first<<<dim3(nblk, rt.ntiles), blk, 0, st>>>(key0, n, rt.tile, part);
     if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
-    sch_order<<<grid, blk, 0, st>>>(rank, n, order);
-    return hipGetLastError() != hipSuccess ? MOE_ERR_HIP : MOE_OK;
+    sch_order_first<<<grid, blk, 0, st>>>(part, rt.ntiles, n, rank, W > 1 ? order1 : order);
+    if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
+    if (W > 1) {
+      sch_tie_runs<<<dim3(1), dim3(kSel), 0, st>>>(key0, order1, n, run_s, run_e);
+      if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
+      sch_rank_ties<<<grid, blk, 0, st>>>(bits, n, W, order1, run_s, run_e, rank);
+      if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
+      sch_order<<<grid, blk, 0, st>>>(rank, n, order);
+      if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
+    }
+    return MOE_OK;
   };
 
   bool done = false;

@@ -84,3 +84,19 @@ def test_iteration_limit_and_no_guard():
 def test_k_equals_E():
     routes = np.tile(np.arange(4, dtype=np.uint8), (50, 2, 1))
     _check(routes, 4)
+
+
+def test_first_word_ties_resolved_on_later_words():
+    # With E = 64 the first path word is exactly layer 0: making layer 0 equal
+    # for every token puts all of them in one run that the later words decide.
+    routes = synth.predicted_routes(3000, 5, 64, 2, 0.7, 1.0, seed=31)
+    routes[:, 0, :] = routes[0, 0, :]
+    _check(routes, 64)
+
+
+def test_repeated_multiword_paths():
+    # 40 distinct paths of 3 words, each repeated many times: equal keys are
+    # ordered by token index.
+    base = synth.predicted_routes(40, 4, 40, 3, 0.5, 1.0, seed=32)
+    pick = np.random.default_rng(33).integers(0, 40, size=2000)
+    _check(base[pick], 40)
