@@ -8,21 +8,22 @@
 //   order    signature order: ascending per-layer expert ids, layer 0 first,
 //            then token index. For two paths with the same number of ids per
 //            layer, a precedes b iff the lowest bit where they differ is set in
-//            a, so the order is decided word by word on the packed paths: first
-//            by counting, for every token, the tokens whose (first word, index)
-//            precede its own, then by re-ranking each run of equal first words
-//            on the remaining words.
+//            a, which for one word is descending order of its bit reversal.
+//            Chunks of 2048 tokens are sorted in LDS (bitonic) on the first two
+//            words, later words and the index deciding ties; the signature rank
+//            of a token is the sum of its lower bounds in every sorted chunk.
 //   init     m1 = argmin_i sum_j d_ij over all tokens, m2 = argmax_i d(i, m1)
 //   iterate  delta_i = d(i,m1) - d(i,m2) and its histogram; the threshold
 //            delta* where the count reaches n1; batch 1 = delta < delta* plus
 //            the first tokens at delta* in signature order; per-batch column
 //            counts c_b; sum_{j in C} d_ij = |C| |r_i| + sum_j |r_j|
-//            - 2 sum_{b in r_i} c_b; per-batch argmin -> new centroids;
-//            a device-side flag stops the remaining rounds once they settle
+//            - 2 sum_{b in r_i} c_b; per-batch argmin -> new centroids, until
+//            they repeat or max_iters rounds
 //   finish   Eq. 2 before/after from the column counts, the optional guard,
 //            perm by stable compaction, demand, info.
-// All ties go to the lower signature rank. The launch sequence depends only
-// on the shapes and max_iters; nothing is read back to the host.
+// All ties go to the lower signature rank. The rounds run in one cooperative
+// launch over tokens laid out in signature order (a per-phase launch sequence
+// covers shapes beyond its limits); nothing is read back to the host.
 #include "common.h"
 
 #include <algorithm>
@@ -31,11 +32,17 @@ namespace moe {
 namespace {
 
 constexpr int kT = 256;          // threads of grid-parallel kernels
-constexpr int kSel = 1024;       // threads of single-block kernels
+constexpr int kSel = 1024;       // threads of single-block and finish kernels
+constexpr int kPackT = 64;       // tokens per pack block
+constexpr int kPackMaxBytes = 16384;  // route bytes a pack block stages in LDS
+constexpr int kChunk = 2048;     // tokens per sorted chunk
+constexpr int kSortT = 1024;     // threads of the chunk sort and merge-rank blocks
+constexpr int kMaxRankGroups = 16;    // chunk groups of the merge rank
 
 // state words
 enum {
-  ST_M1 = 0, ST_M2, ST_DONE, ST_ITERS, ST_CONV, ST_AM1, ST_AM2, ST_TOT0, ST_TOT1, ST_NWORDS = 16
+  ST_M1 = 0, ST_M2, ST_DONE, ST_ITERS, ST_CONV, ST_AM1, ST_AM2, ST_USE_ORIG, ST_BEFORE,
+  ST_AFTER, ST_NWORDS = 16
 };
 
 struct Cand {
@@ -101,17 +108,39 @@ __device__ int block_excl_scan(int v, int* total) {
 __device__ __forceinline__ uint64_t lowbit(uint64_t d) { return d & (0ull - d); }
 
 // ---------------------------------------------------------------- kernels
-__global__ void __launch_bounds__(kT)
+// Packs kPackT tokens per block: their routes are staged in LDS with
+// coalesced loads when they fit, each token's words are built in registers
+// (only the layers overlapping a word are read for it) and written row-major.
+// key0 / key1 are the sort keys of the first two words (0 when W == 1).
+__global__ void __launch_bounds__(kPackT)
 sch_pack(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
-         uint64_t* __restrict__ bits, uint64_t* __restrict__ bits_t, uint64_t* __restrict__ key0,
+         uint64_t* __restrict__ bits, uint64_t* __restrict__ key0, uint64_t* __restrict__ key1,
          int32_t* __restrict__ ones) {
-  const int i = blockIdx.x * kT + threadIdx.x;
-  if (i >= N) return;
-  const int LE = L * E;
-  const uint8_t* r = routes + (int64_t)i * L * k;
+  __shared__ uint8_t s_r[kPackMaxBytes];
+  const int Lk = L * k, LE = L * E;
+  const int t0 = blockIdx.x * kPackT;
+  const int nt = min(kPackT, N - t0);
+  const uint8_t* src = routes + (int64_t)t0 * Lk;
+  const bool staged = kPackT * Lk <= kPackMaxBytes;
+  if (staged) {
+    const int nbytes = nt * Lk;
+    int q0 = 0;
+    if ((reinterpret_cast<uintptr_t>(src) & 3) == 0) {
+      const uint32_t* s4 = reinterpret_cast<const uint32_t*>(src);
+      uint32_t* d4 = reinterpret_cast<uint32_t*>(s_r);
+      for (int q = threadIdx.x; q < nbytes / 4; q += kPackT) d4[q] = s4[q];
+      q0 = nbytes & ~3;
+    }
+    for (int q = q0 + threadIdx.x; q < nbytes; q += kPackT) s_r[q] = src[q];
+    __syncthreads();
+  }
+  const int t = threadIdx.x;
+  if (t >= nt) return;
+  const int i = t0 + t;
+  const uint8_t* r = staged ? s_r + t * Lk : src + (int64_t)t * Lk;
   uint64_t* b = bits + (int64_t)i * W;
+  uint64_t k0 = 0, k1 = 0;
   int c = 0;
-  // Word w holds bits [64w, 64w + 64): only the layers that overlap it are read.
   for (int w = 0; w < W; ++w) {
     const int lo = w * 64, hi = min(lo + 64, LE);
     uint64_t word = 0;
@@ -122,146 +151,141 @@ sch_pack(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
         if (e < E && bit >= 0 && bit < 64) word |= 1ull << bit;
       }
     b[w] = word;
-    bits_t[(int64_t)w * N + i] = word;          // word-major copy: coalesced per word
     c += __popcll(word);
-    // Signature order on the first word alone is ascending order of the
-    // complemented bit reversal: the lowest differing bit becomes the highest.
-    if (w == 0) key0[i] = ~__builtin_bitreverse64(word);
+    if (w == 0) k0 = ~__builtin_bitreverse64(word);
+    if (w == 1) k1 = ~__builtin_bitreverse64(word);
   }
+  key0[i] = k0;
+  key1[i] = k1;
   ones[i] = c;
 }
 
-// Signature rank, first level: part[t][i] = #{j in j-tile t : (key0_j, j) <
-// (key0_i, i)}. The j-keys are uniform across the wave (scalar loads), so a
-// pair costs one 64-bit compare and one add with carry; the index tie-break
-// is uniform per tile except on the tile that overlaps the block's own rows.
-__global__ void __launch_bounds__(kT)
-sch_rank_first(const uint64_t* __restrict__ key0, int N, int tile, int32_t* __restrict__ part) {
-  const int i = blockIdx.x * kT + threadIdx.x;
-  const int j0 = blockIdx.y * tile;
-  const int jn = min(tile, N - j0);
-  const int ib0 = blockIdx.x * kT, ib1 = min(N, ib0 + kT) - 1;
-  const uint64_t ki = i < N ? key0[i] : 0ull;
-  const uint64_t* kj = key0 + j0;
+// (key0, key1, token) order; when the first two words agree, the later words
+// of the packed paths decide (lowest differing bit set first), then the token
+// index. Indices >= N are padding and compare by index alone.
+__device__ __forceinline__ bool key_less(uint64_t a0, uint64_t a1, int ia, uint64_t b0,
+                                         uint64_t b1, int ib, const uint64_t* __restrict__ bits,
+                                         int W, int N) {
+  if (a0 != b0) return a0 < b0;
+  if (a1 != b1) return a1 < b1;
+  if (W > 2 && ia < N && ib < N) {
+    const uint64_t* pa = bits + (int64_t)ia * W;
+    const uint64_t* pb = bits + (int64_t)ib * W;
+    for (int w = 2; w < W; ++w) {
+      const uint64_t a = pa[w];
+      const uint64_t d = a ^ pb[w];
+      if (d) return (a & lowbit(d)) != 0;
+    }
+  }
+  return ia < ib;
+}
+
+// Sorts each chunk of kChunk consecutive tokens by key_less (bitonic network
+// in LDS, one compare-exchange per thread and step; the tail chunk is padded
+// with keys that sort last).
+__global__ void __launch_bounds__(kSortT)
+sch_sort_chunks(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ key1,
+                const uint64_t* __restrict__ bits, int N, int W, uint64_t* __restrict__ s0,
+                uint64_t* __restrict__ s1, int32_t* __restrict__ sidx) {
+  static_assert(kChunk == 2 * kSortT, "one compare-exchange per thread and step");
+  __shared__ uint64_t a0[kChunk], a1[kChunk];
+  __shared__ int32_t ai[kChunk];
+  const int c0 = blockIdx.x * kChunk;
+  const int cn = min(kChunk, N - c0);
+  for (int p = threadIdx.x; p < kChunk; p += kSortT) {
+    const bool real = p < cn;
+    a0[p] = real ? key0[c0 + p] : ~0ull;
+    a1[p] = real ? key1[c0 + p] : ~0ull;
+    ai[p] = real ? c0 + p : INT32_MAX;
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  for (int kk = 2; kk <= kChunk; kk <<= 1) {
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      const int x = ((t & ~(j - 1)) << 1) | (t & (j - 1));   // bit j of x clear
+      const int y = x + j;
+      const bool up = (x & kk) == 0;
+      const uint64_t x0 = a0[x], x1 = a1[x], y0 = a0[y], y1 = a1[y];
+      const int xi = ai[x], yi = ai[y];
+      const bool y_first = key_less(y0, y1, yi, x0, x1, xi, bits, W, N);
+      if (y_first == up) {                         // pairs are disjoint within a step
+        a0[x] = y0; a1[x] = y1; ai[x] = yi;
+        a0[y] = x0; a1[y] = x1; ai[y] = xi;
+      }
+      __syncthreads();
+    }
+  }
+  for (int p = threadIdx.x; p < cn; p += kSortT) {
+    s0[c0 + p] = a0[p];
+    s1[c0 + p] = a1[p];
+    sidx[c0 + p] = ai[p];
+  }
+}
+
+// part[g][i] = #{tokens before i} summed over the sorted chunks of group g
+// (chunks g, g + G, g + 2G, ...): each chunk is staged in LDS and searched
+// with a branch-free lower bound.
+__global__ void __launch_bounds__(kSortT)
+sch_merge_rank(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ key1,
+               const uint64_t* __restrict__ bits, int N, int W, int nchunks,
+               const uint64_t* __restrict__ s0, const uint64_t* __restrict__ s1,
+               const int32_t* __restrict__ sidx, int32_t* __restrict__ part) {
+  __shared__ uint64_t a0[kChunk], a1[kChunk];
+  __shared__ int32_t ai[kChunk];
+  const int i = blockIdx.x * kSortT + threadIdx.x;
+  const uint64_t x0 = i < N ? key0[i] : 0ull, x1 = i < N ? key1[i] : 0ull;
   int cnt = 0;
-  if (j0 + jn - 1 < ib0) {                          // every j < every i: ties count
-    int q = 0;
-    for (; q + 16 <= jn; q += 16)
-#pragma unroll
-      for (int u = 0; u < 16; ++u) cnt += kj[q + u] <= ki;
-    for (; q < jn; ++q) cnt += kj[q] <= ki;
-  } else if (j0 > ib1) {                            // every j > every i: ties do not
-    int q = 0;
-    for (; q + 16 <= jn; q += 16)
-#pragma unroll
-      for (int u = 0; u < 16; ++u) cnt += kj[q + u] < ki;
-    for (; q < jn; ++q) cnt += kj[q] < ki;
-  } else {
-    for (int q = 0; q < jn; ++q) {
-      const uint64_t a = kj[q];
-      cnt += a < ki || (a == ki && j0 + q < i);
+  for (int c = blockIdx.y; c < nchunks; c += gridDim.y) {
+    const int c0 = c * kChunk;
+    const int cn = min(kChunk, N - c0);
+    __syncthreads();
+    for (int p = threadIdx.x; p < cn; p += kSortT) {
+      a0[p] = s0[c0 + p];
+      a1[p] = s1[c0 + p];
+      ai[p] = sidx[c0 + p];
+    }
+    __syncthreads();
+    if (i < N) {
+      int lo = 0;
+      for (int step = kChunk; step > 0; step >>= 1) {
+        const int m = lo + step - 1;
+        if (lo + step <= cn && key_less(a0[m], a1[m], ai[m], x0, x1, i, bits, W, N)) lo += step;
+      }
+      cnt += lo;
     }
   }
   if (i < N) part[(int64_t)blockIdx.y * N + i] = cnt;
 }
 
-// rank[i] = sum of the tile counts; order1[rank[i]] = i.
+// rank[i] = sum over groups; order[rank[i]] = i.
 __global__ void __launch_bounds__(kT)
-sch_order_first(const int32_t* __restrict__ part, int ntiles, int N, int32_t* __restrict__ rank,
-                int32_t* __restrict__ order1) {
+sch_rank_sum(const int32_t* __restrict__ part, int ngroups, int N, int32_t* __restrict__ rank,
+             int32_t* __restrict__ order) {
   const int i = blockIdx.x * kT + threadIdx.x;
   if (i >= N) return;
   int r = 0;
-  for (int t = 0; t < ntiles; ++t) r += part[(int64_t)t * N + i];
+  for (int g = 0; g < ngroups; ++g) r += part[(int64_t)g * N + i];
   rank[i] = r;
-  order1[r] = i;
+  if (r < N) order[r] = i;                        // always: the chunk counts add up to a permutation
 }
 
-// Runs of equal first words in first-level order: gs[p] / ge[p] = first / last
-// position of the run holding position p. One block; each thread walks a
-// contiguous chunk and the chunk boundaries are joined by block scans.
-__global__ void __launch_bounds__(kSel)
-sch_tie_runs(const uint64_t* __restrict__ key0, const int32_t* __restrict__ order1, int N,
-             int32_t* __restrict__ gs, int32_t* __restrict__ ge) {
-  __shared__ int s_a[kSel];
-  const int tid = threadIdx.x;
-  const int per = (N + kSel - 1) / kSel;
-  const int p0 = min(N, tid * per), p1 = min(N, p0 + per);
-  auto key = [&](int p) { return key0[order1[p]]; };
-  // last run start inside the chunk
-  int last = -1;
-  for (int p = p0; p < p1; ++p)
-    if (p == 0 || key(p) != key(p - 1)) last = p;
-  s_a[tid] = last;
-  __syncthreads();
-  for (int o = 1; o < kSel; o <<= 1) {              // inclusive max-scan
-    const int v = tid >= o ? s_a[tid - o] : -1;
-    __syncthreads();
-    s_a[tid] = max(s_a[tid], v);
-    __syncthreads();
-  }
-  int cur = tid > 0 ? s_a[tid - 1] : -1;
-  for (int p = p0; p < p1; ++p) {
-    if (p == 0 || key(p) != key(p - 1)) cur = p;
-    gs[p] = cur;
-  }
-  __syncthreads();
-  // first run end inside the chunk
-  int first = N;
-  for (int p = p1 - 1; p >= p0; --p)
-    if (p == N - 1 || key(p) != key(p + 1)) first = p;
-  s_a[tid] = first;
-  __syncthreads();
-  for (int o = 1; o < kSel; o <<= 1) {              // inclusive min-scan from the right
-    const int v = tid + o < kSel ? s_a[tid + o] : N;
-    __syncthreads();
-    s_a[tid] = min(s_a[tid], v);
-    __syncthreads();
-  }
-  cur = tid + 1 < kSel ? s_a[tid + 1] : N;
-  for (int p = p1 - 1; p >= p0; --p) {
-    if (p == N - 1 || key(p) != key(p + 1)) cur = p;
-    ge[p] = cur;
-  }
-}
-
-// Second level: inside a run of equal first words the remaining words (then
-// the token index) decide; rank[i] = run start + #{run members before i}.
+// Paths and path sizes in signature order, word-major: bits_s[w][r] is word w
+// of the token at signature position r.
 __global__ void __launch_bounds__(kT)
-sch_rank_ties(const uint64_t* __restrict__ bits, int N, int W, const int32_t* __restrict__ order1,
-              const int32_t* __restrict__ gs, const int32_t* __restrict__ ge,
-              int32_t* __restrict__ rank) {
-  const int p = blockIdx.x * kT + threadIdx.x;
-  if (p >= N) return;
-  const int s = gs[p], e = ge[p];
-  if (s == e) return;
-  const int i = order1[p];
-  const uint64_t* bi = bits + (int64_t)i * W;
-  int cnt = 0;
-  for (int m = s; m <= e; ++m) {
-    if (m == p) continue;
-    const int j = order1[m];
-    const uint64_t* bj = bits + (int64_t)j * W;
-    int before = j < i;
-    for (int w = 1; w < W; ++w) {
-      const uint64_t a = bj[w];
-      const uint64_t d = a ^ bi[w];
-      if (d) {
-        before = (a & lowbit(d)) != 0;
-        break;
-      }
-    }
-    cnt += before;
-  }
-  rank[i] = s + cnt;
+sch_repack(const uint64_t* __restrict__ bits, const int32_t* __restrict__ ones,
+           const int32_t* __restrict__ order, int N, int W, uint64_t* __restrict__ bits_s,
+           int32_t* __restrict__ ones_s) {
+  const int r = blockIdx.x * kT + threadIdx.x;
+  if (r >= N) return;
+  const int i = order[r];
+  const uint64_t* b = bits + (int64_t)i * W;
+  for (int w = 0; w < W; ++w) bits_s[(int64_t)w * N + r] = b[w];
+  ones_s[r] = ones[i];
 }
 
-__global__ void __launch_bounds__(kT)
-sch_order(const int32_t* __restrict__ rank, int N, int32_t* __restrict__ order) {
-  const int i = blockIdx.x * kT + threadIdx.x;
-  if (i < N) order[rank[i]] = i;
-}
-
+// ------------------------------------------- per-phase launches (fallback)
+// Used when the shapes exceed the cooperative kernel's LDS limits or a
+// cooperative launch is refused; token-index space throughout.
 // Column counts. mode 0: all tokens -> cnt[0]; mode 1: original split
 // (i < n1 -> cnt[0], else cnt[1]); mode 2: current batches (in1[i] -> cnt[0]).
 // tot[c] accumulates |r_i| of the tokens counted into cnt[c].
@@ -451,80 +475,38 @@ sch_select(int N, int n1, int nbins, int off, const int32_t* __restrict__ delta,
   }
 }
 
-__global__ void __launch_bounds__(kSel)
-sch_finish(int N, int n1, int L, int E, int keep_if_worse, int trivial,
-           const int32_t* __restrict__ in1, const int32_t* __restrict__ cnt,
-           const int32_t* __restrict__ cnt_orig, const int64_t* __restrict__ state,
-           const int32_t* __restrict__ err,
-           int32_t* __restrict__ perm, int32_t* __restrict__ demand, int64_t* __restrict__ info) {
-  const int LE = L * E;
-  int a = 0, b = 0;
-  for (int q = threadIdx.x; q < LE; q += kSel) {
-    a += (cnt_orig[q] > 0) + (cnt_orig[LE + q] > 0);
-    if (!trivial) b += (cnt[q] > 0) + (cnt[LE + q] > 0);
-  }
-  int before, after;
-  block_excl_scan<kSel>(a, &before);
-  block_excl_scan<kSel>(b, &after);
-  if (trivial) after = before;
-  const bool use_orig = trivial || (keep_if_worse && after > before);
-  const int32_t* src = use_orig ? cnt_orig : cnt;
-  // stable compaction: batch 1 in ascending index, then batch 2
-  const int per = (N + kSel - 1) / kSel;
-  const int i0 = min(N, (int)threadIdx.x * per), i1 = min(N, i0 + per);
-  int mine = 0;
-  for (int i = i0; i < i1; ++i) mine += use_orig ? (i < n1) : (in1[i] != 0);
-  int tot1;
-  int p1 = block_excl_scan<kSel>(mine, &tot1);
-  int p2 = tot1 + (i0 - p1);
-  for (int i = i0; i < i1; ++i) {
-    const bool one = use_orig ? (i < n1) : (in1[i] != 0);
-    if (one) perm[p1++] = i;
-    else perm[p2++] = i;
-  }
-  if (demand)
-    for (int q = threadIdx.x; q < 2 * LE; q += kSel) demand[q] = src[q];
-  if (threadIdx.x == 0) {
-    // a bounded wait that timed out in the cooperative loop marks the result
-    info[0] = (*err) ? -1 : (trivial ? 0 : state[ST_ITERS]);
-    info[1] = trivial ? 1 : state[ST_CONV];
-    info[2] = trivial ? -1 : state[ST_AM1];
-    info[3] = trivial ? -1 : state[ST_AM2];
-    info[4] = before;
-    info[5] = use_orig ? before : after;
-    info[6] = (!trivial && use_orig) ? 1 : 0;
-    info[7] = n1;
-  }
-}
-
 // ------------------------------------------------ cooperative round loop
-// All rounds in one cooperative launch (every block resident): block b owns
-// a contiguous range of token indices and the same range of signature ranks.
-// Data that crosses blocks inside the launch is read and written with
-// device-scope atomics, and phases are separated by a grid barrier on a
-// monotonic arrival counter: every thread issues an agent-scope release fence
-// before its block arrives (the XCD L2s are not coherent with each other, and
-// a workgroup barrier does not wait for the other waves' memory operations)
-// and an acquire fence after the wait. Every barrier wait is
-// bounded: past the bound the block records an error and goes on, so the
+// All rounds in one cooperative launch (every block resident). Tokens are
+// addressed by signature position r: block b owns a contiguous range of
+// positions and keeps its per-position state (delta, batch) in memory that
+// only the owning thread touches, so ties are broken by position directly.
+// Data that crosses blocks is written with device-scope atomics (sums, minima)
+// or agent-scope atomic stores and read with agent-scope atomic loads; phases
+// are separated by a grid barrier on a monotonic arrival counter, with an
+// agent-scope release fence before a block arrives and an acquire fence after
+// the wait (the XCD L2s are not coherent with each other). Every barrier wait
+// is bounded: past the bound the block records an error and goes on, so the
 // launch always terminates (the result is then flagged, never trusted).
-// Candidates are packed as (value << 24 | signature rank) and reduced with a
-// 64-bit atomicMin, which keeps the lower-rank tie rule.
+// Candidates are packed as (value << 24 | position) and reduced with a 64-bit
+// atomicMin, which keeps the lower-position tie rule. A round needs three
+// barriers: after the histogram, after the assignment, after the candidates.
 constexpr int kCoopT = 256;
 constexpr int kCoopMaxLE = 8192;
+constexpr int kCoopMaxBins = 4096;
+constexpr int kCoopMaxBlocks = 1024;
 constexpr unsigned kSpinBound = 1u << 20;
 
-// Shared data within the launch: reads as an atomic add of zero, writes as an
-// atomic exchange, the same path the accumulating atomics take.
-__device__ __forceinline__ int ld_coh(const int32_t* p) {
-  return atomicAdd(const_cast<int32_t*>(p), 0);
+__device__ __forceinline__ int ld_ag(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_coh(int32_t* p, int32_t v) { atomicExch(p, v); }
-__device__ __forceinline__ unsigned long long ld_coh64(const unsigned long long* p) {
-  return atomicAdd(const_cast<unsigned long long*>(p), 0ull);
+__device__ __forceinline__ unsigned long long ld_ag64(const unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_coh64(unsigned long long* p, unsigned long long v) {
-  atomicExch(p, v);
+__device__ __forceinline__ void st_ag(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_ag64(unsigned long long* p, unsigned long long v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ void grid_sync(unsigned* bar, unsigned nblk, int32_t* err) {
@@ -558,19 +540,19 @@ __device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v)
 }
 
 struct CoopArgs {
-  const uint64_t* bits_t;   // [W][N] word-major paths
-  const int32_t* ones;
-  const int32_t* rank;
-  const int32_t* order;
-  int N, W, LE, n1, nbins, off, max_iters, trivial, twoLk;
-  int32_t* delta;           // [N]
-  int32_t* in1;             // [N]
-  int32_t* hist;            // [nbins]
-  int32_t* cnt;             // [2][LE]
-  int32_t* cnt_orig;        // [2][LE]
-  unsigned long long* tot;  // [4]: batch sums, then input-split sums
-  unsigned long long* cand; // [2]
-  int32_t* tiecnt;          // [nblk]
+  const uint64_t* bits_s;   // [W][N] paths in signature order
+  const int32_t* ones_s;    // [N] path sizes in signature order
+  const int32_t* order;     // [N] token at each signature position
+  int N, W, LE, n1, nbins, off, max_iters, twoLk;
+  int32_t* delta_s;         // [N] by position (owning thread only)
+  int32_t* in1_s;           // [N] by position (owning thread only)
+  int32_t* in1;             // [N] by token: the final batch-1 flags
+  int32_t* hist;            // [2][nbins] global histograms of alternate rounds
+  int32_t* hpart;           // [gridDim][nbins] per-block histograms
+  int32_t* cnt;             // [LE] batch-1 column counts
+  int32_t* cnt_orig;        // [2][LE] column counts of the input split
+  unsigned long long* tot;  // [4]: [0] batch-1 path-size sum, [2..3] input split
+  unsigned long long* cand; // [8]: m1, m2 of the start, then 3 slots of 2
   unsigned* bar;
   int32_t* err;
   int64_t* state;
@@ -578,19 +560,21 @@ struct CoopArgs {
 
 __global__ void __launch_bounds__(kCoopT)
 sch_coop(CoopArgs a) {
-  __shared__ int32_t s_c[2 * kCoopMaxLE];        // local column counts / copy of cnt
+  __shared__ int32_t s_c[2 * kCoopMaxLE];        // batch counts / signed count changes
+  __shared__ int32_t s_all[kCoopMaxLE];          // column counts over all tokens
+  __shared__ int32_t s_h[kCoopMaxBins];
   __shared__ uint64_t s_med[2][kCoopMaxLE / 64];
   __shared__ unsigned long long s_red[kCoopT / kWave];
-  __shared__ int s_thr, s_q;
   __shared__ unsigned long long s_tot[2];
+  __shared__ int s_thr, s_q;
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const unsigned nblk = gridDim.x;
-  const int N = a.N, W = a.W, LE = a.LE;
+  const int N = a.N, W = a.W, LE = a.LE, nbins = a.nbins, off = a.off, n1 = a.n1;
   const int per = (N + (int)nblk - 1) / (int)nblk;
   const int t0 = min(N, (int)blockIdx.x * per), t1 = min(N, t0 + per);
 
-  auto word = [&](int i, int w) { return a.bits_t[(int64_t)w * N + i]; };
+  auto word = [&](int r, int w) { return a.bits_s[(int64_t)w * N + r]; };
 
   auto block_min_u64 = [&](unsigned long long v) {
     v = wave_min_u64(v);
@@ -602,178 +586,211 @@ sch_coop(CoopArgs a) {
     return r;
   };
 
-  // Column counts of this block's tokens into global cnt (batch of token i
-  // from `batch_of`), plus |r| sums into tot[2 * which + batch].
-  auto count = [&](auto batch_of, int32_t* dst, int which) {
-    for (int q = tid; q < 2 * LE; q += kCoopT) s_c[q] = 0;
-    if (tid < 2) s_tot[tid] = 0;
-    __syncthreads();
-    for (int i = t0 + tid; i < t1; i += kCoopT) {
-      const int c = batch_of(i);
-      for (int w = 0; w < W; ++w) {
-        uint64_t x = word(i, w);
-        while (x) {
-          atomicAdd(&s_c[c * LE + w * 64 + __builtin_ctzll(x)], 1);
-          x &= x - 1;
-        }
-      }
-      atomicAdd(&s_tot[c], (unsigned long long)a.ones[i]);
-    }
-    __syncthreads();
-    for (int q = tid; q < 2 * LE; q += kCoopT)
-      if (s_c[q]) atomicAdd(&dst[q], s_c[q]);
-    if (tid < 2 && s_tot[tid]) atomicAdd(&a.tot[2 * which + tid], s_tot[tid]);
-  };
-
-  // Candidate key of token i under the batch sums copied into s_c / s_tot.
-  auto dist_key = [&](int i, int c, int64_t size) -> unsigned long long {
-    const int32_t* cc = s_c + c * LE;
+  // (sum_j in batch d(r, j)) << 24 | r under the counts cc of that batch
+  auto dist_key = [&](int r, const int32_t* cc, int64_t size, unsigned long long tot) {
     int64_t g = 0;
     for (int w = 0; w < W; ++w) {
-      uint64_t x = word(i, w);
+      uint64_t x = word(r, w);
       while (x) {
         g += cc[w * 64 + __builtin_ctzll(x)];
         x &= x - 1;
       }
     }
-    const int64_t D = size * a.ones[i] + (int64_t)s_tot[c] - 2 * g;
-    return ((unsigned long long)D << 24) | (unsigned long long)a.rank[i];
+    const int64_t D = size * a.ones_s[r] + (int64_t)tot - 2 * g;
+    return ((unsigned long long)D << 24) | (unsigned long long)r;
+  };
+  auto decode = [&](unsigned long long key) {
+    const int r = (int)(key & 0xFFFFFF);
+    return r < N ? r : 0;                         // empty batch only after a barrier error
   };
 
   // ---- input split: column counts (Eq. 2 before, demand of the original)
-  count([&](int i) { return i < a.n1 ? 0 : 1; }, a.cnt_orig, 1);
-  if (a.trivial) return;                          // uniform over the grid
+  for (int q = tid; q < 2 * LE; q += kCoopT) s_c[q] = 0;
+  if (tid < 2) s_tot[tid] = 0;
+  __syncthreads();
+  for (int r = t0 + tid; r < t1; r += kCoopT) {
+    const int c = a.order[r] < n1 ? 0 : 1;
+    for (int w = 0; w < W; ++w) {
+      uint64_t x = word(r, w);
+      while (x) {
+        atomicAdd(&s_c[c * LE + w * 64 + __builtin_ctzll(x)], 1);
+        x &= x - 1;
+      }
+    }
+    atomicAdd(&s_tot[c], (unsigned long long)a.ones_s[r]);
+    a.in1_s[r] = 0;
+  }
+  __syncthreads();
+  for (int q = tid; q < 2 * LE; q += kCoopT)
+    if (s_c[q]) atomicAdd(&a.cnt_orig[q], s_c[q]);
+  if (tid < 2 && s_tot[tid]) atomicAdd(&a.tot[2 + tid], s_tot[tid]);
   grid_sync(a.bar, nblk, a.err);
 
   // ---- m1: least total distance; counts over everyone = both input batches
-  for (int q = tid; q < LE; q += kCoopT) s_c[q] = ld_coh(a.cnt_orig + q) + ld_coh(a.cnt_orig + LE + q);
-  if (tid == 0) s_tot[0] = ld_coh64(a.tot + 2) + ld_coh64(a.tot + 3);
+  for (int q = tid; q < LE; q += kCoopT) s_all[q] = ld_ag(a.cnt_orig + q) + ld_ag(a.cnt_orig + LE + q);
+  const unsigned long long tot_all = ld_ag64(a.tot + 2) + ld_ag64(a.tot + 3);
   __syncthreads();
   {
     unsigned long long best = ~0ull;
-    for (int i = t0 + tid; i < t1; i += kCoopT) {
-      const unsigned long long k = dist_key(i, 0, N);
-      best = k < best ? k : best;
+    for (int r = t0 + tid; r < t1; r += kCoopT) {
+      const unsigned long long key = dist_key(r, s_all, N, tot_all);
+      best = key < best ? key : best;
     }
     best = block_min_u64(best);
     if (tid == 0) atomicMin(&a.cand[0], best);
   }
   grid_sync(a.bar, nblk, a.err);
-  auto decode = [&](unsigned long long key) {
-    const int r = (int)(key & 0xFFFFFF);
-    return r < N ? a.order[r] : 0;               // empty batch only after a barrier error
-  };
-  int m1 = decode(ld_coh64(a.cand));
+  int m1 = decode(ld_ag64(a.cand));
   for (int w = tid; w < W; w += kCoopT) s_med[0][w] = word(m1, w);
   __syncthreads();
-  // ---- m2: farthest from m1, as a minimum of (2Lk - d, rank)
+  // ---- m2: farthest from m1, as a minimum of (2Lk - d, position)
   {
     unsigned long long best = ~0ull;
-    for (int i = t0 + tid; i < t1; i += kCoopT) {
-      if (i == m1) continue;
+    for (int r = t0 + tid; r < t1; r += kCoopT) {
+      if (r == m1) continue;
       int d = 0;
-      for (int w = 0; w < W; ++w) d += __popcll(word(i, w) ^ s_med[0][w]);
-      const unsigned long long k = ((unsigned long long)(a.twoLk - d) << 24) | (unsigned long long)a.rank[i];
-      best = k < best ? k : best;
+      for (int w = 0; w < W; ++w) d += __popcll(word(r, w) ^ s_med[0][w]);
+      const unsigned long long key = ((unsigned long long)(a.twoLk - d) << 24) | (unsigned long long)r;
+      best = key < best ? key : best;
     }
     best = block_min_u64(best);
     if (tid == 0) atomicMin(&a.cand[1], best);
   }
   grid_sync(a.bar, nblk, a.err);
-  int m2 = decode(ld_coh64(a.cand + 1));
+  int m2 = decode(ld_ag64(a.cand + 1));
 
-  int iters = 0, conv = 0, am1 = -1, am2 = -1;
+  int iters = 0, conv = 0, am1 = m1, am2 = m2;
   for (int it = 1; it <= a.max_iters; ++it) {
-    // A: delta_i = d(i, m1) - d(i, m2) for own tokens, histogram
+    int32_t* hc = a.hist + (it & 1) * nbins;       // this round's histogram
+    unsigned long long* cs = a.cand + 2 + 2 * (it % 3);
+    // A: delta for own positions, block histogram; clear the next round's
+    // histogram and candidate slots (last read two barriers ago)
     for (int w = tid; w < W; w += kCoopT) {
       s_med[0][w] = word(m1, w);
       s_med[1][w] = word(m2, w);
     }
+    for (int v = tid; v < nbins; v += kCoopT) s_h[v] = 0;
     __syncthreads();
-    for (int i = t0 + tid; i < t1; i += kCoopT) {
+    for (int r = t0 + tid; r < t1; r += kCoopT) {
       int d = 0;
       for (int w = 0; w < W; ++w) {
-        const uint64_t x = word(i, w);
+        const uint64_t x = word(r, w);
         d += __popcll(x ^ s_med[0][w]) - __popcll(x ^ s_med[1][w]);
       }
-      st_coh(a.delta + i, d);
-      atomicAdd(&a.hist[d + a.off], 1);
+      a.delta_s[r] = d;
+      atomicAdd(&s_h[d + off], 1);
+    }
+    {
+      int32_t* hn = a.hist + ((it + 1) & 1) * nbins;
+      for (int v = blockIdx.x * kCoopT + tid; v < nbins; v += (int)nblk * kCoopT) st_ag(hn + v, 0);
+      if (blockIdx.x == 0 && tid < 2) st_ag64(a.cand + 2 + 2 * ((it + 1) % 3) + tid, ~0ull);
+    }
+    __syncthreads();
+    {
+      int32_t* hp = a.hpart + (int64_t)blockIdx.x * nbins;
+      for (int v = tid; v < nbins; v += kCoopT) {
+        const int h = s_h[v];
+        st_ag(hp + v, h);
+        if (h) atomicAdd(hc + v, h);
+      }
     }
     grid_sync(a.bar, nblk, a.err);
-    // B: threshold (every block alike), ties of own rank range; resets
+    // B: threshold (every block alike), ties of lower blocks, assignment in
+    // position order; batch changes update the batch-1 counts
+    if (tid == 0) {                               // defaults that keep indices in range
+      s_thr = nbins - 1 - off;
+      s_q = n1;
+    }
     {
-      const int pb = (a.nbins + kCoopT - 1) / kCoopT;
-      const int v0 = min(a.nbins, tid * pb), v1 = min(a.nbins, v0 + pb);
+      const int pb = (nbins + kCoopT - 1) / kCoopT;
+      const int v0 = min(nbins, tid * pb), v1 = min(nbins, v0 + pb);
       int local = 0;
-      for (int v = v0; v < v1; ++v) local += ld_coh(a.hist + v);
+      for (int v = v0; v < v1; ++v) local += ld_ag(hc + v);
       int total;
       int cum = block_excl_scan<kCoopT>(local, &total);
       for (int v = v0; v < v1; ++v) {
-        const int h = ld_coh(a.hist + v);
-        if (cum < a.n1 && cum + h >= a.n1) {
-          s_thr = v - a.off;
-          s_q = a.n1 - cum;
+        const int h = ld_ag(hc + v);
+        if (cum < n1 && cum + h >= n1) {
+          s_thr = v - off;
+          s_q = n1 - cum;
         }
         cum += h;
       }
     }
+    for (int q = tid; q < LE; q += kCoopT) s_c[q] = 0;
+    if (tid == 0) s_tot[0] = 0;
     __syncthreads();
     const int thr = s_thr, q = s_q;
-    const int sub = (t1 - t0 + kCoopT - 1) / kCoopT;      // ranks per thread
-    const int r0 = min(t1, t0 + tid * sub), r1 = min(t1, r0 + sub);
-    int ties = 0;
-    for (int r = r0; r < r1; ++r) ties += ld_coh(a.delta + a.order[r]) == thr;
-    int btot;
-    int pre_in_block = block_excl_scan<kCoopT>(ties, &btot);
-    if (tid == 0) st_coh(a.tiecnt + blockIdx.x, btot);
-    if (blockIdx.x == 0) {
-      if (tid < 2) st_coh64(a.cand + tid, ~0ull);
-      if (tid < 2) st_coh64(a.tot + tid, 0ull);
-    }
-    for (int qq = blockIdx.x * kCoopT + tid; qq < 2 * LE; qq += (int)nblk * kCoopT) st_coh(a.cnt + qq, 0);
-    grid_sync(a.bar, nblk, a.err);
-    // C: the first n1 in (delta, rank) order go to batch 1; hist reset
+    int pre;
     {
-      int before = 0;
-      for (unsigned b = 0; b < blockIdx.x; ++b) before += ld_coh(a.tiecnt + b);
-      int pre = before + pre_in_block;
-      for (int r = r0; r < r1; ++r) {
-        const int i = a.order[r];
-        const int d = ld_coh(a.delta + i);
-        st_coh(a.in1 + i, d < thr ? 1 : (d > thr ? 0 : (pre++ < q ? 1 : 0)));
-      }
+      int lower = 0;
+      for (int b = tid; b < (int)blockIdx.x; b += kCoopT) lower += ld_ag(a.hpart + (int64_t)b * nbins + thr + off);
+      int total;
+      block_excl_scan<kCoopT>(lower, &total);
+      pre = total;
     }
-    for (int v = blockIdx.x * kCoopT + tid; v < a.nbins; v += (int)nblk * kCoopT) st_coh(a.hist + v, 0);
+    for (int base = t0; base < t1; base += kCoopT) {
+      const int r = base + tid;
+      const bool own = r < t1;
+      const int d = own ? a.delta_s[r] : 0;
+      int ties;
+      const int x = block_excl_scan<kCoopT>(own && d == thr ? 1 : 0, &ties);
+      if (own) {
+        const int nw = d < thr ? 1 : (d > thr ? 0 : (pre + x < q ? 1 : 0));
+        if (nw != a.in1_s[r]) {
+          const int sgn = nw ? 1 : -1;
+          for (int w = 0; w < W; ++w) {
+            uint64_t y = word(r, w);
+            while (y) {
+              atomicAdd(&s_c[w * 64 + __builtin_ctzll(y)], sgn);
+              y &= y - 1;
+            }
+          }
+          atomicAdd(&s_tot[0], (unsigned long long)(int64_t)(sgn * a.ones_s[r]));
+          a.in1_s[r] = nw;
+        }
+      }
+      pre += ties;
+    }
+    __syncthreads();
+    for (int qq = tid; qq < LE; qq += kCoopT)
+      if (s_c[qq]) atomicAdd(&a.cnt[qq], s_c[qq]);
+    if (tid == 0 && s_tot[0]) atomicAdd(&a.tot[0], s_tot[0]);
     am1 = m1;
     am2 = m2;
     iters = it;
     grid_sync(a.bar, nblk, a.err);
-    // D: batch column counts
-    count([&](int i) { return ld_coh(a.in1 + i) ? 0 : 1; }, a.cnt, 0);
-    grid_sync(a.bar, nblk, a.err);
-    // E: centroid candidates per batch
-    for (int qq = tid; qq < 2 * LE; qq += kCoopT) s_c[qq] = ld_coh(a.cnt + qq);
-    if (tid < 2) s_tot[tid] = ld_coh64(a.tot + tid);
+    // C: centroid candidates per batch
+    for (int qq = tid; qq < LE; qq += kCoopT) {
+      const int c1 = ld_ag(a.cnt + qq);
+      s_c[qq] = c1;
+      s_c[LE + qq] = s_all[qq] - c1;
+    }
+    if (tid == 0) {
+      const unsigned long long t1s = ld_ag64(a.tot);
+      s_tot[0] = t1s;
+      s_tot[1] = tot_all - t1s;
+    }
     __syncthreads();
     {
       unsigned long long b0 = ~0ull, b1 = ~0ull;
-      for (int i = t0 + tid; i < t1; i += kCoopT) {
-        const int c = ld_coh(a.in1 + i) ? 0 : 1;
-        const unsigned long long k = dist_key(i, c, c == 0 ? a.n1 : N - a.n1);
-        if (c == 0) b0 = k < b0 ? k : b0;
-        else b1 = k < b1 ? k : b1;
+      for (int r = t0 + tid; r < t1; r += kCoopT) {
+        const int c = a.in1_s[r] ? 0 : 1;
+        const unsigned long long key = dist_key(r, s_c + c * LE, c == 0 ? n1 : N - n1, s_tot[c]);
+        if (c == 0) b0 = key < b0 ? key : b0;
+        else b1 = key < b1 ? key : b1;
       }
       b0 = block_min_u64(b0);
       b1 = block_min_u64(b1);
       if (tid == 0) {
-        atomicMin(&a.cand[0], b0);
-        atomicMin(&a.cand[1], b1);
+        atomicMin(cs, b0);
+        atomicMin(cs + 1, b1);
       }
     }
     grid_sync(a.bar, nblk, a.err);
-    // F: new centroids; stop when they repeat (same decision in every block)
-    const int n1c = decode(ld_coh64(a.cand));
-    const int n2c = decode(ld_coh64(a.cand + 1));
+    // D: new centroids; stop when they repeat (same decision in every block)
+    const int n1c = decode(ld_ag64(cs));
+    const int n2c = decode(ld_ag64(cs + 1));
     if (n1c == m1 && n2c == m2) {
       conv = 1;
       break;
@@ -781,25 +798,30 @@ sch_coop(CoopArgs a) {
     m1 = n1c;
     m2 = n2c;
   }
+  for (int r = t0 + tid; r < t1; r += kCoopT) a.in1[a.order[r]] = a.in1_s[r];
   if (blockIdx.x == 0 && tid == 0) {
     a.state[ST_ITERS] = iters;
     a.state[ST_CONV] = conv;
-    a.state[ST_AM1] = am1;
-    a.state[ST_AM2] = am2;
+    a.state[ST_AM1] = a.order[am1];
+    a.state[ST_AM2] = a.order[am2];
   }
 }
 
-// Clears the small scratch of one call (a kernel rather than memset nodes,
-// so that the sequence can be captured in a graph).
+// Clears the scratch of one call (a kernel rather than memset nodes, so that
+// the sequence can be captured in a graph).
 __global__ void __launch_bounds__(kT)
-sch_init(int32_t* __restrict__ hist, int nbins, int32_t* __restrict__ cnt_orig, int LE2,
-         unsigned long long* __restrict__ tot, unsigned long long* __restrict__ cand,
-         unsigned* __restrict__ bar, int32_t* __restrict__ err, int64_t* __restrict__ state) {
+sch_init(int32_t* __restrict__ hist, int nbins2, int32_t* __restrict__ cnt_orig,
+         int32_t* __restrict__ cnt, int LE2, unsigned long long* __restrict__ tot,
+         unsigned long long* __restrict__ cand, unsigned* __restrict__ bar,
+         int32_t* __restrict__ err, int64_t* __restrict__ state) {
   const int g = blockIdx.x * kT + threadIdx.x, stride = gridDim.x * kT;
-  for (int q = g; q < nbins; q += stride) hist[q] = 0;
-  for (int q = g; q < LE2; q += stride) cnt_orig[q] = 0;
+  for (int q = g; q < nbins2; q += stride) hist[q] = 0;
+  for (int q = g; q < LE2; q += stride) {
+    cnt_orig[q] = 0;
+    cnt[q] = 0;
+  }
   if (g < 4) tot[g] = 0;
-  if (g < 2) cand[g] = ~0ull;
+  if (g < 8) cand[g] = ~0ull;
   if (g < ST_NWORDS) state[g] = 0;
   if (g == 0) {
     *bar = 0;
@@ -807,22 +829,100 @@ sch_init(int32_t* __restrict__ hist, int nbins, int32_t* __restrict__ cnt_orig, 
   }
 }
 
+// ------------------------------------------------ finish
+// Eq. 2 before / after and the guard decision (block 0), and the batch-1
+// count of each kSel-token block of token indices. The batch-2 column counts
+// are the all-token counts minus the batch-1 counts.
+__global__ void __launch_bounds__(kSel)
+sch_fin_count(int N, int LE, int keep_if_worse, int trivial, const int32_t* __restrict__ in1,
+              const int32_t* __restrict__ cnt, const int32_t* __restrict__ cnt_orig,
+              int32_t* __restrict__ blkcnt, int64_t* __restrict__ state) {
+  if (blockIdx.x == 0) {
+    int a = 0, b = 0;
+    for (int q = threadIdx.x; q < LE; q += kSel) {
+      const int o0 = cnt_orig[q], o1 = cnt_orig[LE + q];
+      a += (o0 > 0) + (o1 > 0);
+      if (!trivial) {
+        const int c1 = cnt[q];
+        b += (c1 > 0) + (o0 + o1 - c1 > 0);
+      }
+    }
+    int before, after;
+    block_excl_scan<kSel>(a, &before);
+    block_excl_scan<kSel>(b, &after);
+    if (trivial) after = before;
+    if (threadIdx.x == 0) {
+      state[ST_BEFORE] = before;
+      state[ST_AFTER] = after;
+      state[ST_USE_ORIG] = (trivial || (keep_if_worse && after > before)) ? 1 : 0;
+    }
+  }
+  if (trivial) return;
+  const int i = blockIdx.x * kSel + threadIdx.x;
+  int tot1;
+  block_excl_scan<kSel>((i < N && in1[i] != 0) ? 1 : 0, &tot1);
+  if (threadIdx.x == 0) blkcnt[blockIdx.x] = tot1;
+}
+
+// perm by stable compaction (batch 1 ascending, then batch 2), demand, info.
+__global__ void __launch_bounds__(kSel)
+sch_fin_scatter(int N, int n1, int LE, int trivial, const int32_t* __restrict__ in1,
+                const int32_t* __restrict__ cnt, const int32_t* __restrict__ cnt_orig,
+                const int32_t* __restrict__ blkcnt, const int64_t* __restrict__ state,
+                const int32_t* __restrict__ err, int32_t* __restrict__ perm,
+                int32_t* __restrict__ demand, int64_t* __restrict__ info) {
+  const bool use_orig = state[ST_USE_ORIG] != 0;
+  const int i = blockIdx.x * kSel + threadIdx.x;
+  if (use_orig) {
+    if (i < N) perm[i] = i;                       // [0, n1) then [n1, N), each ascending
+  } else {
+    const int nb = (int)gridDim.x;
+    int lower = 0, all = 0;
+    for (int b = threadIdx.x; b < nb; b += kSel) {
+      const int c = blkcnt[b];
+      all += c;
+      if (b < (int)blockIdx.x) lower += c;
+    }
+    int tot1, below;
+    block_excl_scan<kSel>(all, &tot1);
+    block_excl_scan<kSel>(lower, &below);
+    const int one = (i < N && in1[i] != 0) ? 1 : 0;
+    int blk;
+    const int x = block_excl_scan<kSel>(one, &blk);
+    if (i < N) perm[one ? below + x : tot1 + i - (below + x)] = i;
+  }
+  if (blockIdx.x != 0) return;
+  if (demand)
+    for (int q = threadIdx.x; q < LE; q += kSel) {
+      const int o0 = cnt_orig[q], o1 = cnt_orig[LE + q];
+      const int c1 = use_orig ? o0 : cnt[q];
+      demand[q] = c1;
+      demand[LE + q] = o0 + o1 - c1;
+    }
+  if (threadIdx.x == 0) {
+    // a bounded wait that timed out in the cooperative loop marks the result
+    info[0] = (*err) ? -1 : (trivial ? 0 : state[ST_ITERS]);
+    info[1] = trivial ? 1 : state[ST_CONV];
+    info[2] = trivial ? -1 : state[ST_AM1];
+    info[3] = trivial ? -1 : state[ST_AM2];
+    info[4] = state[ST_BEFORE];
+    info[5] = use_orig ? state[ST_BEFORE] : state[ST_AFTER];
+    info[6] = (!trivial && use_orig) ? 1 : 0;
+    info[7] = n1;
+  }
+}
+
 struct SchLayout {
-  size_t bits, bits_t, key0, ones, rank, part, order1, runs, order, delta, in1, cnt, cnt_orig,
-      hist, tot, state, cand, cand2, tiecnt, bar, total;
+  size_t bits, bits_s, key0, key1, skey0, skey1, sidx, part, ones, ones_s, rank, order, delta,
+      in1, in1_s, cnt, cnt_orig, hist, hpart, tot, state, cand, cand8, blkcnt, bar, total;
 };
 
-// j-tiling of the first-level rank: about 2048 blocks in all, tiles of a
-// multiple of 64 tokens.
-struct RankTiles {
-  int tile, ntiles;
-};
+int rank_groups(int64_t N) {
+  return (int)std::min<int64_t>(kMaxRankGroups, ceil_div(N, kChunk));
+}
 
-RankTiles rank_tiles(int64_t N) {
-  const int64_t nbi = ceil_div(N, kT);
-  const int64_t want = std::max<int64_t>(1, std::min<int64_t>(64, 2048 / nbi));
-  const int64_t tile = align_up(ceil_div(N, want), 64);
-  return RankTiles{(int)tile, (int)ceil_div(N, tile)};
+bool coop_shapes(int64_t N, int64_t L, int64_t E, int64_t k) {
+  return L * E <= kCoopMaxLE && N < (1 << 24) && 4 * L * k + 1 <= kCoopMaxBins;
 }
 
 SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
@@ -830,6 +930,8 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
   const int64_t LE = (int64_t)L * E;
   const int64_t nbins = 4 * (int64_t)L * k + 1;
   const int64_t nblk = ceil_div(N, kT);
+  const int64_t coop_blocks =
+      coop_shapes(N, L, E, k) ? std::min<int64_t>(kCoopMaxBlocks, ceil_div(N, kCoopT)) : 0;
   SchLayout s{};
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -838,24 +940,29 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
     return at;
   };
   s.bits = take(N * W * 8);
-  s.bits_t = take(N * W * 8);
+  s.bits_s = take(coop_blocks ? N * W * 8 : 0);
   s.key0 = take(N * 8);
+  s.key1 = take(N * 8);
+  s.skey0 = take(N * 8);
+  s.skey1 = take(N * 8);
+  s.sidx = take(N * 4);
+  s.part = take((size_t)rank_groups(N) * N * 4);
   s.ones = take(N * 4);
+  s.ones_s = take(N * 4);
   s.rank = take(N * 4);
-  s.part = take((size_t)rank_tiles(N).ntiles * N * 4);
-  s.order1 = take(N * 4);
-  s.runs = take(2 * N * 4);
   s.order = take(N * 4);
   s.delta = take(N * 4);
   s.in1 = take(N * 4);
+  s.in1_s = take(N * 4);
   s.cnt = take(2 * LE * 4);
   s.cnt_orig = take(2 * LE * 4);
-  s.hist = take(nbins * 4);
+  s.hist = take(2 * nbins * 4);
+  s.hpart = take(coop_blocks * nbins * 4);
   s.tot = take(4 * 8);
   s.state = take(ST_NWORDS * 8);
   s.cand = take(nblk * 2 * sizeof(Cand));
-  s.cand2 = take(2 * 8);
-  s.tiecnt = take(nblk * 4);
+  s.cand8 = take(8 * 8);
+  s.blkcnt = take(ceil_div(N, kSel) * 4);
   s.bar = take(2 * 4);                    // arrival counter, error flag
   s.total = o;
   return s;
@@ -886,25 +993,29 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
     return MOE_ERR_WORKSPACE;
   char* ws = static_cast<char*>(workspace);
   auto* bits = reinterpret_cast<uint64_t*>(ws + lay.bits);
-  auto* bits_t = reinterpret_cast<uint64_t*>(ws + lay.bits_t);
+  auto* bits_s = reinterpret_cast<uint64_t*>(ws + lay.bits_s);
   auto* key0 = reinterpret_cast<uint64_t*>(ws + lay.key0);
+  auto* key1 = reinterpret_cast<uint64_t*>(ws + lay.key1);
+  auto* skey0 = reinterpret_cast<uint64_t*>(ws + lay.skey0);
+  auto* skey1 = reinterpret_cast<uint64_t*>(ws + lay.skey1);
+  auto* sidx = reinterpret_cast<int32_t*>(ws + lay.sidx);
   auto* part = reinterpret_cast<int32_t*>(ws + lay.part);
-  auto* order1 = reinterpret_cast<int32_t*>(ws + lay.order1);
-  auto* run_s = reinterpret_cast<int32_t*>(ws + lay.runs);
-  auto* run_e = run_s + N;
   auto* ones = reinterpret_cast<int32_t*>(ws + lay.ones);
+  auto* ones_s = reinterpret_cast<int32_t*>(ws + lay.ones_s);
   auto* rank = reinterpret_cast<int32_t*>(ws + lay.rank);
   auto* order = reinterpret_cast<int32_t*>(ws + lay.order);
   auto* delta = reinterpret_cast<int32_t*>(ws + lay.delta);
   auto* in1 = reinterpret_cast<int32_t*>(ws + lay.in1);
+  auto* in1_s = reinterpret_cast<int32_t*>(ws + lay.in1_s);
   auto* cnt = reinterpret_cast<int32_t*>(ws + lay.cnt);
   auto* cnt_orig = reinterpret_cast<int32_t*>(ws + lay.cnt_orig);
   auto* hist = reinterpret_cast<int32_t*>(ws + lay.hist);
+  auto* hpart = reinterpret_cast<int32_t*>(ws + lay.hpart);
   auto* tot = reinterpret_cast<unsigned long long*>(ws + lay.tot);
   auto* state = reinterpret_cast<int64_t*>(ws + lay.state);
   auto* cand = reinterpret_cast<Cand*>(ws + lay.cand);
-  auto* cand2 = reinterpret_cast<unsigned long long*>(ws + lay.cand2);
-  auto* tiecnt = reinterpret_cast<int32_t*>(ws + lay.tiecnt);
+  auto* cand8 = reinterpret_cast<unsigned long long*>(ws + lay.cand8);
+  auto* blkcnt = reinterpret_cast<int32_t*>(ws + lay.blkcnt);
   auto* bar = reinterpret_cast<unsigned*>(ws + lay.bar);
   auto* err = reinterpret_cast<int32_t*>(ws + lay.bar + 4);
 
@@ -919,48 +1030,39 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
 
   const bool trivial = (n1 == 0 || n1 == N);
 
-  sch_init<<<dim3((unsigned)std::min<int64_t>(64, ceil_div(std::max(nbins, 2 * LE), kT))), blk, 0,
-             st>>>(hist, nbins, cnt_orig, 2 * LE, tot, cand2, bar, err, state);
+  sch_init<<<dim3((unsigned)std::min<int64_t>(64, ceil_div(std::max(2 * nbins, 2 * LE), kT))), blk,
+             0, st>>>(hist, 2 * nbins, cnt_orig, cnt, 2 * LE, tot, cand8, bar, err, state);
   MOE_CHECK_LAUNCH();
-  sch_pack<<<grid, blk, 0, st>>>(routes, n, L, E, k, W, bits, bits_t, key0, ones);
+  sch_pack<<<dim3((unsigned)ceil_div(N, kPackT)), dim3(kPackT), 0, st>>>(routes, n, L, E, k, W,
+                                                                         bits, key0, key1, ones);
   MOE_CHECK_LAUNCH();
-  // Signature order: (first word, index) by counting, then runs of equal
-  // first words re-ranked on the remaining words.
-  auto launch_rank = [&]() -> int {
-    const RankTiles rt = rank_tiles(N);
-    sch_rank_first<<<dim3(nblk, rt.ntiles), blk, 0, st>>>(key0, n, rt.tile, part);
-    if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
-    sch_order_first<<<grid, blk, 0, st>>>(part, rt.ntiles, n, rank, W > 1 ? order1 : order);
-    if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
-    if (W > 1) {
-      sch_tie_runs<<<dim3(1), dim3(kSel), 0, st>>>(key0, order1, n, run_s, run_e);
-      if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
-      sch_rank_ties<<<grid, blk, 0, st>>>(bits, n, W, order1, run_s, run_e, rank);
-      if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
-      sch_order<<<grid, blk, 0, st>>>(rank, n, order);
-      if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
-    }
-    return MOE_OK;
-  };
 
   bool done = false;
-  const bool coop_fits = LE <= kCoopMaxLE && N < (1 << 24) && 2 * (int64_t)L * k < (1 << 15);
-  if (!trivial && coop_fits) {
-    const int rc = launch_rank();
-    if (rc != MOE_OK) return rc;
-    const int cus = device_cu_count();
-    const int nb = (int)std::max<int64_t>(1, std::min<int64_t>(cus, ceil_div(N, kCoopT)));
-    CoopArgs ca{bits_t, ones, rank, order, n, W, LE, (int)n1, nbins, off, max_iters, 0,
-                2 * L * k, delta, in1, hist, cnt, cnt_orig, tot, cand2, tiecnt, bar, err, state};
-    void* args[] = {&ca};
-    if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&sch_coop), dim3(nb),
-                                   dim3(kCoopT), args, 0, st) == hipSuccess) {
-      done = true;
-    } else {
-      (void)hipGetLastError();                 // fall back to one launch per phase
-      MOE_TRY(fill_i64(state, 0, ST_NWORDS, st));
-      MOE_TRY(fill_i32(cnt_orig, 0, 2 * (int64_t)LE, st));
-      MOE_TRY(fill_i32(hist, 0, nbins, st));
+  if (!trivial) {
+    // signature order: sorted chunks, then every token's rank by lower bounds
+    const int nchunks = (int)ceil_div(N, kChunk), ngroups = rank_groups(N);
+    sch_sort_chunks<<<dim3(nchunks), dim3(kSortT), 0, st>>>(key0, key1, bits, n, W, skey0, skey1,
+                                                            sidx);
+    MOE_CHECK_LAUNCH();
+    sch_merge_rank<<<dim3((unsigned)ceil_div(N, kSortT), ngroups), dim3(kSortT), 0, st>>>(
+        key0, key1, bits, n, W, nchunks, skey0, skey1, sidx, part);
+    MOE_CHECK_LAUNCH();
+    sch_rank_sum<<<grid, blk, 0, st>>>(part, ngroups, n, rank, order);
+    MOE_CHECK_LAUNCH();
+    if (coop_shapes(N, L, E, k)) {
+      sch_repack<<<grid, blk, 0, st>>>(bits, ones, order, n, W, bits_s, ones_s);
+      MOE_CHECK_LAUNCH();
+      const int cus = device_cu_count();
+      const int nb = (int)std::max<int64_t>(
+          1, std::min<int64_t>({(int64_t)cus, ceil_div(N, kCoopT), (int64_t)kCoopMaxBlocks}));
+      CoopArgs ca{bits_s, ones_s, order, n, W, LE, (int)n1, nbins, off, max_iters, 2 * L * k,
+                  delta, in1_s, in1, hist, hpart, cnt, cnt_orig, tot, cand8, bar, err, state};
+      void* args[] = {&ca};
+      if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&sch_coop), dim3(nb),
+                                     dim3(kCoopT), args, 0, st) == hipSuccess)
+        done = true;
+      else
+        (void)hipGetLastError();                 // nothing ran: take the per-phase path
     }
   }
   if (!done) {
@@ -972,10 +1074,6 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
     MOE_CHECK_LAUNCH();
     if (!trivial) {
       MOE_TRY(fill_i64(reinterpret_cast<int64_t*>(tot), 0, 2, st));
-      if (!coop_fits) {
-        const int rc = launch_rank();
-        if (rc != MOE_OK) return rc;
-      }
       // m1: least total distance to every token
       sch_colcount<<<grid, blk, cc_lds, st>>>(bits, ones, n, W, LE, 0, (int)n1, in1, cnt, tot,
                                              state);
@@ -1008,9 +1106,12 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
       }
     }
   }
-  sch_finish<<<dim3(1), dim3(kSel), 0, st>>>(n, (int)n1, L, E, keep_original_if_worse,
-                                            trivial ? 1 : 0, in1, cnt, cnt_orig, state, err,
-                                            perm, demand, info);
+  const dim3 fgrid((unsigned)ceil_div(N, kSel));
+  sch_fin_count<<<fgrid, dim3(kSel), 0, st>>>(n, LE, keep_original_if_worse, trivial ? 1 : 0, in1,
+                                             cnt, cnt_orig, blkcnt, state);
+  MOE_CHECK_LAUNCH();
+  sch_fin_scatter<<<fgrid, dim3(kSel), 0, st>>>(n, (int)n1, LE, trivial ? 1 : 0, in1, cnt,
+                                               cnt_orig, blkcnt, state, err, perm, demand, info);
   MOE_CHECK_LAUNCH();
 #undef MOE_TRY
   return MOE_OK;

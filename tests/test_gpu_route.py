@@ -82,6 +82,24 @@ def test_x_mode_deepseek_token_bias_no_renorm():
     _x_mode_case(5, 4096, 5, bias_kind="token", renorm=False)
 
 
+@pytest.mark.parametrize("T", [17, 8209])
+def test_x_mode_64_token_tiles_ragged(T):
+    # 33..64 experts run in 64-token tiles: one partial tile, and many tiles
+    # with a ragged last one
+    _x_mode_case(5, T, 11, bias_kind="expert")
+
+
+def test_x_mode_48_experts():
+    cfg = dict(synth.config(4), E=40, k=5)
+    inp = synth.layer_inputs(cfg, 12, T=300, parts=("x", "router"))
+    idx, w, z = ops.route(to_dev(inp["x"]), to_dev(inp["w_router"]), 5, want_logits=True)
+    x, wr = synth.values(inp["x"]), synth.values(inp["w_router"])
+    z_ref = oracle.router_logits(x, wr)
+    assert (np.abs(to_host(z) - z_ref) <= logit_bound(x, wr, z_ref)).all()
+    assert np.array_equal(to_host(idx), oracle.topk_select(z_ref, 5))
+    assert np.max(np.abs(to_host(w) - oracle.gate_weights(z_ref, to_host(idx), True))) <= 1e-5
+
+
 def test_x_mode_wide_expert_count():
     cfg = dict(synth.config(4), E=256, k=8)
     inp = synth.layer_inputs(cfg, 9, T=100, parts=("x", "router"))
