@@ -9,7 +9,7 @@
 //            then token index. For two paths with the same number of ids per
 //            layer, a precedes b iff the lowest bit where they differ is set in
 //            a, which for one word is descending order of its bit reversal.
-//            Chunks of 2048 tokens are sorted in LDS (bitonic) on the first two
+//            Chunks of 512 tokens are sorted in LDS (bitonic) on the first three
 //            words, later words and the index deciding ties; the signature rank
 //            of a token is the sum of its lower bounds in every sorted chunk.
 //   init     m1 = argmin_i sum_j d_ij over all tokens, m2 = argmax_i d(i, m1)
@@ -35,8 +35,9 @@ constexpr int kT = 256;          // threads of grid-parallel kernels
 constexpr int kSel = 1024;       // threads of single-block and finish kernels
 constexpr int kPackT = 64;       // tokens per pack block
 constexpr int kPackMaxBytes = 16384;  // route bytes a pack block stages in LDS
-constexpr int kChunk = 2048;     // tokens per sorted chunk
-constexpr int kSortT = 1024;     // threads of the chunk sort and merge-rank blocks
+constexpr int kChunk = 512;      // tokens per sorted chunk
+constexpr int kSortT = 256;      // threads of the chunk sort blocks
+constexpr int kMergeT = 1024;    // threads of the merge-rank blocks
 constexpr int kMaxRankGroups = 16;    // chunk groups of the merge rank
 
 // state words
@@ -111,25 +112,35 @@ __device__ __forceinline__ uint64_t lowbit(uint64_t d) { return d & (0ull - d); 
 // Packs kPackT tokens per block: their routes are staged in LDS with
 // coalesced loads when they fit, each token's words are built in registers
 // (only the layers overlapping a word are read for it) and written row-major.
-// key0 / key1 are the sort keys of the first two words (0 when W == 1).
+// key0 / key1 / key2 are the sort keys of the first three words (0 past W).
+template <bool STAGED>
 __global__ void __launch_bounds__(kPackT)
 sch_pack(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
          uint64_t* __restrict__ bits, uint64_t* __restrict__ key0, uint64_t* __restrict__ key1,
-         int32_t* __restrict__ ones) {
-  __shared__ uint8_t s_r[kPackMaxBytes];
+         uint64_t* __restrict__ key2, int32_t* __restrict__ ones) {
+  __shared__ __attribute__((aligned(16))) uint8_t s_r[kPackMaxBytes];
   const int Lk = L * k, LE = L * E;
   const int t0 = blockIdx.x * kPackT;
   const int nt = min(kPackT, N - t0);
   const uint8_t* src = routes + (int64_t)t0 * Lk;
-  const bool staged = kPackT * Lk <= kPackMaxBytes;
-  if (staged) {
+  if constexpr (STAGED) {
+    // 16-byte pieces, eight loads in flight per thread, then the odd tail
     const int nbytes = nt * Lk;
     int q0 = 0;
-    if ((reinterpret_cast<uintptr_t>(src) & 3) == 0) {
-      const uint32_t* s4 = reinterpret_cast<const uint32_t*>(src);
-      uint32_t* d4 = reinterpret_cast<uint32_t*>(s_r);
-      for (int q = threadIdx.x; q < nbytes / 4; q += kPackT) d4[q] = s4[q];
-      q0 = nbytes & ~3;
+    if ((reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+      const uint4* s16 = reinterpret_cast<const uint4*>(src);
+      uint4* d16 = reinterpret_cast<uint4*>(s_r);
+      const int n16 = nbytes / 16;
+      for (int q = threadIdx.x; q < n16; q += 8 * kPackT) {
+        uint4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (q + u * kPackT < n16) v[u] = s16[q + u * kPackT];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (q + u * kPackT < n16) d16[q + u * kPackT] = v[u];
+      }
+      q0 = n16 * 16;
     }
     for (int q = q0 + threadIdx.x; q < nbytes; q += kPackT) s_r[q] = src[q];
     __syncthreads();
@@ -137,44 +148,72 @@ sch_pack(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
   const int t = threadIdx.x;
   if (t >= nt) return;
   const int i = t0 + t;
-  const uint8_t* r = staged ? s_r + t * Lk : src + (int64_t)t * Lk;
+  const uint8_t* r;
+  if constexpr (STAGED) r = s_r + t * Lk;
+  else r = src + (int64_t)t * Lk;
   uint64_t* b = bits + (int64_t)i * W;
-  uint64_t k0 = 0, k1 = 0;
+  uint64_t k0 = 0, k1 = 0, k2 = 0;
   int c = 0;
   for (int w = 0; w < W; ++w) {
     const int lo = w * 64, hi = min(lo + 64, LE);
     uint64_t word = 0;
-    for (int l = lo / E; l * E < hi; ++l)
-      for (int j = 0; j < k; ++j) {
-        const int e = r[l * k + j];
+    for (int l = lo / E; l * E < hi; ++l) {
+      auto set = [&](int e) {
         const int bit = l * E + e - lo;
         if (e < E && bit >= 0 && bit < 64) word |= 1ull << bit;
+      };
+      if (k <= 8) {                              // the layer's ids read together
+        int ev[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) ev[j] = j < k ? r[l * k + j] : E;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) set(ev[j]);
+      } else {
+        for (int j = 0; j < k; ++j) set(r[l * k + j]);
       }
+    }
     b[w] = word;
     c += __popcll(word);
     if (w == 0) k0 = ~__builtin_bitreverse64(word);
     if (w == 1) k1 = ~__builtin_bitreverse64(word);
+    if (w == 2) k2 = ~__builtin_bitreverse64(word);
   }
   key0[i] = k0;
   key1[i] = k1;
+  key2[i] = k2;
   ones[i] = c;
 }
 
-// (key0, key1, token) order; when the first two words agree, the later words
-// of the packed paths decide (lowest differing bit set first), then the token
-// index. Indices >= N are padding and compare by index alone.
-__device__ __forceinline__ bool key_less(uint64_t a0, uint64_t a1, int ia, uint64_t b0,
-                                         uint64_t b1, int ib, const uint64_t* __restrict__ bits,
-                                         int W, int N) {
-  if (a0 != b0) return a0 < b0;
-  if (a1 != b1) return a1 < b1;
-  if (W > 2 && ia < N && ib < N) {
+// (key0, key1, key2, token) order; when the first three words agree, the
+// later words of the packed paths decide (lowest differing bit set first),
+// then the token index. Indices >= N are padding and compare by index alone.
+struct SKey {
+  uint64_t k0, k1, k2;
+  int32_t idx;
+};
+__device__ __forceinline__ bool key_less(const SKey& a, const SKey& b,
+                                         const uint64_t* __restrict__ bits, int W, int N) {
+  if (a.k0 != b.k0) return a.k0 < b.k0;
+  if (a.k1 != b.k1) return a.k1 < b.k1;
+  if (a.k2 != b.k2) return a.k2 < b.k2;
+  const int ia = a.idx, ib = b.idx;
+  if (ia == ib) return false;                    // a token against itself
+  if (W > 3 && ia < N && ib < N) {
+    // eight words of each path per round trip
     const uint64_t* pa = bits + (int64_t)ia * W;
     const uint64_t* pb = bits + (int64_t)ib * W;
-    for (int w = 2; w < W; ++w) {
-      const uint64_t a = pa[w];
-      const uint64_t d = a ^ pb[w];
-      if (d) return (a & lowbit(d)) != 0;
+    for (int w0 = 3; w0 < W; w0 += 8) {
+      uint64_t va[8], vb[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        va[u] = w0 + u < W ? pa[w0 + u] : 0ull;
+        vb[u] = w0 + u < W ? pb[w0 + u] : 0ull;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint64_t d = va[u] ^ vb[u];
+        if (d) return (va[u] & lowbit(d)) != 0;
+      }
     }
   }
   return ia < ib;
@@ -185,10 +224,11 @@ __device__ __forceinline__ bool key_less(uint64_t a0, uint64_t a1, int ia, uint6
 // with keys that sort last).
 __global__ void __launch_bounds__(kSortT)
 sch_sort_chunks(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ key1,
-                const uint64_t* __restrict__ bits, int N, int W, uint64_t* __restrict__ s0,
-                uint64_t* __restrict__ s1, int32_t* __restrict__ sidx) {
+                const uint64_t* __restrict__ key2, const uint64_t* __restrict__ bits, int N,
+                int W, uint64_t* __restrict__ s0, uint64_t* __restrict__ s1,
+                uint64_t* __restrict__ s2, int32_t* __restrict__ sidx) {
   static_assert(kChunk == 2 * kSortT, "one compare-exchange per thread and step");
-  __shared__ uint64_t a0[kChunk], a1[kChunk];
+  __shared__ uint64_t a0[kChunk], a1[kChunk], a2[kChunk];
   __shared__ int32_t ai[kChunk];
   const int c0 = blockIdx.x * kChunk;
   const int cn = min(kChunk, N - c0);
@@ -196,6 +236,7 @@ sch_sort_chunks(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ 
     const bool real = p < cn;
     a0[p] = real ? key0[c0 + p] : ~0ull;
     a1[p] = real ? key1[c0 + p] : ~0ull;
+    a2[p] = real ? key2[c0 + p] : ~0ull;
     ai[p] = real ? c0 + p : INT32_MAX;
   }
   __syncthreads();
@@ -205,12 +246,10 @@ sch_sort_chunks(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ 
       const int x = ((t & ~(j - 1)) << 1) | (t & (j - 1));   // bit j of x clear
       const int y = x + j;
       const bool up = (x & kk) == 0;
-      const uint64_t x0 = a0[x], x1 = a1[x], y0 = a0[y], y1 = a1[y];
-      const int xi = ai[x], yi = ai[y];
-      const bool y_first = key_less(y0, y1, yi, x0, x1, xi, bits, W, N);
-      if (y_first == up) {                         // pairs are disjoint within a step
-        a0[x] = y0; a1[x] = y1; ai[x] = yi;
-        a0[y] = x0; a1[y] = x1; ai[y] = xi;
+      const SKey kx{a0[x], a1[x], a2[x], ai[x]}, ky{a0[y], a1[y], a2[y], ai[y]};
+      if (key_less(ky, kx, bits, W, N) == up) {    // pairs are disjoint within a step
+        a0[x] = ky.k0; a1[x] = ky.k1; a2[x] = ky.k2; ai[x] = ky.idx;
+        a0[y] = kx.k0; a1[y] = kx.k1; a2[y] = kx.k2; ai[y] = kx.idx;
       }
       __syncthreads();
     }
@@ -218,6 +257,7 @@ sch_sort_chunks(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ 
   for (int p = threadIdx.x; p < cn; p += kSortT) {
     s0[c0 + p] = a0[p];
     s1[c0 + p] = a1[p];
+    s2[c0 + p] = a2[p];
     sidx[c0 + p] = ai[p];
   }
 }
@@ -225,23 +265,25 @@ sch_sort_chunks(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ 
 // part[g][i] = #{tokens before i} summed over the sorted chunks of group g
 // (chunks g, g + G, g + 2G, ...): each chunk is staged in LDS and searched
 // with a branch-free lower bound.
-__global__ void __launch_bounds__(kSortT)
+__global__ void __launch_bounds__(kMergeT)
 sch_merge_rank(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ key1,
-               const uint64_t* __restrict__ bits, int N, int W, int nchunks,
-               const uint64_t* __restrict__ s0, const uint64_t* __restrict__ s1,
+               const uint64_t* __restrict__ key2, const uint64_t* __restrict__ bits, int N,
+               int W, int nchunks, const uint64_t* __restrict__ s0,
+               const uint64_t* __restrict__ s1, const uint64_t* __restrict__ s2,
                const int32_t* __restrict__ sidx, int32_t* __restrict__ part) {
-  __shared__ uint64_t a0[kChunk], a1[kChunk];
+  __shared__ uint64_t a0[kChunk], a1[kChunk], a2[kChunk];
   __shared__ int32_t ai[kChunk];
-  const int i = blockIdx.x * kSortT + threadIdx.x;
-  const uint64_t x0 = i < N ? key0[i] : 0ull, x1 = i < N ? key1[i] : 0ull;
+  const int i = blockIdx.x * kMergeT + threadIdx.x;
+  const SKey me{i < N ? key0[i] : 0ull, i < N ? key1[i] : 0ull, i < N ? key2[i] : 0ull, i};
   int cnt = 0;
   for (int c = blockIdx.y; c < nchunks; c += gridDim.y) {
     const int c0 = c * kChunk;
     const int cn = min(kChunk, N - c0);
     __syncthreads();
-    for (int p = threadIdx.x; p < cn; p += kSortT) {
+    for (int p = threadIdx.x; p < cn; p += kMergeT) {
       a0[p] = s0[c0 + p];
       a1[p] = s1[c0 + p];
+      a2[p] = s2[c0 + p];
       ai[p] = sidx[c0 + p];
     }
     __syncthreads();
@@ -249,7 +291,8 @@ sch_merge_rank(const uint64_t* __restrict__ key0, const uint64_t* __restrict__ k
       int lo = 0;
       for (int step = kChunk; step > 0; step >>= 1) {
         const int m = lo + step - 1;
-        if (lo + step <= cn && key_less(a0[m], a1[m], ai[m], x0, x1, i, bits, W, N)) lo += step;
+        if (lo + step <= cn && key_less(SKey{a0[m], a1[m], a2[m], ai[m]}, me, bits, W, N))
+          lo += step;
       }
       cnt += lo;
     }
@@ -477,26 +520,32 @@ sch_select(int N, int n1, int nbins, int off, const int32_t* __restrict__ delta,
 
 // ------------------------------------------------ cooperative round loop
 // All rounds in one cooperative launch (every block resident). Tokens are
-// addressed by signature position r: block b owns a contiguous range of
-// positions and keeps its per-position state (delta, batch) in memory that
-// only the owning thread touches, so ties are broken by position directly.
-// Data that crosses blocks is written with device-scope atomics (sums, minima)
-// or agent-scope atomic stores and read with agent-scope atomic loads; phases
-// are separated by a grid barrier on a monotonic arrival counter, with an
-// agent-scope release fence before a block arrives and an acquire fence after
-// the wait (the XCD L2s are not coherent with each other). Every barrier wait
+// addressed by signature position r: block b owns a contiguous range of at
+// most PPT * kCoopT positions, thread t positions t0 + t + j kCoopT (j < PPT),
+// and keeps their state (delta, batch) in registers and their path words in
+// LDS when they fit, so ties are broken by position directly. Data that
+// crosses blocks is written with device-scope atomics (sums, minima) or
+// agent-scope atomic stores and read with agent-scope atomic loads -- never
+// with plain accesses, since the XCD L2s are not coherent with each other --
+// and phases are separated by a grid barrier on a monotonic arrival counter
+// that orders those operations (see grid_sync). Every barrier wait
 // is bounded: past the bound the block records an error and goes on, so the
 // launch always terminates (the result is then flagged, never trusted).
-// Candidates are packed as (value << 24 | position) and reduced with a 64-bit
-// atomicMin, which keeps the lower-position tie rule. A round needs three
+// Candidates are packed as (value << 24 | position); their minimum keeps the
+// lower-position tie rule. A round needs three
 // barriers: after the histogram, after the assignment, after the candidates.
 constexpr int kCoopT = 256;
 constexpr int kCoopMaxLE = 8192;
 constexpr int kCoopMaxBins = 4096;
 constexpr int kCoopMaxBlocks = 1024;
+constexpr int kCoopMaxPPT = 4;
+constexpr size_t kCoopMaxLds = 160 * 1024 - 2048;   // dynamic LDS limit (static part aside)
 constexpr unsigned kSpinBound = 1u << 20;
 
 __device__ __forceinline__ int ld_ag(const int32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned ld_ag(const unsigned* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ unsigned long long ld_ag64(const unsigned long long* p) {
@@ -510,16 +559,19 @@ __device__ __forceinline__ void st_ag64(unsigned long long* p, unsigned long lon
 }
 
 __device__ void grid_sync(unsigned* bar, unsigned nblk, int32_t* err) {
-  // Release: every wave waits for its own stores and atomics and writes the
-  // XCD's L2 back, so the arrival below is ordered after all of them (a
-  // workgroup barrier alone does not wait for other waves' memory traffic).
-  __threadfence();
+  // Every datum that crosses blocks inside the launch is read and written with
+  // agent-scope atomic operations, which are performed coherently across the
+  // XCDs (they bypass the XCD-local caches), so the barrier only has to order
+  // them: each wave waits until its own memory operations have completed, then
+  // one thread arrives and polls. No cache write-back or invalidation is
+  // needed -- those cost a serialised L2 operation per wave and block.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (threadIdx.x == 0) {
     const unsigned arrived = atomicAdd(bar, 1u) + 1u;
     const unsigned target = (arrived + nblk - 1u) / nblk * nblk;
     unsigned spins = 0;
-    while (atomicAdd(bar, 0u) < target) {
+    while (ld_ag(bar) < target) {
       __builtin_amdgcn_s_sleep(1);
       if (++spins == kSpinBound) {
         atomicExch(err, 1);
@@ -528,7 +580,6 @@ __device__ void grid_sync(unsigned* bar, unsigned nblk, int32_t* err) {
     }
   }
   __syncthreads();
-  __threadfence();                               // acquire: drop stale cached lines
 }
 
 __device__ __forceinline__ unsigned long long wave_min_u64(unsigned long long v) {
@@ -543,27 +594,51 @@ struct CoopArgs {
   const uint64_t* bits_s;   // [W][N] paths in signature order
   const int32_t* ones_s;    // [N] path sizes in signature order
   const int32_t* order;     // [N] token at each signature position
-  int N, W, LE, n1, nbins, off, max_iters, twoLk;
-  int32_t* delta_s;         // [N] by position (owning thread only)
-  int32_t* in1_s;           // [N] by position (owning thread only)
+  const uint8_t* routes;    // [N][L k] route ids by token
+  int N, W, LE, n1, nbins, off, max_iters, twoLk, bits_lds, rt_lds, E, k, Lk, L;
   int32_t* in1;             // [N] by token: the final batch-1 flags
   int32_t* hist;            // [2][nbins] global histograms of alternate rounds
   int32_t* hpart;           // [gridDim][nbins] per-block histograms
   int32_t* cnt;             // [LE] batch-1 column counts
   int32_t* cnt_orig;        // [2][LE] column counts of the input split
   unsigned long long* tot;  // [4]: [0] batch-1 path-size sum, [2..3] input split
-  unsigned long long* cand; // [8]: m1, m2 of the start, then 3 slots of 2
+  unsigned long long* cand; // [4][2][gridDim]: per-block candidates, 3 round slots + start
   unsigned* bar;
   int32_t* err;
   int64_t* state;
 };
 
+// Dynamic LDS of the cooperative kernel: the two medoids' words (2 W), the
+// block's own path words (PPT W kCoopT) when bits_lds and route ids
+// (PPT L k kCoopT bytes) when rt_lds, batch counts (2 LE), all-token counts
+// (LE), histogram (nbins).
+struct CoopLds {
+  size_t c, all, h, med, bits, rt, cb, total;
+};
+__host__ __device__ inline CoopLds coop_lds(int LE, int nbins, int W, int Lk, int ppt,
+                                           bool bits_lds, bool rt_lds) {
+  CoopLds s{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = (o + bytes + 15) / 16 * 16;
+    return at;
+  };
+  s.med = take(2 * (size_t)W * 8);
+  s.bits = take(bits_lds ? (size_t)ppt * W * kCoopT * 8 : 0);
+  s.rt = take(rt_lds ? (size_t)ppt * Lk * kCoopT : 0);
+  s.cb = take(rt_lds ? (size_t)Lk * 4 : 0);
+  s.c = take(2 * (size_t)LE * 4);
+  s.all = take((size_t)LE * 4);
+  s.h = take((size_t)nbins * 4);
+  s.total = o;
+  return s;
+}
+
+template <int PPT>
 __global__ void __launch_bounds__(kCoopT)
 sch_coop(CoopArgs a) {
-  __shared__ int32_t s_c[2 * kCoopMaxLE];        // batch counts / signed count changes
-  __shared__ int32_t s_all[kCoopMaxLE];          // column counts over all tokens
-  __shared__ int32_t s_h[kCoopMaxBins];
-  __shared__ uint64_t s_med[2][kCoopMaxLE / 64];
+  extern __shared__ __attribute__((aligned(16))) char smem[];
   __shared__ unsigned long long s_red[kCoopT / kWave];
   __shared__ unsigned long long s_tot[2];
   __shared__ int s_thr, s_q;
@@ -571,10 +646,108 @@ sch_coop(CoopArgs a) {
   const int lane = lane_id();
   const unsigned nblk = gridDim.x;
   const int N = a.N, W = a.W, LE = a.LE, nbins = a.nbins, off = a.off, n1 = a.n1;
+  const bool bits_lds = a.bits_lds != 0, rt_lds = a.rt_lds != 0;
+  const int Lk = a.Lk;
+  const CoopLds L = coop_lds(LE, nbins, W, Lk, PPT, bits_lds, rt_lds);
+  int32_t* s_c = reinterpret_cast<int32_t*>(smem + L.c);
+  int32_t* s_all = reinterpret_cast<int32_t*>(smem + L.all);
+  int32_t* s_h = reinterpret_cast<int32_t*>(smem + L.h);
+  uint64_t* s_med = reinterpret_cast<uint64_t*>(smem + L.med);      // [2][W]
+  uint64_t* s_bits = reinterpret_cast<uint64_t*>(smem + L.bits);    // [PPT][W][kCoopT]
+  uint8_t* s_rt = reinterpret_cast<uint8_t*>(smem + L.rt);          // [PPT][L k][kCoopT]
+  int32_t* s_cb = reinterpret_cast<int32_t*>(smem + L.cb);          // [L k] first column of the id's layer
   const int per = (N + (int)nblk - 1) / (int)nblk;
   const int t0 = min(N, (int)blockIdx.x * per), t1 = min(N, t0 + per);
+  int pos[PPT];
+  bool own[PPT];
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) {
+    pos[j] = t0 + tid + j * kCoopT;
+    own[j] = pos[j] < t1;
+  }
 
-  auto word = [&](int r, int w) { return a.bits_s[(int64_t)w * N + r]; };
+  auto gword = [&](int r, int w) { return a.bits_s[(int64_t)w * N + r]; };
+  auto word = [&](int j, int w) {
+    return bits_lds ? s_bits[((int64_t)j * W + w) * kCoopT + tid] : gword(pos[j], w);
+  };
+  const int rot0 = rt_lds ? (lane % a.L) * a.k : 0;
+  // The columns of a path: from its route ids staged in LDS (a loop of fixed
+  // length L k, ids >= E skipped), else from the set bits of its words.
+  auto for_cols = [&](int j, auto&& f) {
+    if (rt_lds) {
+      // Eight ids per round trip, every access unconditional (clamped index,
+      // masked use) so that the loads issue back to back. Lane l starts at
+      // layer l mod L: neighbouring positions hold similar routes, and their
+      // LDS atomics would otherwise hit the same column together.
+      const uint8_t* rt = s_rt + (int64_t)j * Lk * kCoopT + tid;
+      int q = rot0;
+      for (int q0 = 0; q0 < Lk; q0 += 8) {
+        int e[8], base[8];
+        bool in[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          in[u] = q0 + u < Lk;
+          const int qq = q + u < Lk ? q + u : q + u - Lk;
+          const int qc = in[u] ? qq : 0;
+          e[u] = rt[qc * kCoopT];
+          base[u] = s_cb[qc];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const bool ok = in[u] && e[u] < a.E;
+          f(ok ? base[u] + e[u] : 0, ok);
+        }
+        q += 8;
+        q -= q >= Lk ? Lk : 0;
+      }
+    } else {
+      for (int w = 0; w < W; ++w) {
+        uint64_t x = word(j, w);
+        while (x) {
+          f(w * 64 + __builtin_ctzll(x), true);
+          x &= x - 1;
+        }
+      }
+    }
+  };
+  if (bits_lds) {                                // eight words per round trip
+#pragma unroll
+    for (int j = 0; j < PPT; ++j)
+      for (int w0 = 0; w0 < W; w0 += 8) {
+        uint64_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = (own[j] && w0 + u < W) ? gword(pos[j], w0 + u) : 0ull;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (w0 + u < W) s_bits[((int64_t)j * W + w0 + u) * kCoopT + tid] = v[u];
+      }
+  }
+  if (rt_lds) {                                  // each token's ids, transposed
+    for (int q = tid; q < Lk; q += kCoopT) s_cb[q] = (q / a.k) * a.E;
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+      const uint8_t* src = own[j] ? a.routes + (int64_t)a.order[pos[j]] * Lk : nullptr;
+      uint8_t* dst = s_rt + (int64_t)j * Lk * kCoopT + tid;
+      if ((Lk & 3) == 0 && (reinterpret_cast<uintptr_t>(a.routes) & 3) == 0) {
+        for (int q0 = 0; q0 < Lk; q0 += 32) {        // eight 4-byte loads per round trip
+          uint32_t v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            v[u] = (src && q0 + 4 * u < Lk) ? *reinterpret_cast<const uint32_t*>(src + q0 + 4 * u) : 0xFFFFFFFFu;
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            if (q0 + 4 * u < Lk)
+#pragma unroll
+              for (int b = 0; b < 4; ++b) dst[(q0 + 4 * u + b) * kCoopT] = (uint8_t)(v[u] >> (8 * b));
+        }
+      } else {
+        for (int q = 0; q < Lk; ++q) dst[q * kCoopT] = src ? src[q] : 0xFF;
+      }
+    }
+  }
+  int ones[PPT];
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) ones[j] = own[j] ? a.ones_s[pos[j]] : 0;
 
   auto block_min_u64 = [&](unsigned long long v) {
     v = wave_min_u64(v);
@@ -585,19 +758,58 @@ sch_coop(CoopArgs a) {
     __syncthreads();
     return r;
   };
+  // Candidates: every block stores its minimum in its own entry of a slot
+  // (no contended atomics); after the barrier every block reduces the slot.
+  auto cand_slot = [&](int slot, int c) { return a.cand + ((int64_t)slot * 2 + c) * nblk; };
+  auto put_cand = [&](int slot, int c, unsigned long long v) {
+    if (tid == 0) st_ag64(cand_slot(slot, c) + blockIdx.x, v);
+  };
+  auto min_cand = [&](int slot, int c) {
+    const unsigned long long* p = cand_slot(slot, c);
+    unsigned long long v = ~0ull;
+    for (int b = tid; b < (int)nblk; b += kCoopT) {
+      const unsigned long long x = ld_ag64(p + b);
+      v = x < v ? x : v;
+    }
+    return block_min_u64(v);
+  };
 
-  // (sum_j in batch d(r, j)) << 24 | r under the counts cc of that batch
-  auto dist_key = [&](int r, const int32_t* cc, int64_t size, unsigned long long tot) {
-    int64_t g = 0;
-    for (int w = 0; w < W; ++w) {
-      uint64_t x = word(r, w);
-      while (x) {
-        g += cc[w * 64 + __builtin_ctzll(x)];
+  // sum of cc over the set bits of x, four gathers in flight (absent bits
+  // read cc[0] and add nothing)
+  auto gather = [](uint64_t x, const int32_t* cc) -> int {
+    int g = 0;
+    while (x) {
+      int b[4];
+      bool has[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        has[u] = x != 0;
+        b[u] = has[u] ? __builtin_ctzll(x) : 0;
         x &= x - 1;
       }
+      int v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = cc[b[u]];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) g += has[u] ? v[u] : 0;
     }
-    const int64_t D = size * a.ones_s[r] + (int64_t)tot - 2 * g;
-    return ((unsigned long long)D << 24) | (unsigned long long)r;
+    return g;
+  };
+  // (sum_j in batch d(r, j)) << 24 | r under the counts cc of that batch
+  auto dist_key = [&](int j, const int32_t* cc, int64_t size, unsigned long long tot) {
+    int64_t g = 0;
+    if (rt_lds) {
+      int gi = 0;
+      for_cols(j, [&](int col, bool ok) {
+        const int v = cc[col];
+        gi += ok ? v : 0;
+      });
+      g = gi;
+    } else {
+      for (int w = 0; w < W; ++w) g += gather(word(j, w), cc + w * 64);
+    }
+    const int64_t D = size * ones[j] + (int64_t)tot - 2 * g;
+    return ((unsigned long long)D << 24) | (unsigned long long)pos[j];
   };
   auto decode = [&](unsigned long long key) {
     const int r = (int)(key & 0xFFFFFF);
@@ -608,17 +820,13 @@ sch_coop(CoopArgs a) {
   for (int q = tid; q < 2 * LE; q += kCoopT) s_c[q] = 0;
   if (tid < 2) s_tot[tid] = 0;
   __syncthreads();
-  for (int r = t0 + tid; r < t1; r += kCoopT) {
-    const int c = a.order[r] < n1 ? 0 : 1;
-    for (int w = 0; w < W; ++w) {
-      uint64_t x = word(r, w);
-      while (x) {
-        atomicAdd(&s_c[c * LE + w * 64 + __builtin_ctzll(x)], 1);
-        x &= x - 1;
-      }
-    }
-    atomicAdd(&s_tot[c], (unsigned long long)a.ones_s[r]);
-    a.in1_s[r] = 0;
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) {
+    if (!own[j]) continue;
+    const int c = a.order[pos[j]] < n1 ? 0 : 1;
+    int32_t* dst = s_c + c * LE;
+    for_cols(j, [&](int col, bool ok) { atomicAdd(&dst[col], ok ? 1 : 0); });
+    atomicAdd(&s_tot[c], (unsigned long long)ones[j]);
   }
   __syncthreads();
   for (int q = tid; q < 2 * LE; q += kCoopT)
@@ -632,58 +840,65 @@ sch_coop(CoopArgs a) {
   __syncthreads();
   {
     unsigned long long best = ~0ull;
-    for (int r = t0 + tid; r < t1; r += kCoopT) {
-      const unsigned long long key = dist_key(r, s_all, N, tot_all);
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+      if (!own[j]) continue;
+      const unsigned long long key = dist_key(j, s_all, N, tot_all);
       best = key < best ? key : best;
     }
-    best = block_min_u64(best);
-    if (tid == 0) atomicMin(&a.cand[0], best);
+    put_cand(3, 0, block_min_u64(best));
   }
   grid_sync(a.bar, nblk, a.err);
-  int m1 = decode(ld_ag64(a.cand));
-  for (int w = tid; w < W; w += kCoopT) s_med[0][w] = word(m1, w);
+  int m1 = decode(min_cand(3, 0));
+  for (int w = tid; w < W; w += kCoopT) s_med[w] = gword(m1, w);
   __syncthreads();
   // ---- m2: farthest from m1, as a minimum of (2Lk - d, position)
   {
     unsigned long long best = ~0ull;
-    for (int r = t0 + tid; r < t1; r += kCoopT) {
-      if (r == m1) continue;
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+      if (!own[j] || pos[j] == m1) continue;
       int d = 0;
-      for (int w = 0; w < W; ++w) d += __popcll(word(r, w) ^ s_med[0][w]);
-      const unsigned long long key = ((unsigned long long)(a.twoLk - d) << 24) | (unsigned long long)r;
+      for (int w = 0; w < W; ++w) d += __popcll(word(j, w) ^ s_med[w]);
+      const unsigned long long key = ((unsigned long long)(a.twoLk - d) << 24) | (unsigned long long)pos[j];
       best = key < best ? key : best;
     }
-    best = block_min_u64(best);
-    if (tid == 0) atomicMin(&a.cand[1], best);
+    put_cand(3, 1, block_min_u64(best));
   }
   grid_sync(a.bar, nblk, a.err);
-  int m2 = decode(ld_ag64(a.cand + 1));
+  int m2 = decode(min_cand(3, 1));
 
+  int delta[PPT], in1[PPT];
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) in1[j] = 0;
   int iters = 0, conv = 0, am1 = m1, am2 = m2;
   for (int it = 1; it <= a.max_iters; ++it) {
     int32_t* hc = a.hist + (it & 1) * nbins;       // this round's histogram
-    unsigned long long* cs = a.cand + 2 + 2 * (it % 3);
+    const int cslot = it % 3;
     // A: delta for own positions, block histogram; clear the next round's
     // histogram and candidate slots (last read two barriers ago)
+    __syncthreads();                              // s_med of the previous medoids is free
     for (int w = tid; w < W; w += kCoopT) {
-      s_med[0][w] = word(m1, w);
-      s_med[1][w] = word(m2, w);
+      s_med[w] = gword(m1, w);
+      s_med[W + w] = gword(m2, w);
     }
     for (int v = tid; v < nbins; v += kCoopT) s_h[v] = 0;
     __syncthreads();
-    for (int r = t0 + tid; r < t1; r += kCoopT) {
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
+      delta[j] = 0;
+      if (!own[j]) continue;
       int d = 0;
       for (int w = 0; w < W; ++w) {
-        const uint64_t x = word(r, w);
-        d += __popcll(x ^ s_med[0][w]) - __popcll(x ^ s_med[1][w]);
+        const uint64_t x = word(j, w);
+        d += __popcll(x ^ s_med[w]) - __popcll(x ^ s_med[W + w]);
       }
-      a.delta_s[r] = d;
+      delta[j] = d;
       atomicAdd(&s_h[d + off], 1);
     }
     {
       int32_t* hn = a.hist + ((it + 1) & 1) * nbins;
       for (int v = blockIdx.x * kCoopT + tid; v < nbins; v += (int)nblk * kCoopT) st_ag(hn + v, 0);
-      if (blockIdx.x == 0 && tid < 2) st_ag64(a.cand + 2 + 2 * ((it + 1) % 3) + tid, ~0ull);
     }
     __syncthreads();
     {
@@ -697,19 +912,23 @@ sch_coop(CoopArgs a) {
     grid_sync(a.bar, nblk, a.err);
     // B: threshold (every block alike), ties of lower blocks, assignment in
     // position order; batch changes update the batch-1 counts
+    for (int v = tid; v < nbins; v += kCoopT) s_h[v] = ld_ag(hc + v);
     if (tid == 0) {                               // defaults that keep indices in range
       s_thr = nbins - 1 - off;
       s_q = n1;
     }
+    for (int q = tid; q < LE; q += kCoopT) s_c[q] = 0;
+    if (tid == 0) s_tot[0] = 0;
+    __syncthreads();
     {
       const int pb = (nbins + kCoopT - 1) / kCoopT;
       const int v0 = min(nbins, tid * pb), v1 = min(nbins, v0 + pb);
       int local = 0;
-      for (int v = v0; v < v1; ++v) local += ld_ag(hc + v);
+      for (int v = v0; v < v1; ++v) local += s_h[v];
       int total;
       int cum = block_excl_scan<kCoopT>(local, &total);
       for (int v = v0; v < v1; ++v) {
-        const int h = ld_ag(hc + v);
+        const int h = s_h[v];
         if (cum < n1 && cum + h >= n1) {
           s_thr = v - off;
           s_q = n1 - cum;
@@ -717,8 +936,6 @@ sch_coop(CoopArgs a) {
         cum += h;
       }
     }
-    for (int q = tid; q < LE; q += kCoopT) s_c[q] = 0;
-    if (tid == 0) s_tot[0] = 0;
     __syncthreads();
     const int thr = s_thr, q = s_q;
     int pre;
@@ -729,25 +946,18 @@ sch_coop(CoopArgs a) {
       block_excl_scan<kCoopT>(lower, &total);
       pre = total;
     }
-    for (int base = t0; base < t1; base += kCoopT) {
-      const int r = base + tid;
-      const bool own = r < t1;
-      const int d = own ? a.delta_s[r] : 0;
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) {
       int ties;
-      const int x = block_excl_scan<kCoopT>(own && d == thr ? 1 : 0, &ties);
-      if (own) {
+      const int x = block_excl_scan<kCoopT>(own[j] && delta[j] == thr ? 1 : 0, &ties);
+      if (own[j]) {
+        const int d = delta[j];
         const int nw = d < thr ? 1 : (d > thr ? 0 : (pre + x < q ? 1 : 0));
-        if (nw != a.in1_s[r]) {
+        if (nw != in1[j]) {
           const int sgn = nw ? 1 : -1;
-          for (int w = 0; w < W; ++w) {
-            uint64_t y = word(r, w);
-            while (y) {
-              atomicAdd(&s_c[w * 64 + __builtin_ctzll(y)], sgn);
-              y &= y - 1;
-            }
-          }
-          atomicAdd(&s_tot[0], (unsigned long long)(int64_t)(sgn * a.ones_s[r]));
-          a.in1_s[r] = nw;
+          for_cols(j, [&](int col, bool ok) { atomicAdd(&s_c[col], ok ? sgn : 0); });
+          atomicAdd(&s_tot[0], (unsigned long long)(int64_t)(sgn * ones[j]));
+          in1[j] = nw;
         }
       }
       pre += ties;
@@ -774,23 +984,21 @@ sch_coop(CoopArgs a) {
     __syncthreads();
     {
       unsigned long long b0 = ~0ull, b1 = ~0ull;
-      for (int r = t0 + tid; r < t1; r += kCoopT) {
-        const int c = a.in1_s[r] ? 0 : 1;
-        const unsigned long long key = dist_key(r, s_c + c * LE, c == 0 ? n1 : N - n1, s_tot[c]);
+#pragma unroll
+      for (int j = 0; j < PPT; ++j) {
+        if (!own[j]) continue;
+        const int c = in1[j] ? 0 : 1;
+        const unsigned long long key = dist_key(j, s_c + c * LE, c == 0 ? n1 : N - n1, s_tot[c]);
         if (c == 0) b0 = key < b0 ? key : b0;
         else b1 = key < b1 ? key : b1;
       }
-      b0 = block_min_u64(b0);
-      b1 = block_min_u64(b1);
-      if (tid == 0) {
-        atomicMin(cs, b0);
-        atomicMin(cs + 1, b1);
-      }
+      put_cand(cslot, 0, block_min_u64(b0));
+      put_cand(cslot, 1, block_min_u64(b1));
     }
     grid_sync(a.bar, nblk, a.err);
     // D: new centroids; stop when they repeat (same decision in every block)
-    const int n1c = decode(ld_ag64(cs));
-    const int n2c = decode(ld_ag64(cs + 1));
+    const int n1c = decode(min_cand(cslot, 0));
+    const int n2c = decode(min_cand(cslot, 1));
     if (n1c == m1 && n2c == m2) {
       conv = 1;
       break;
@@ -798,7 +1006,9 @@ sch_coop(CoopArgs a) {
     m1 = n1c;
     m2 = n2c;
   }
-  for (int r = t0 + tid; r < t1; r += kCoopT) a.in1[a.order[r]] = a.in1_s[r];
+#pragma unroll
+  for (int j = 0; j < PPT; ++j)
+    if (own[j]) a.in1[a.order[pos[j]]] = in1[j];
   if (blockIdx.x == 0 && tid == 0) {
     a.state[ST_ITERS] = iters;
     a.state[ST_CONV] = conv;
@@ -913,8 +1123,8 @@ sch_fin_scatter(int N, int n1, int LE, int trivial, const int32_t* __restrict__ 
 }
 
 struct SchLayout {
-  size_t bits, bits_s, key0, key1, skey0, skey1, sidx, part, ones, ones_s, rank, order, delta,
-      in1, in1_s, cnt, cnt_orig, hist, hpart, tot, state, cand, cand8, blkcnt, bar, total;
+  size_t bits, bits_s, key0, key1, key2, skey0, skey1, skey2, sidx, part, ones, ones_s, rank, order, delta,
+      in1, cnt, cnt_orig, hist, hpart, tot, state, cand, cand8, blkcnt, bar, total;
 };
 
 int rank_groups(int64_t N) {
@@ -943,8 +1153,10 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
   s.bits_s = take(coop_blocks ? N * W * 8 : 0);
   s.key0 = take(N * 8);
   s.key1 = take(N * 8);
+  s.key2 = take(N * 8);
   s.skey0 = take(N * 8);
   s.skey1 = take(N * 8);
+  s.skey2 = take(N * 8);
   s.sidx = take(N * 4);
   s.part = take((size_t)rank_groups(N) * N * 4);
   s.ones = take(N * 4);
@@ -953,7 +1165,6 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
   s.order = take(N * 4);
   s.delta = take(N * 4);
   s.in1 = take(N * 4);
-  s.in1_s = take(N * 4);
   s.cnt = take(2 * LE * 4);
   s.cnt_orig = take(2 * LE * 4);
   s.hist = take(2 * nbins * 4);
@@ -961,7 +1172,7 @@ SchLayout sch_layout(int64_t N, int32_t L, int32_t E, int32_t k) {
   s.tot = take(4 * 8);
   s.state = take(ST_NWORDS * 8);
   s.cand = take(nblk * 2 * sizeof(Cand));
-  s.cand8 = take(8 * 8);
+  s.cand8 = take(8 * 8 * (size_t)std::max<int64_t>(1, coop_blocks));
   s.blkcnt = take(ceil_div(N, kSel) * 4);
   s.bar = take(2 * 4);                    // arrival counter, error flag
   s.total = o;
@@ -996,8 +1207,10 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   auto* bits_s = reinterpret_cast<uint64_t*>(ws + lay.bits_s);
   auto* key0 = reinterpret_cast<uint64_t*>(ws + lay.key0);
   auto* key1 = reinterpret_cast<uint64_t*>(ws + lay.key1);
+  auto* key2 = reinterpret_cast<uint64_t*>(ws + lay.key2);
   auto* skey0 = reinterpret_cast<uint64_t*>(ws + lay.skey0);
   auto* skey1 = reinterpret_cast<uint64_t*>(ws + lay.skey1);
+  auto* skey2 = reinterpret_cast<uint64_t*>(ws + lay.skey2);
   auto* sidx = reinterpret_cast<int32_t*>(ws + lay.sidx);
   auto* part = reinterpret_cast<int32_t*>(ws + lay.part);
   auto* ones = reinterpret_cast<int32_t*>(ws + lay.ones);
@@ -1006,7 +1219,6 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   auto* order = reinterpret_cast<int32_t*>(ws + lay.order);
   auto* delta = reinterpret_cast<int32_t*>(ws + lay.delta);
   auto* in1 = reinterpret_cast<int32_t*>(ws + lay.in1);
-  auto* in1_s = reinterpret_cast<int32_t*>(ws + lay.in1_s);
   auto* cnt = reinterpret_cast<int32_t*>(ws + lay.cnt);
   auto* cnt_orig = reinterpret_cast<int32_t*>(ws + lay.cnt_orig);
   auto* hist = reinterpret_cast<int32_t*>(ws + lay.hist);
@@ -1033,19 +1245,23 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   sch_init<<<dim3((unsigned)std::min<int64_t>(64, ceil_div(std::max(2 * nbins, 2 * LE), kT))), blk,
              0, st>>>(hist, 2 * nbins, cnt_orig, cnt, 2 * LE, tot, cand8, bar, err, state);
   MOE_CHECK_LAUNCH();
-  sch_pack<<<dim3((unsigned)ceil_div(N, kPackT)), dim3(kPackT), 0, st>>>(routes, n, L, E, k, W,
-                                                                         bits, key0, key1, ones);
+  if ((int64_t)kPackT * L * k <= kPackMaxBytes)
+    sch_pack<true><<<dim3((unsigned)ceil_div(N, kPackT)), dim3(kPackT), 0, st>>>(
+        routes, n, L, E, k, W, bits, key0, key1, key2, ones);
+  else
+    sch_pack<false><<<dim3((unsigned)ceil_div(N, kPackT)), dim3(kPackT), 0, st>>>(
+        routes, n, L, E, k, W, bits, key0, key1, key2, ones);
   MOE_CHECK_LAUNCH();
 
   bool done = false;
   if (!trivial) {
     // signature order: sorted chunks, then every token's rank by lower bounds
     const int nchunks = (int)ceil_div(N, kChunk), ngroups = rank_groups(N);
-    sch_sort_chunks<<<dim3(nchunks), dim3(kSortT), 0, st>>>(key0, key1, bits, n, W, skey0, skey1,
-                                                            sidx);
+    sch_sort_chunks<<<dim3(nchunks), dim3(kSortT), 0, st>>>(key0, key1, key2, bits, n, W, skey0,
+                                                            skey1, skey2, sidx);
     MOE_CHECK_LAUNCH();
-    sch_merge_rank<<<dim3((unsigned)ceil_div(N, kSortT), ngroups), dim3(kSortT), 0, st>>>(
-        key0, key1, bits, n, W, nchunks, skey0, skey1, sidx, part);
+    sch_merge_rank<<<dim3((unsigned)ceil_div(N, kMergeT), ngroups), dim3(kMergeT), 0, st>>>(
+        key0, key1, key2, bits, n, W, nchunks, skey0, skey1, skey2, sidx, part);
     MOE_CHECK_LAUNCH();
     sch_rank_sum<<<grid, blk, 0, st>>>(part, ngroups, n, rank, order);
     MOE_CHECK_LAUNCH();
@@ -1055,14 +1271,29 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
       const int cus = device_cu_count();
       const int nb = (int)std::max<int64_t>(
           1, std::min<int64_t>({(int64_t)cus, ceil_div(N, kCoopT), (int64_t)kCoopMaxBlocks}));
-      CoopArgs ca{bits_s, ones_s, order, n, W, LE, (int)n1, nbins, off, max_iters, 2 * L * k,
-                  delta, in1_s, in1, hist, hpart, cnt, cnt_orig, tot, cand8, bar, err, state};
-      void* args[] = {&ca};
-      if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(&sch_coop), dim3(nb),
-                                     dim3(kCoopT), args, 0, st) == hipSuccess)
-        done = true;
-      else
-        (void)hipGetLastError();                 // nothing ran: take the per-phase path
+      const int ppt = (int)ceil_div(ceil_div(N, nb), kCoopT);
+      if (ppt <= kCoopMaxPPT) {
+        const int ppt_t = ppt <= 1 ? 1 : (ppt <= 2 ? 2 : 4);
+        const int Lk = L * k;
+        const bool bits_lds = coop_lds(LE, nbins, W, Lk, ppt_t, true, false).total <= kCoopMaxLds;
+        const bool rt_lds = E <= 255 &&
+            coop_lds(LE, nbins, W, Lk, ppt_t, bits_lds, true).total <= kCoopMaxLds;
+        const size_t lds = coop_lds(LE, nbins, W, Lk, ppt_t, bits_lds, rt_lds).total;
+        CoopArgs ca{bits_s, ones_s, order, routes, n, W, LE, (int)n1, nbins, off, max_iters,
+                    2 * L * k, bits_lds ? 1 : 0, rt_lds ? 1 : 0, E, k, Lk, L, in1, hist, hpart, cnt,
+                    cnt_orig, tot, cand8, bar, err, state};
+        void* args[] = {&ca};
+        const void* fn = ppt_t == 1 ? reinterpret_cast<const void*>(&sch_coop<1>)
+                         : ppt_t == 2 ? reinterpret_cast<const void*>(&sch_coop<2>)
+                                      : reinterpret_cast<const void*>(&sch_coop<4>);
+        if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) ==
+                hipSuccess &&
+            hipLaunchCooperativeKernel(fn, dim3(nb), dim3(kCoopT), args, (unsigned)lds, st) ==
+                hipSuccess)
+          done = true;
+        else
+          (void)hipGetLastError();               // nothing ran: take the per-phase path
+      }
     }
   }
   if (!done) {

@@ -100,3 +100,17 @@ def test_repeated_multiword_paths():
     base = synth.predicted_routes(40, 4, 40, 3, 0.5, 1.0, seed=32)
     pick = np.random.default_rng(33).integers(0, 40, size=2000)
     _check(base[pick], 40)
+
+
+def test_several_positions_per_thread():
+    # more tokens than 256 per compute unit: each thread of the round loop
+    # owns several signature positions
+    routes = synth.predicted_routes(70000, 3, 16, 2, 0.7, 1.0, seed=41)
+    _check(routes, 16)
+
+
+def test_long_paths_read_from_memory():
+    # 32 layers x 256 experts = 128 words per path: the block's paths do not
+    # fit in LDS next to the column counts and are read from memory
+    routes = synth.predicted_routes(3000, 32, 256, 2, 0.7, 1.0, seed=42)
+    _check(routes, 256)
