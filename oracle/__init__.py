@@ -22,6 +22,8 @@ Modules and the passages they follow:
   schedule  -- routing paths (Sec. 3.2), the rebatching objective (Sec. 3.3.1,
                Eq. 2) and its K-means-style approximation (Sec. 3.3.2)
   slots     -- per-layer resident-set rule from predicted demand (Sec. 3.4.1)
+  cache     -- cross-layer slot planning, real-time correction and the LRU
+               baseline of the expert cache engine (Sec. 3.4)
   layer     -- the composed MoE layer and the dense-FFN identity used as a pin
 """
 from .gating import router_logits, topk_select, softmax, gate_weights, route
@@ -31,6 +33,7 @@ from .combine import combine
 from .schedule import (route_bits, eq2_objective, signature_rank, hamming_to,
                        cluster_distance_sums, schedule, batch_accuracy)
 from .slots import plan_slots
+from .cache import plec_order, plec_run, lru_run
 from .layer import moe_layer, dense_ffn
 
 __all__ = [
@@ -38,5 +41,6 @@ __all__ = [
     "permute", "silu", "swiglu", "swiglu_loops", "expert_ffn", "combine",
     "route_bits", "eq2_objective", "signature_rank", "hamming_to",
     "cluster_distance_sums", "schedule", "batch_accuracy", "plan_slots",
+    "plec_order", "plec_run", "lru_run",
     "moe_layer", "dense_ffn",
 ]
