@@ -211,6 +211,58 @@ int moe_combine(const void* y_perm, int32_t dtype, int64_t H, int64_t rows,
                 const void* y_shared, int32_t accumulate, void* y,
                 int32_t* incomplete, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Expert cache engine (Sec. 3.4). Host-side planning over small integer
+ * tables, and the loading of whole experts into device cache slots.
+ *
+ * moe_plec_order -- the load order of PLEC's cross-layer plan (Sec. 3.4.1):
+ *   every (layer, expert) with predicted demand > 0, layers in execution
+ *   order, larger demand first, equal demand lower expert id first.
+ *   demand [L,E] int32 HOST array (tokens predicted to use expert e at
+ *   layer l); items [L*E][2] int32 HOST output of (layer, expert) pairs;
+ *   n_items: their number. Errors: MOE_ERR_ARG on NULL or L, E < 1.
+ *
+ * moe_plec_run -- one batch through all layers under a cache of `budget`
+ *   slots shared by all layers: the cache is filled in load order before the
+ *   first layer; when a layer has run its slots are refilled with the next
+ *   items of later layers; an expert the batch actually uses (actual_demand
+ *   > 0) is a hit if resident, else it is loaded at once (real-time
+ *   correction, Sec. 3.4.2) into a free slot, else over an unused expert of
+ *   the same layer, else over the later-layer item latest in load order
+ *   (queued again), else it is served without caching. All arrays HOST:
+ *   pred_demand, actual_demand [L,E] int32; prefetch [budget][2] int32 output
+ *   (may be NULL with n_prefetch) = the items loaded before the first layer;
+ *   hits, needed [L] int64 outputs; loads = every expert load of the batch.
+ *
+ * moe_lru_run -- the baseline: a fixed cache of `capacity` experts per layer
+ *   with least-recently-used replacement, kept across B batches; a layer's
+ *   used experts are looked up in ascending id. actual_demand [B,L,E] int32
+ *   HOST; hits, needed: totals (HOST int64 outputs).
+ *
+ * moe_load_experts -- copies whole experts into cache slots: for i < n,
+ *   expert expert_ids[i] of the store (w_gate_src, w_up_src [E_store,F,H],
+ *   w_down_src [E_store,H,F], dtype) into slot slot_ids[i] of the cache
+ *   (w_gate, w_up [S,F,H], w_down [S,H,F] DEVICE arrays), as asynchronous
+ *   copies on `stream`. expert_ids, slot_ids: HOST int32 [n]. The store is
+ *   normally pinned host memory (copies from pageable memory are staged and
+ *   do not overlap); any address HIP can copy from is accepted. The caller
+ *   must not let kernels that read a destination slot run concurrently.
+ *   Errors: MOE_ERR_ARG on NULL pointers, ids out of range or a destination
+ *   slot named twice (nothing is enqueued); MOE_ERR_HIP if a copy cannot be
+ *   enqueued.
+ * ---------------------------------------------------------------------- */
+int moe_plec_order(const int32_t* demand, int32_t L, int32_t E, int32_t* items,
+                   int32_t* n_items);
+int moe_plec_run(const int32_t* pred_demand, const int32_t* actual_demand, int32_t L,
+                 int32_t E, int32_t budget, int32_t* prefetch, int32_t* n_prefetch,
+                 int64_t* hits, int64_t* needed, int64_t* loads);
+int moe_lru_run(const int32_t* actual_demand, int32_t B, int32_t L, int32_t E,
+                int32_t capacity, int64_t* hits, int64_t* needed);
+int moe_load_experts(const void* w_gate_src, const void* w_up_src, const void* w_down_src,
+                     int32_t E_store, void* w_gate, void* w_up, void* w_down, int32_t S,
+                     int64_t H, int64_t F, int32_t dtype, const int32_t* expert_ids,
+                     const int32_t* slot_ids, int32_t n, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

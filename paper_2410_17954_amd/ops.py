@@ -53,6 +53,10 @@ def load_library(path=None):
         "moe_expert_ffn": (I32, [P, I32, I64, I64, I64, P, I32, P, I32, P, P, P, P, P, SZ, P]),
         "moe_combine": (I32, [P, I32, I64, I64, P, I64, I64, I32, P, P, P, P, I32, P, I32, P,
                               P, P]),
+        "moe_plec_order": (I32, [P, I32, I32, P, P]),
+        "moe_plec_run": (I32, [P, P, I32, I32, I32, P, P, P, P, P]),
+        "moe_lru_run": (I32, [P, I32, I32, I32, I32, P, P]),
+        "moe_load_experts": (I32, [P, P, P, I32, P, P, P, I32, I64, I64, I32, P, P, I32, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -65,7 +69,8 @@ def load_library(path=None):
 def exported_symbols():
     return ["moe_abi_version", "moe_status_str", "moe_route", "moe_schedule_workspace",
             "moe_schedule", "moe_permute_workspace", "moe_permute",
-            "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine"]
+            "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_plec_order",
+            "moe_plec_run", "moe_lru_run", "moe_load_experts"]
 
 
 def _check(name, status):
@@ -311,3 +316,79 @@ def plan_slots(demand, S):
     for s_idx, e in enumerate(sorted(keyed)):
         slot[e] = s_idx
     return slot
+
+
+# ------------------------------------------------------------- expert cache
+def _host_i32(a):
+    a = np.ascontiguousarray(a, dtype=np.int32)
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def plec_order(demand):
+    """moe_plec_order over demand int [L, E] (host). Returns int32 [n, 2]
+    (layer, expert) in load order."""
+    lib = load_library()
+    d, dp = _host_i32(demand)
+    L, E = d.shape
+    items = np.empty((L * E, 2), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check("moe_plec_order", lib.moe_plec_order(dp, L, E, items.ctypes.data_as(ctypes.c_void_p),
+                                                ctypes.byref(n)))
+    return items[:n.value]
+
+
+def plec_run(pred_demand, actual_demand, budget):
+    """moe_plec_run: one batch under a shared cache of `budget` slots. Returns
+    dict(prefetch int32 [n, 2], hits int64 [L], needed int64 [L], loads)."""
+    lib = load_library()
+    p, pp = _host_i32(pred_demand)
+    a, ap = _host_i32(actual_demand)
+    if p.shape != a.shape:
+        raise ValueError("pred_demand and actual_demand must both be [L, E]")
+    L, E = p.shape
+    pre = np.empty((max(int(budget), 1), 2), dtype=np.int32)
+    npre = ctypes.c_int32(0)
+    hits = np.empty(L, dtype=np.int64)
+    needed = np.empty(L, dtype=np.int64)
+    loads = ctypes.c_int64(0)
+    st = lib.moe_plec_run(pp, ap, L, E, int(budget), pre.ctypes.data_as(ctypes.c_void_p),
+                          ctypes.byref(npre), hits.ctypes.data_as(ctypes.c_void_p),
+                          needed.ctypes.data_as(ctypes.c_void_p), ctypes.byref(loads))
+    _check("moe_plec_run", st)
+    return {"prefetch": pre[:npre.value], "hits": hits, "needed": needed, "loads": loads.value}
+
+
+def lru_run(actual_demands, capacity):
+    """moe_lru_run over actual_demands int [B, L, E]: returns (hits, needed)."""
+    lib = load_library()
+    a, ap = _host_i32(actual_demands)
+    B, L, E = a.shape
+    hits, needed = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check("moe_lru_run", lib.moe_lru_run(ap, B, L, E, int(capacity), ctypes.byref(hits),
+                                          ctypes.byref(needed)))
+    return hits.value, needed.value
+
+
+def load_experts(store, cache, expert_ids, slot_ids, stream=None):
+    """moe_load_experts: store = (w_gate, w_up, w_down) tensors [E_store, ...]
+    (normally pinned host memory), cache = the same three on the device
+    [S, ...]; copies expert expert_ids[i] into slot slot_ids[i] on `stream`."""
+    lib = load_library()
+    sg, su, sd = store
+    cg, cu, cd = cache
+    E_store, F, H = sg.shape
+    S = cg.shape[0]
+    if sd.shape != (E_store, H, F) or cd.shape != (S, H, F) or cg.shape != (S, F, H):
+        raise ValueError("store [E,F,H],[E,F,H],[E,H,F] and cache [S,F,H],[S,F,H],[S,H,F]")
+    _dev(cg, cu, cd)
+    for t in (sg, su, sd):
+        if not t.is_contiguous() or t.dtype != cg.dtype:
+            raise ValueError("store tensors must be contiguous and of the cache's dtype")
+    e, ep = _host_i32(expert_ids)
+    s, sp = _host_i32(slot_ids)
+    if e.shape != s.shape:
+        raise ValueError("expert_ids and slot_ids must have the same length")
+    st = lib.moe_load_experts(_ptr(sg), _ptr(su), _ptr(sd), E_store, _ptr(cg), _ptr(cu),
+                              _ptr(cd), S, H, F, _dtype_code(cg), ep, sp, int(e.shape[0]),
+                              _stream(stream))
+    _check("moe_load_experts", st)

@@ -200,6 +200,25 @@ def predicted_routes(N, L, E, k, keep, s, seed):
     return routes.astype(np.uint8)
 
 
+def predicted_and_actual_routes(N, L, E, k, keep, s, acc, seed):
+    """(actual, predicted) uint8 [N, L, k]: actual routes from the Markov chain
+    of predicted_routes; the prediction keeps each choice with probability
+    acc and otherwise names another expert the token does not use at that
+    layer (a predictor of accuracy ~acc per choice)."""
+    actual = predicted_routes(N, L, E, k, keep, s, seed)
+    g = rng_for(seed, "misc")
+    pred = actual.astype(np.int64).copy()
+    for l in range(L):
+        for j in range(k):
+            flip = g.random(N) >= acc
+            for i in np.nonzero(flip)[0]:
+                used = set(actual[i, l].tolist()) | set(pred[i, l].tolist())
+                free = [e for e in range(E) if e not in used]
+                if free:
+                    pred[i, l, j] = free[int(g.integers(len(free)))]
+    return actual, pred.astype(np.uint8)
+
+
 def route_boost_bias(routes, layer, E, boost, base=None):
     """Per-token bias [N, E] (f32): `boost` on the experts predicted for
     `layer`, plus an optional per-expert base bias."""

@@ -1,0 +1,94 @@
+"""The library's expert-cache planning and simulation (host code, no GPU)
+against the oracle of Sec. 3.4: load order, PLEC runs with correction, LRU,
+and the worked example of Sec. 3.4.1 through the C ABI."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_17954_amd import ops, synth
+from paper_2410_17954_amd.build import library_path
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _demand(routes, E):
+    """tokens using expert e at layer l: [L, E] (input preparation)"""
+    N, L, k = routes.shape
+    d = np.zeros((L, E), np.int64)
+    for l in range(L):
+        for j in range(k):
+            np.add.at(d[l], routes[:, l, j].astype(np.int64), 1)
+    return d
+
+
+@pytest.fixture(scope="module", autouse=True)
+def lib():
+    if not os.path.exists(library_path()):
+        from paper_2410_17954_amd import build
+        build.build(verbose=False)
+    return ops.load_library()
+
+
+def test_worked_example_through_the_abi():
+    g = json.load(open(os.path.join(GOLDEN, "plec_worked_example.json")))
+    r = ops.plec_run(g["pred_demand"], g["pred_demand"], g["budget"])
+    assert r["prefetch"].tolist() == g["prefetch"]
+    assert r["loads"] == g["loads"]
+    assert r["hits"].tolist() == r["needed"].tolist() == [3, 2]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_plec_matches_oracle(seed):
+    g = np.random.default_rng(seed)
+    for _ in range(40):
+        L, E = int(g.integers(1, 7)), int(g.integers(1, 20))
+        pred = (g.random((L, E)) < 0.4) * g.integers(1, 6, size=(L, E))
+        act = np.where(g.random((L, E)) < 0.8, pred, (g.random((L, E)) < 0.3) * 2)
+        budget = int(g.integers(0, L * E + 2))
+        ref = oracle.plec_run(pred.tolist(), act.tolist(), budget)
+        got = ops.plec_run(pred, act, budget)
+        assert [tuple(x) for x in got["prefetch"].tolist()] == ref["prefetch"]
+        assert got["hits"].tolist() == ref["hits"]
+        assert got["needed"].tolist() == ref["needed"]
+        assert got["loads"] == ref["loads"]
+        assert [tuple(x) for x in ops.plec_order(pred).tolist()] == oracle.plec_order(pred.tolist())
+
+
+@pytest.mark.parametrize("capacity", [0, 1, 3, 8])
+def test_lru_matches_oracle(capacity):
+    g = np.random.default_rng(capacity)
+    seq = (g.random((12, 4, 10)) < 0.3).astype(np.int32)
+    assert ops.lru_run(seq, capacity) == oracle.lru_run(seq.tolist(), capacity)
+
+
+def test_hit_ratio_on_predicted_routes():
+    """Fig. 10's comparison on synthetic routes: batches of tokens with
+    Markov routes, a predictor that keeps each choice with probability 0.9,
+    PLEC with a shared budget of CS x L slots against per-layer LRU caches of
+    CS slots. Both implementations agree batch by batch; PLEC's hit ratio is
+    at least the fraction of used experts that were predicted when the budget
+    covers every layer's predicted set."""
+    L, E, k, B, BS, CS = 6, 32, 1, 10, 8, 8
+    act_all, pred_all = synth.predicted_and_actual_routes(B * BS, L, E, k, 0.7, 1.1, 0.9, seed=5)
+    ph = pn = 0
+    acts = []
+    for b in range(B):
+        sl = slice(b * BS, (b + 1) * BS)
+        a = _demand(act_all[sl], E)
+        p = _demand(pred_all[sl], E)
+        acts.append(a)
+        r = ops.plec_run(p, a, CS * L)
+        ref = oracle.plec_run(p.tolist(), a.tolist(), CS * L)
+        assert r["hits"].tolist() == ref["hits"]
+        ph += int(r["hits"].sum())
+        pn += int(r["needed"].sum())
+        if (p > 0).sum(1).max() <= CS * L:
+            predicted_and_used = int(((p > 0) & (a > 0)).sum())
+            assert int(r["hits"].sum()) >= predicted_and_used
+    lh, ln = ops.lru_run(np.stack(acts), CS)
+    assert (lh, ln) == oracle.lru_run(np.stack(acts).tolist(), CS)
+    assert ln == pn
+    assert ph / pn > lh / ln
