@@ -16,23 +16,33 @@ import numpy as np
 from . import ops
 
 
-def correction_slots(counts, slot_of_expert, S):
-    """Host decision: the missed experts and the slots they are loaded into,
-    in rounds when there are more misses than slots to take. counts [E] rows
-    per expert, slot_of_expert [E] (-1 = not resident). Returns a list of
-    (expert_ids, slot_ids) rounds."""
+def correction_plan(counts, slot_of_expert, S):
+    """Host decision: which missed experts are loaded into which slots, in
+    rounds. counts [E] rows per expert, slot_of_expert [E] (-1 = not
+    resident). Two groups of slots take misses: group 0, the slots the
+    resident computation does not read (free, or holding a resident expert
+    the batch does not use), usable at once; group 1, the slots of resident
+    experts the batch uses, usable once the resident experts have been
+    computed. Rounds alternate between the groups, so each round's loads wait
+    only for the computation that last read its slots. Returns a list of
+    (group, expert_ids, slot_ids)."""
     counts = np.asarray(counts)
     slot = np.asarray(slot_of_expert)
     E = counts.shape[0]
     misses = [e for e in range(E) if counts[e] > 0 and slot[e] < 0]
-    used = set(int(slot[e]) for e in range(E) if slot[e] >= 0 and counts[e] > 0)
-    takeable = [s for s in range(S) if s not in used]
-    if misses and not takeable:
-        raise ValueError("every slot holds an expert the batch uses: no slot for the misses")
+    busy = sorted(set(int(slot[e]) for e in range(E) if slot[e] >= 0 and counts[e] > 0))
+    groups = [[s for s in range(S) if s not in set(busy)], busy]
+    if misses and not any(groups):
+        raise ValueError("no cache slot to load the missed experts into")
     rounds = []
-    for i in range(0, len(misses), max(len(takeable), 1)):
-        ex = misses[i:i + len(takeable)]
-        rounds.append((np.array(ex, np.int32), np.array(takeable[:len(ex)], np.int32)))
+    i, g = 0, 0 if groups[0] else 1
+    while i < len(misses):
+        sl = groups[g]
+        if sl:
+            ex = misses[i:i + len(sl)]
+            rounds.append((g, np.array(ex, np.int32), np.array(sl[:len(ex)], np.int32)))
+            i += len(ex)
+        g = 1 - g
     return rounds
 
 
@@ -40,8 +50,11 @@ def run_layer(x, topk_idx, topk_w, E, store, cache, slot_of_expert, token_ids=No
               workspaces=None, copy_stream=None):
     """One MoE layer over the batch `token_ids` with the cache `cache` (device
     (w_gate, w_up, w_down) [S, ...]) holding the experts slot_of_expert maps
-    (host int [E]), correcting misses from `store` (host tensors [E, ...]).
-    Returns (y, info) with info = dict(misses, rounds, incomplete_before)."""
+    (host int [E]), correcting misses from `store` (host tensors [E, ...],
+    pinned for the loads to overlap). The loads overwrite cache slots: on
+    return the cache holds what the last rounds loaded. Returns (y, info)
+    with info = dict(misses, rounds, incomplete) (incomplete: the tokens the
+    resident experts alone did not complete)."""
     torch = ops._torch()
     dev = x.device
     comp = torch.cuda.current_stream()
@@ -49,40 +62,42 @@ def run_layer(x, topk_idx, topk_w, E, store, cache, slot_of_expert, token_ids=No
     n_tokens, k = topk_idx.shape
     T = token_ids.shape[0] if token_ids is not None else n_tokens
     H = x.shape[1]
-    F = cache[0].shape[1]
     S = cache[0].shape[0]
     ws = workspaces or {}
-    perm_ws = ws.get("permute")
-    ffn_ws = ws.get("ffn")
-    offs, rop, por, xp = ops.permute(x, topk_idx, E, token_ids=token_ids, workspace=perm_ws)
-    slot_host = np.asarray(slot_of_expert, dtype=np.int32)
-    slot_dev = torch.from_numpy(slot_host).to(dev)
-    # resident experts first (compute stream)
-    yp = torch.empty((T * k, H), dtype=x.dtype, device=dev)
-    ops.expert_ffn(xp, offs, *cache, slot_of_expert=slot_dev, y_perm=yp, workspace=ffn_ws)
-    # misses need the rows per expert on the host (one small copy)
+    offs, rop, por, xp = ops.permute(x, topk_idx, E, token_ids=token_ids,
+                                     workspace=ws.get("permute"))
+    # the misses need the rows per expert on the host (one small copy)
     counts = torch.diff(offs).cpu().numpy()
-    rounds = correction_slots(counts, slot_host, S)
-    # the first round's loads go to slots the resident experts do not read, so
-    # they run on the copy stream while the resident experts compute
-    done = torch.cuda.Event()
-    done.record(comp)
-    y, inc = ops.combine(yp, topk_idx, topk_w, rop, token_ids=token_ids, slot_of_expert=slot_dev,
-                         y=y)
-    for r, (ex, sl) in enumerate(rounds):
-        if r > 0:
-            copy.wait_event(done)         # the previous round's slots are free again
+    slot_host = np.asarray(slot_of_expert, dtype=np.int32)
+    rounds = correction_plan(counts, slot_host, S)
+    # every slot table goes up in one transfer, before any cross-stream wait
+    tables = np.full((1 + len(rounds), E), -1, np.int32)
+    tables[0] = slot_host
+    for r, (_, ex, sl) in enumerate(rounds):
+        tables[1 + r, ex] = sl
+    tables_dev = torch.from_numpy(tables).pin_memory().to(dev, non_blocking=True)
+    # resident experts (compute stream)
+    yp = torch.empty((T * k, H), dtype=x.dtype, device=dev)
+    ops.expert_ffn(xp, offs, *cache, slot_of_expert=tables_dev[0], y_perm=yp,
+                   workspace=ws.get("ffn"))
+    last_read = [None, torch.cuda.Event()]       # per slot group: its last reader
+    last_read[1].record(comp)
+    y, inc = ops.combine(yp, topk_idx, topk_w, rop, token_ids=token_ids,
+                         slot_of_expert=tables_dev[0], y=y)
+    for r, (g, ex, sl) in enumerate(rounds):
+        if last_read[g] is not None:
+            copy.wait_event(last_read[g])
         ops.load_experts(store, cache, ex, sl, stream=copy)
         loaded = torch.cuda.Event()
         loaded.record(copy)
         comp.wait_event(loaded)
-        miss_slot = np.full(E, -1, np.int32)
-        miss_slot[ex] = sl
-        miss_dev = torch.from_numpy(miss_slot).to(dev)
-        ops.expert_ffn(xp, offs, *cache, slot_of_expert=miss_dev, y_perm=yp, workspace=ffn_ws)
-        ops.combine(yp, topk_idx, topk_w, rop, token_ids=token_ids, slot_of_expert=miss_dev, y=y,
-                    accumulate=True, want_incomplete=False)
+        ops.expert_ffn(xp, offs, *cache, slot_of_expert=tables_dev[1 + r], y_perm=yp,
+                       workspace=ws.get("ffn"))
         done = torch.cuda.Event()
         done.record(comp)
-    return y, {"misses": int(sum(len(ex) for ex, _ in rounds)), "rounds": len(rounds),
+        last_read[g] = done
+        ops.combine(yp, topk_idx, topk_w, rop, token_ids=token_ids,
+                    slot_of_expert=tables_dev[1 + r], y=y, accumulate=True,
+                    want_incomplete=False)
+    return y, {"misses": int(sum(len(ex) for _, ex, _ in rounds)), "rounds": len(rounds),
                "incomplete": inc}

@@ -46,7 +46,8 @@ def test_load_experts_rejects_bad_ids():
 
 @pytest.mark.parametrize("S,resident,rounds", [
     (8, [0, -1, 1, -1, 2, 3, -1, -1], 1),   # four spare slots take the four misses at once
-    (3, [0, 1, -1, -1, -1, -1, -1, -1], 6),  # one spare slot: six rounds of one expert
+    (3, [0, 1, -1, -1, -1, -1, -1, -1], 4),  # one spare slot, then the two resident slots once
+                                             # the resident experts are done: rounds of 1, 2, 1, 2
 ])
 def test_corrected_layer_equals_all_resident_layer(S, resident, rounds):
     cfg = dict(synth.config(2), T=512, H=512, F=1024)
