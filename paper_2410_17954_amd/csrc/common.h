@@ -26,6 +26,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
 // ---------------------------------------------------------------- waves
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }

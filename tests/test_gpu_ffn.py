@@ -129,3 +129,44 @@ def test_full_shape_sampled_rows(cfg_id):
         ref[a] = oracle.swiglu(synth.values(x[r:r + 1]), synth.values(inp["w_gate"][e]),
                                synth.values(inp["w_up"][e]), synth.values(inp["w_down"][e]))[0]
     assert rel_max_err(got[sample], ref) <= 1e-2
+
+
+@pytest.mark.parametrize("counts,H,F", [
+    ([1], 64, 64),                          # one row, one K batch
+    ([1, 3, 16, 0, 17, 2], 512, 1408),      # few-row experts beside one with 17 rows
+    ([16, 16, 16, 16], 256, 512),           # every expert at the few-row limit
+    ([2, 7, 0, 5], 192, 320),               # K = 6 and 10 steps of 32: partial batches
+])
+def test_bf16_few_rows_per_expert(counts, H, F):
+    # experts with at most 16 rows take the weight-streaming kernels
+    _run(counts, H, F, None, len(counts), seed=sum(counts) + H + F)
+
+
+def test_bf16_few_rows_resident_subset():
+    counts = [3, 0, 16, 1, 200, 9]
+    slot = [1, 0, -1, 3, 2, -1]
+    _run(counts, 256, 384, slot, 4, seed=23, extra_rows=5)
+
+
+def test_full_shape_decode_batch():
+    """Decode-sized batch at the full 8-expert shape (H 4096, F 14336): 24
+    tokens with top-2 give a few rows per expert; every row is checked."""
+    cfg = synth.config(2)
+    E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
+    idx = synth.random_topk_idx(24, E, k, seed=77)
+    counts = np.bincount(idx.ravel(), minlength=E)
+    assert counts.max() <= 16
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    R = int(offsets[-1])
+    inp = synth.layer_inputs(cfg, 2, T=R, parts=("x", "experts"))
+    x = inp["x"]
+    y = ops.expert_ffn(to_dev(x), to_dev(offsets), to_dev(inp["w_gate"]), to_dev(inp["w_up"]),
+                       to_dev(inp["w_down"]))
+    got = vals(y)
+    ref = np.empty((R, H))
+    for e in range(E):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        if hi > lo:
+            ref[lo:hi] = oracle.swiglu(synth.values(x[lo:hi]), synth.values(inp["w_gate"][e]),
+                                       synth.values(inp["w_up"][e]), synth.values(inp["w_down"][e]))
+    assert rel_max_err(got, ref) <= 1e-2
