@@ -44,6 +44,10 @@ def parse():
                         "a Qwen-shaped layer with 32 of 60 experts resident, misses loaded "
                         "from pinned host memory while the resident experts compute, and "
                         "PLEC against per-layer LRU hit ratios on synthetic predicted routes")
+    p.add_argument("--decode", action="store_true",
+                   help="instead of the layer throughput, measure decode-sized batches of the "
+                        "Mixtral-shaped layer (4 to 256 tokens, all 8 experts resident): "
+                        "per-stage times and the expert weights' read bandwidth")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 counter_collection.csv files (FETCH_SIZE, "
                         "WRITE_SIZE) of a --copy-probe-mib run into the traffic file, then exit")
@@ -217,6 +221,81 @@ def ece_report(args):
     print(json.dumps(rec))
 
 
+def decode_report(args):
+    """Decode-sized batches through route, permute, expert FFN and combine (one
+    JSON line). The 2.8 GB of expert weights do not fit the 256 MB last-level
+    cache, so each step reads them from HBM; a 512 MB fill before every step
+    makes sure of it."""
+    import torch
+    from paper_2410_17954_amd import ops, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.config(2)
+    H, E, F, k = cfg["H"], cfg["E"], cfg["F"], cfg["k"]
+    Tmax = 256
+    inp = synth.layer_inputs(cfg, args.seed, T=Tmax, parts=("x", "router", "experts"))
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+
+    wr = up(inp["w_router"])
+    wg, wu, wd = (up(inp[n]) for n in ("w_gate", "w_up", "w_down"))
+    flush = torch.empty(512 * 2 ** 20 // 4, dtype=torch.float32, device=dev)
+    out = []
+    for T in (4, 16, 64, 256):
+        x = up(inp["x"][:T])
+        ws_p = ops.workspace_tensor(ops.permute_workspace(T, k, E), dev)
+        ws_f = ops.workspace_tensor(ops.expert_ffn_workspace(T * k, H, F, E), dev)
+        idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+        gw = torch.empty((T, k), dtype=torch.float32, device=dev)
+        offs = torch.empty(E + 1, dtype=torch.int32, device=dev)
+        rop = torch.empty(T * k, dtype=torch.int32, device=dev)
+        por = torch.empty(T * k, dtype=torch.int32, device=dev)
+        xp = torch.empty((T * k, H), dtype=torch.bfloat16, device=dev)
+        yp = torch.empty_like(xp)
+        y = torch.empty_like(x)
+        inc = torch.empty(T, dtype=torch.int32, device=dev)
+
+        def step(ev):
+            ev[0].record()
+            ops.route(x, wr, k, topk_idx=idx, topk_w=gw)
+            ev[1].record()
+            ops.permute(x, idx, E, expert_offsets=offs, row_of_pair=rop, pair_of_row=por,
+                        x_perm=xp, workspace=ws_p)
+            ev[2].record()
+            ops.expert_ffn(xp, offs, wg, wu, wd, y_perm=yp, workspace=ws_f)
+            ev[3].record()
+            ops.combine(yp, idx, gw, rop, y=y, incomplete=inc)
+            ev[4].record()
+
+        times = []
+        for rep in range(args.warmup + 7):
+            flush.fill_(float(rep))
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+            # the launches queue behind a short wait so that host time is not counted
+            torch.cuda._sleep(1000000)
+            step(ev)
+            torch.cuda.synchronize()
+            if rep >= args.warmup:
+                times.append([ev[i].elapsed_time(ev[i + 1]) for i in range(4)])
+        med = np.median(np.array(times), axis=0)
+        counts = np.bincount(idx.cpu().numpy().ravel(), minlength=E)
+        wbytes = int((counts > 0).sum()) * 3 * H * F * 2
+        out.append({"tokens": T, "max_rows_per_expert": int(counts.max()),
+                    "experts_used": int((counts > 0).sum()),
+                    "route_ms": round(float(med[0]), 4), "permute_ms": round(float(med[1]), 4),
+                    "ffn_ms": round(float(med[2]), 4), "combine_ms": round(float(med[3]), 4),
+                    "step_ms": round(float(med.sum()), 4),
+                    "ffn_weight_GBps": round(wbytes / (float(med[2]) * 1e-3) / 1e9, 1),
+                    "ffn_hbm_frac": round(wbytes / (float(med[2]) * 1e-3) / 1e9 / PEAK_HBM_GBS, 3)})
+    rec = {"metric": "decode-sized MoE-layer steps: stage times and expert-weight read bandwidth",
+           "config": {"workload": f"Mixtral-8x7B-shaped layer: H={H}, E={E}, F={F}, top-{k}, "
+                                  "all experts resident, weights read from HBM every step"},
+           "steps": out, "data": "synthetic"}
+    print(json.dumps(rec))
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -232,6 +311,9 @@ def main():
         sys.exit(2)
     if args.ece:
         ece_report(args)
+        return
+    if args.decode:
+        decode_report(args)
         return
     import torch
     from paper_2410_17954_amd import ops, synth

@@ -46,18 +46,20 @@ constexpr int kTailWords = 1 + kMaxTailTiles;
 constexpr int kCounterWords = kClaimWords + 2 * kTailWords;
 
 // Per-expert row-tile prefix of resident experts; also clears the counters.
-// Resident experts with at most small_max rows (when small_max > 0) get no
-// row tiles here: they are listed for the small-row kernels instead
-// (small[0] = their number, small[1..] = their ids in ascending order).
+// Resident experts with at most 16 * small_tiles rows (small_tiles 0, 1 or 2)
+// get no row tiles here: they are listed for the few-row kernels instead,
+// those with at most 16 rows in one list and those with 17 to 32 in another
+// (list[0] = the number of experts, list[1..] = their ids in ascending order).
 __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
                                  const int32_t* __restrict__ slot, int E, int S,
-                                 int64_t max_rows, int bm, int small_max,
+                                 int64_t max_rows, int bm, int small_tiles,
                                  int32_t* __restrict__ prefix) {
   if (blockIdx.x != 0) return;
   for (int q = threadIdx.x; q < kCounterWords; q += blockDim.x) prefix[E + 1 + q] = 0;
   if (threadIdx.x != 0) return;
-  int32_t* const small = prefix + E + 1 + kCounterWords;
-  int32_t run = 0, ns = 0;
+  int32_t* const list1 = prefix + E + 1 + kCounterWords;
+  int32_t* const list2 = list1 + E + 1;
+  int32_t run = 0, n1 = 0, n2 = 0;
   for (int e = 0; e < E; ++e) {
     prefix[e] = run;
     const int s = slot ? slot[e] : e;
@@ -65,11 +67,14 @@ __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
     lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
     hi = hi < lo ? lo : (hi > max_rows ? max_rows : hi);
     if (s < 0 || s >= S || hi == lo) continue;
-    if (hi - lo <= small_max) small[1 + ns++] = e;
-    else run += (int32_t)((hi - lo + bm - 1) / bm);
+    const int64_t m = hi - lo;
+    if (m <= 16 * small_tiles && m <= 16) list1[1 + n1++] = e;
+    else if (m <= 16 * small_tiles) list2[1 + n2++] = e;
+    else run += (int32_t)((m + bm - 1) / bm);
   }
   prefix[E] = run;
-  small[0] = ns;
+  list1[0] = n1;
+  list2[0] = n2;
 }
 
 // silu(g) * u with the hardware exp2 and reciprocal (about 2 ulp of float32,
@@ -265,116 +270,139 @@ ffn_gemm_bf16(const uint16_t* __restrict__ A, int64_t K,
 }
 
 // ------------------------------------------------------- few rows per expert
-// An expert with at most kSmallRows rows (decode-sized batches) is bound by
-// reading its weights once, not by MFMA. A block of four waves owns
+// An expert with at most 16 * MT rows (decode-sized batches; MT = 1 or 2) is
+// bound by reading its weights once, not by MFMA. A block of four waves owns
 // kSmallCols output columns (weight rows) of one such expert; wave w streams
 // the w-th quarter of the K range of those rows with 16x16x32 MFMAs (the
-// expert's rows padded to 16 with zeros, which are never loaded), and the four
-// partial sums are added through LDS in wave order. Splitting K inside the
+// expert's rows padded to 16 * MT with zeros, which are never loaded), and
+// the four partial sums are added through LDS in wave order. Splitting K inside the
 // block, rather than giving each wave its own columns, keeps the addresses
 // the whole chip reads at one time close together, which DRAM serves faster.
-constexpr int kSmallRows = 16;
 constexpr int kSmallNT = 2;                      // 16-column MFMA tiles per block
 constexpr int kSmallCols = 16 * kSmallNT;
 constexpr int kSmallU = 4;                       // K steps of 32 loaded per batch
 constexpr int kSmallWaves = 4;
 
-template <int EPI>
+template <int EPI, int MT>
 __global__ void __launch_bounds__(64 * kSmallWaves)
 ffn_small_bf16(const uint16_t* __restrict__ A, int64_t K, const uint16_t* __restrict__ B0,
                const uint16_t* __restrict__ B1, int64_t F, int64_t H,
                const int32_t* __restrict__ offsets, const int32_t* __restrict__ slot,
-               int64_t max_rows, const int32_t* __restrict__ small, uint16_t* __restrict__ C) {
+               int64_t max_rows, const int32_t* __restrict__ list, uint16_t* __restrict__ C) {
   constexpr int NB = EPI == 0 ? 2 : 1;           // gate and up, or down
-  __shared__ f32x4_t part[kSmallWaves][kSmallNT][NB][kWave];
-  const int64_t N_out = EPI == 0 ? F : H;
-  const int ncb = (int)((N_out + kSmallCols - 1) / kSmallCols);
-  const int64_t units = (int64_t)small[0] * ncb;
+  __shared__ f32x4_t part[kSmallWaves][MT][kSmallNT][NB][kWave];
+  const int64_t N_out = EPI == 0 ? F : H;        // a multiple of kSmallCols (fast path)
+  const int ncb = (int)(N_out / kSmallCols);
+  const int64_t units = (int64_t)list[0] * ncb;
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int r = lane & 15;                       // A row / B column of this lane
+  const int kq = (lane >> 4) * 8;                // its 8-wide slice of a K step
+  const int64_t ks = K / 32;
+  const int64_t per = (ks + kSmallWaves - 1) / kSmallWaves;
+  const int64_t kb = min(ks, wave * per), ke = min(ks, kb + per);
+  const int64_t kfull = kb + (ke - kb) / kSmallU * kSmallU;
+  // byte offset of this lane's B slice from a weight tile's first row
+  const uint32_t b_off = (uint32_t)(((int64_t)r * K + kq) * 2);
   // units (expert, column block) in order, the grid striding over them: at any
   // time the blocks work on neighbouring columns
   for (int64_t unit = blockIdx.x; unit < units; unit += gridDim.x) {
     const int li = (int)(unit / ncb), cb = (int)(unit % ncb);
-    const int e = small[1 + li];
+    const int e = list[1 + li];
     const int s = slot ? slot[e] : e;
     int64_t lo = offsets[e], hi = offsets[e + 1];
     lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
     hi = hi < lo ? lo : (hi > max_rows ? max_rows : hi);
-    const int m = (int)min(hi - lo, (int64_t)kSmallRows);
-    const int lane = lane_id();
-    const int wave = threadIdx.x / kWave;
+    const int m = (int)min(hi - lo, (int64_t)(16 * MT));
     const int64_t n0 = (int64_t)cb * kSmallCols;
-    const int r = lane & 15;                       // A row / B column of this lane
-    const int kq = (lane >> 4) * 8;                // its 8-wide slice of a K step
-    const bool row_ok = r < m;
-    const int64_t ks = K / 32;
-    const int64_t per = (ks + kSmallWaves - 1) / kSmallWaves;
-    const int64_t kb = min(ks, wave * per), ke = min(ks, kb + per);
-    const uint16_t* const arow = A + (lo + (row_ok ? r : 0)) * K + kq;
-    const uint16_t* bp[kSmallNT][NB];
+    // wave-uniform bases plus 32-bit lane offsets. With one row tile, lanes of
+    // rows past m load nothing (masked off, so no data comes back) and feed
+    // zeros; with two, every lane loads (rows past m read the expert's last
+    // row, whose products land in rows that are never stored): most of those
+    // lanes are live, and the masks would cost registers and occupancy.
+    const char* const a_base = reinterpret_cast<const char*>(A + lo * K);
+    uint32_t a_off[MT];
+    bool a_on[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      a_on[i] = 16 * i + r < m;
+      a_off[i] = (uint32_t)(((int64_t)min(16 * i + r, m - 1) * K + kq) * 2);
+    }
+    const char* b_base[kSmallNT][NB];
 #pragma unroll
     for (int j = 0; j < kSmallNT; ++j) {
-      int64_t c = n0 + 16 * j + r;
-      if (c >= N_out) c = 0;                       // loaded, never stored
-      bp[j][0] = B0 + ((int64_t)s * N_out + c) * K + kq;
-      if constexpr (EPI == 0) bp[j][1] = B1 + ((int64_t)s * N_out + c) * K + kq;
+      b_base[j][0] = reinterpret_cast<const char*>(B0 + ((int64_t)s * N_out + n0 + 16 * j) * K);
+      if constexpr (EPI == 0)
+        b_base[j][1] = reinterpret_cast<const char*>(B1 + ((int64_t)s * N_out + n0 + 16 * j) * K);
     }
-    f32x4_t acc[kSmallNT][NB];
+    f32x4_t acc[MT][kSmallNT][NB];
 #pragma unroll
-    for (int j = 0; j < kSmallNT; ++j)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) acc[j][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int64_t s0 = kb; s0 < ke; s0 += kSmallU) {
-      uint4 a[kSmallU], w[kSmallU][kSmallNT][NB];
+      for (int j = 0; j < kSmallNT; ++j)
 #pragma unroll
-      for (int u = 0; u < kSmallU; ++u) {
-        const int64_t st = s0 + u;
-        const bool ok = st < ke;
-        a[u] = (ok && row_ok) ? *reinterpret_cast<const uint4*>(arow + st * 32) : make_uint4(0, 0, 0, 0);
+        for (int b = 0; b < NB; ++b) acc[i][j][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    auto steps = [&](int64_t s0, auto n_c) {
+      constexpr int NS = decltype(n_c)::value;
+      uint4 a[NS][MT], w[NS][kSmallNT][NB];
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+        const int64_t kbyte = (s0 + u) * 64;
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+          a[u][i] = (MT == 2 || a_on[i]) ? *reinterpret_cast<const uint4*>(a_base + kbyte + a_off[i])
+                                         : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int j = 0; j < kSmallNT; ++j)
 #pragma unroll
           for (int b = 0; b < NB; ++b)
-            w[u][j][b] = ok ? __builtin_bit_cast(uint4, __builtin_nontemporal_load(
-                                  reinterpret_cast<const u32x4_t*>(bp[j][b] + st * 32)))
-                            : make_uint4(0, 0, 0, 0);
+            w[u][j][b] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4_t*>(b_base[j][b] + kbyte + b_off)));
       }
 #pragma unroll
-      for (int u = 0; u < kSmallU; ++u)
+      for (int u = 0; u < NS; ++u)
 #pragma unroll
-        for (int j = 0; j < kSmallNT; ++j)
+        for (int i = 0; i < MT; ++i)
 #pragma unroll
-          for (int b = 0; b < NB; ++b)
-            acc[j][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8_t, a[u]), __builtin_bit_cast(bf16x8_t, w[u][j][b]),
-                acc[j][b], 0, 0, 0);
-    }
+          for (int j = 0; j < kSmallNT; ++j)
 #pragma unroll
-    for (int j = 0; j < kSmallNT; ++j)
+            for (int b = 0; b < NB; ++b)
+              acc[i][j][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                  __builtin_bit_cast(bf16x8_t, a[u][i]), __builtin_bit_cast(bf16x8_t, w[u][j][b]),
+                  acc[i][j][b], 0, 0, 0);
+    };
+    for (int64_t s0 = kb; s0 < kfull; s0 += kSmallU) steps(s0, std::integral_constant<int, kSmallU>{});
+    for (int64_t s0 = kfull; s0 < ke; ++s0) steps(s0, std::integral_constant<int, 1>{});
 #pragma unroll
-      for (int b = 0; b < NB; ++b) part[wave][j][b][lane] = acc[j][b];
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < kSmallNT; ++j)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) part[wave][i][j][b][lane] = acc[i][j][b];
     __syncthreads();
     // C layout of the 16x16 MFMA: lane holds column (lane % 16), rows
-    // 4 * (lane / 16) + i.
+    // 4 * (lane / 16) + q of its 16-row tile.
     if (wave == 0) {
 #pragma unroll
-      for (int j = 0; j < kSmallNT; ++j) {
-        f32x4_t t[NB];
+      for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          t[b] = part[0][j][b][lane];
+        for (int j = 0; j < kSmallNT; ++j) {
+          f32x4_t t[NB];
 #pragma unroll
-          for (int q = 1; q < kSmallWaves; ++q) t[b] += part[q][j][b][lane];
+          for (int b = 0; b < NB; ++b) {
+            t[b] = part[0][i][j][b][lane];
+#pragma unroll
+            for (int q = 1; q < kSmallWaves; ++q) t[b] += part[q][i][j][b][lane];
+          }
+          const int64_t col = n0 + 16 * j + r;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int rr = 16 * i + (lane >> 4) * 4 + q;
+            if (rr >= m) continue;
+            const float v = EPI == 0 ? swiglu(t[0][q], t[1][q]) : t[0][q];
+            C[(lo + rr) * N_out + col] = f32_to_bf16(v);
+          }
         }
-        const int64_t col = n0 + 16 * j + r;
-        if (col >= N_out) continue;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int rr = (lane >> 4) * 4 + i;
-          if (rr >= m) continue;
-          const float v = EPI == 0 ? swiglu(t[0][i], t[1][i]) : t[0][i];
-          C[(lo + rr) * N_out + col] = f32_to_bf16(v);
-        }
-      }
     }
     __syncthreads();                               // part is rewritten by the next unit
   }
@@ -942,7 +970,7 @@ extern "C" size_t moe_expert_ffn_workspace(int64_t max_rows, int64_t H, int64_t 
   if (max_rows < 1 || H < 1 || F < 1 || E < 1 || !valid_dtype(dtype)) return 0;
   const size_t elt = dtype == MOE_BF16 ? 2 : 4;
   size_t bytes = align_up((size_t)max_rows * (size_t)F * elt, 256);
-  bytes += align_up((size_t)(E + 1 + kCounterWords + E + 1) * sizeof(int32_t), 256);
+  bytes += align_up((size_t)(E + 1 + kCounterWords + 2 * (E + 1)) * sizeof(int32_t), 256);
   if (dtype == MOE_BF16 && fast_path(H, F))
     bytes += (size_t)max_split_pieces(max_rows, H, F, E) * fast::kPieceBytes;
   return bytes;
@@ -987,14 +1015,21 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
 
   const bool fast = fast_path(H, F);
   const int bm = fast ? fast::BM : BM;
-  // experts with few rows go to the weight-streaming kernels (bf16, K
-  // multiples of 32 -- the fast-path shapes)
-  const int small_max = fast ? kSmallRows : 0;
+  // Experts with at most 32 rows go to the weight-streaming kernels when the
+  // batch is decode-sized (at most 32 rows per expert on average): bf16, H and
+  // F multiples of 32 (the fast-path shapes), 32-bit lane offsets within 32
+  // rows of K. Larger batches leave the rare small expert to the large tiles
+  // and launch no few-row kernel at all.
+  const int small_tiles =
+      fast && std::max(H, F) < ((int64_t)1 << 25) && max_rows <= 32 * (int64_t)E ? 2 : 0;
   ffn_tiles_kernel<<<dim3(1), dim3(64), 0, st>>>(expert_offsets, slot_of_expert, E, S, max_rows,
-                                                 bm, small_max, prefix);
+                                                 bm, small_tiles, prefix);
   MOE_CHECK_LAUNCH();
-  const int32_t* const small = prefix + E + 1 + kCounterWords;
-  const bool big = max_rows > small_max;       // else every expert has few rows
+  const int32_t* const list1 = prefix + E + 1 + kCounterWords;
+  const int32_t* const list2 = list1 + E + 1;
+  const bool few = small_tiles > 0;
+  const bool big = max_rows > 16 * small_tiles;  // else every expert has few rows
+  const bool mid = few && max_rows > 16;          // else none has 17 to 32
   int grid = device_cu_count();
   grid = std::min((grid + 7) / 8 * 8, kMaxTailTiles);     // a tail round has < grid tiles
   const auto* xb = static_cast<const uint16_t*>(x_perm);
@@ -1007,30 +1042,46 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
     int32_t* const claim = prefix + E + 1;
     int32_t* const tail = claim + kClaimWords;
     float* const partial = reinterpret_cast<float*>(
-        reinterpret_cast<char*>(prefix) + align_up((size_t)(E + 1 + kCounterWords + E + 1) * 4, 256));
+        reinterpret_cast<char*>(prefix) + align_up((size_t)(E + 1 + kCounterWords + 2 * (E + 1)) * 4, 256));
     const int pieces = (int)max_split_pieces(max_rows, H, F, E);
-    // a grid the chip holds at once (four blocks per compute unit), striding
-    // over the few-row experts' units; with none it does one load per block
+    // two blocks per compute unit, striding over the few-row experts' units
+    // (more blocks in flight spread the reads over more DRAM rows at once and
+    // measured slower; fewer leave bandwidth unused); with no such expert each
+    // block does one load
     const int64_t small_units = (int64_t)E * ceil_div(std::max(F, H), kSmallCols);
-    const unsigned small_grid = (unsigned)std::min<int64_t>(4 * (int64_t)device_cu_count(), small_units);
+    const unsigned small_grid = (unsigned)std::min<int64_t>(2 * (int64_t)device_cu_count(), small_units);
     if (big) {
       ffn_gemm_bf16_fast<0><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
           xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
           claim, tail, partial, pieces, ab);
       MOE_CHECK_LAUNCH();
     }
-    ffn_small_bf16<0><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-        xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, small, ab);
-    MOE_CHECK_LAUNCH();
+    if (few) {
+      ffn_small_bf16<0, 1><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
+          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list1, ab);
+      MOE_CHECK_LAUNCH();
+    }
+    if (mid) {
+      ffn_small_bf16<0, 2><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
+          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list2, ab);
+      MOE_CHECK_LAUNCH();
+    }
     if (big) {
       ffn_gemm_bf16_fast<1><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
           ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
           claim + 8, tail + kTailWords, partial, pieces, yb);
       MOE_CHECK_LAUNCH();
     }
-    ffn_small_bf16<1><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-        ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, small, yb);
-    MOE_CHECK_LAUNCH();
+    if (few) {
+      ffn_small_bf16<1, 1><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
+          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list1, yb);
+      MOE_CHECK_LAUNCH();
+    }
+    if (mid) {
+      ffn_small_bf16<1, 2><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
+          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list2, yb);
+      MOE_CHECK_LAUNCH();
+    }
     return MOE_OK;
   }
   ffn_gemm_bf16<0><<<dim3(grid), dim3(kThreads), 0, st>>>(

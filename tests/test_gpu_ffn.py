@@ -54,6 +54,7 @@ def test_tiny_fp32_config():
 
 @pytest.mark.parametrize("counts,H,F", [
     ([0, 300, 17, 513], 256, 512),        # ragged, several row tiles, an empty expert
+    ([900, 2, 20, 30], 256, 512),          # large batch: its few-row experts take the large tiles
     ([1], 64, 64),                         # one row
     ([256, 256], 128, 192),                # exact tiles, F not a multiple of 64
     ([700, 3, 0, 1029, 64], 512, 1408),    # Qwen-like F
@@ -136,26 +137,33 @@ def test_full_shape_sampled_rows(cfg_id):
     ([1, 3, 16, 0, 17, 2], 512, 1408),      # few-row experts beside one with 17 rows
     ([16, 16, 16, 16], 256, 512),           # every expert at the few-row limit
     ([2, 7, 0, 5], 192, 320),               # K = 6 and 10 steps of 32: partial batches
+    ([17, 32, 16, 33, 24], 256, 416),       # two-tile experts (17..32 rows) beside the others
+    ([31, 1, 29], 160, 96),                 # K = 5 and 3 steps: every wave's range is short
 ])
 def test_bf16_few_rows_per_expert(counts, H, F):
-    # experts with at most 16 rows take the weight-streaming kernels
+    # in decode-sized batches experts with at most 32 rows take the
+    # weight-streaming kernels
     _run(counts, H, F, None, len(counts), seed=sum(counts) + H + F)
 
 
 def test_bf16_few_rows_resident_subset():
-    counts = [3, 0, 16, 1, 200, 9]
+    # decode-sized batch (at most 32 rows per expert on average) with one
+    # expert large enough for the large tiles
+    counts = [3, 0, 16, 1, 120, 9]
     slot = [1, 0, -1, 3, 2, -1]
     _run(counts, 256, 384, slot, 4, seed=23, extra_rows=5)
 
 
-def test_full_shape_decode_batch():
-    """Decode-sized batch at the full 8-expert shape (H 4096, F 14336): 24
-    tokens with top-2 give a few rows per expert; every row is checked."""
+@pytest.mark.parametrize("T", [24, 100])
+def test_full_shape_decode_batch(T):
+    """Decode-sized batch at the full 8-expert shape (H 4096, F 14336): 24 or
+    100 tokens with top-2 give up to 16, or 17 to 32, rows per expert; every
+    row is checked."""
     cfg = synth.config(2)
     E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
-    idx = synth.random_topk_idx(24, E, k, seed=77)
+    idx = synth.random_topk_idx(T, E, k, seed=77)
     counts = np.bincount(idx.ravel(), minlength=E)
-    assert counts.max() <= 16
+    assert counts.max() <= (16 if T == 24 else 32)
     offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
     R = int(offsets[-1])
     inp = synth.layer_inputs(cfg, 2, T=R, parts=("x", "experts"))
