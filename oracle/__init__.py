@@ -31,7 +31,8 @@ from .permute import permute
 from .ffn import silu, swiglu, swiglu_loops, expert_ffn
 from .combine import combine
 from .schedule import (route_bits, eq2_objective, signature_rank, hamming_to,
-                       cluster_distance_sums, schedule, batch_accuracy)
+                       cluster_distance_sums, schedule, batch_accuracy, multi_batch_offsets,
+                       schedule_multi)
 from .slots import plan_slots
 from .cache import plec_order, plec_run, lru_run
 from .layer import moe_layer, dense_ffn
@@ -40,7 +41,8 @@ __all__ = [
     "router_logits", "topk_select", "softmax", "gate_weights", "route",
     "permute", "silu", "swiglu", "swiglu_loops", "expert_ffn", "combine",
     "route_bits", "eq2_objective", "signature_rank", "hamming_to",
-    "cluster_distance_sums", "schedule", "batch_accuracy", "plan_slots",
+    "cluster_distance_sums", "schedule", "batch_accuracy", "multi_batch_offsets",
+    "schedule_multi", "plan_slots",
     "plec_order", "plec_run", "lru_run",
     "moe_layer", "dense_ffn",
 ]

@@ -157,6 +157,71 @@ def schedule(routes, E, n1=None, max_iters=10, keep_original_if_worse=True):
     return perm, demand, info
 
 
+def multi_batch_offsets(N, B):
+    """Batch boundaries of the B-way split of N tokens by recursive bisection:
+    a set of n tokens bound for b batches puts n * (b // 2) // b of them
+    (floor) into the first b // 2 batches and the rest into the other
+    b - b // 2. Returns int64 [B + 1]."""
+    sizes = []
+
+    def rec(n, b):
+        if b == 1:
+            sizes.append(n)
+            return
+        bl = b // 2
+        n1 = n * bl // b
+        rec(n1, bl)
+        rec(n - n1, b - bl)
+
+    rec(int(N), int(B))
+    return np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+
+
+def schedule_multi(routes, E, B, max_iters=10, keep_original_if_worse=True):
+    """B-way rebatching by recursive bisection with the two-way scheduler
+    above (an extension: Sec. 3.3.1 states the problem for two batches).
+
+    A node holds n tokens (in the order its parent's split left them) and the
+    number b of batches they form. b == 1 is a batch. Otherwise the two-way
+    scheduler runs on the node's tokens, re-indexed 0..n-1 in that order, with
+    n1 = n * (b // 2) // b; its batch 1 (in its perm order) becomes the left
+    child with b // 2 batches, its batch 2 the right child with the rest. The
+    batches are the leaves from left to right.
+
+    Returns (perm int64 [N]: the leaves' tokens concatenated,
+             offsets int64 [B + 1],
+             demand int64 [B, L, E]: tokens of each batch using (l, e),
+             info int64 [B - 1, 8]: the two-way info of each split in
+                 pre-order (medoids are node-local indices); a split of an
+                 empty node records [0, 1, -1, -1, 0, 0, 0, 0]).
+    """
+    routes = np.asarray(routes, dtype=np.int64)
+    N, L, k = routes.shape
+    infos = []
+
+    def rec(ids, b):
+        if b == 1:
+            return [ids]
+        bl = b // 2
+        n = len(ids)
+        n1 = n * bl // b
+        if n == 0:
+            infos.append(np.array([0, 1, -1, -1, 0, 0, 0, 0], dtype=np.int64))
+            return rec(ids, bl) + rec(ids, b - bl)
+        p, _, info = schedule(routes[ids], E, n1, max_iters, keep_original_if_worse)
+        infos.append(info)
+        ids = ids[p]
+        return rec(ids[:n1], bl) + rec(ids[n1:], b - bl)
+
+    leaves = rec(np.arange(N, dtype=np.int64), int(B))
+    perm = np.concatenate(leaves).astype(np.int64)
+    offsets = np.concatenate([[0], np.cumsum([len(x) for x in leaves])]).astype(np.int64)
+    r3 = route_bits(routes, E)
+    demand = np.stack([r3[x].sum(axis=0) for x in leaves]).astype(np.int64)
+    info = np.stack(infos) if infos else np.zeros((0, 8), dtype=np.int64)
+    return perm, offsets, demand, info
+
+
 def batch_accuracy(true_bits, pred_bits):
     """Batch-level accuracy of Sec. 4.3.3: the per-layer share of the experts a
     batch really activates that the prediction also activates, averaged over

@@ -226,3 +226,100 @@ def test_batch_accuracy():
     t = np.zeros((2, 1, 8)); t[0, 0, [0, 1]] = 1; t[1, 0, [2, 3]] = 1
     p = np.zeros((1, 1, 8)); p[0, 0, [0, 1, 6]] = 1
     assert oracle.batch_accuracy(t, p) == 0.5
+
+
+# ----------------------------------------------------- B-way recursive bisection
+@pytest.mark.parametrize("N,B,sizes", [
+    (10, 3, [3, 3, 4]),                 # 10*1//3 = 3 | 7 -> 7*1//2 = 3 | 4
+    (16, 4, [4, 4, 4, 4]),
+    (7, 1, [7]),
+    (3, 4, [0, 1, 1, 1]),               # 3*2//4 = 1 -> (0 | 1), 2 -> (1 | 1)
+    (3, 8, [0, 0, 0, 1, 0, 1, 0, 1]),
+    (13, 5, [2, 3, 2, 3, 3]),           # 13*2//5 = 5 -> (2 | 3); 8 -> 8//3 = 2 | 6 -> (3 | 3)
+])
+def test_multi_batch_sizes_by_hand(N, B, sizes):
+    assert oracle.multi_batch_offsets(N, B).tolist() == [0] + np.cumsum(sizes).tolist()
+
+
+def test_multi_one_way_is_the_input_order():
+    routes = _random_routes(11, 3, 6, 2, seed=40)
+    perm, off, demand, info = oracle.schedule_multi(routes, 6, 1)
+    assert perm.tolist() == list(range(11)) and off.tolist() == [0, 11]
+    assert info.shape == (0, 8)
+    ref = np.zeros((3, 6), dtype=np.int64)
+    for i in range(11):
+        for l in range(3):
+            for j in range(2):
+                ref[l, routes[i, l, j]] += 1
+    assert np.array_equal(demand[0], ref)
+
+
+def test_multi_two_ways_is_the_two_way_scheduler():
+    routes = _random_routes(41, 4, 8, 2, seed=41)
+    perm, off, demand, info = oracle.schedule_multi(routes, 8, 2)
+    p2, d2, i2 = oracle.schedule(routes, 8, 20)
+    assert np.array_equal(perm, p2) and np.array_equal(demand, d2)
+    assert off.tolist() == [0, 20, 41] and np.array_equal(info[0], i2)
+
+
+def test_multi_planted_clusters_reach_the_optimum():
+    # four route patterns with disjoint experts, 8 tokens each, shuffled: the
+    # best 4-way split puts one pattern per batch, L*k active pairs each
+    L, E, k = 5, 16, 2
+    pats = [np.array([[2 * c, 2 * c + 1]] * L) for c in range(4)]
+    routes = np.stack([pats[c] for c in range(4) for _ in range(8)])
+    routes = routes[np.random.default_rng(42).permutation(32)]
+    perm, off, demand, info = oracle.schedule_multi(routes, E, 4)
+    batches = [perm[off[b]:off[b + 1]] for b in range(4)]
+    assert _eq2_sets(routes, E, batches) == 4 * L * k
+    for members in batches:
+        assert len({tuple(routes[i].ravel()) for i in members}) == 1
+
+
+def test_multi_small_case_against_brute_force():
+    # 8 tokens into 4 batches of 2: every split is checked against Eq. 2
+    # summed over the batches, and the result is no better than the optimum
+    N, L, E, k = 8, 3, 4, 1
+    routes = _random_routes(N, L, E, k, seed=43)
+    perm, off, demand, info = oracle.schedule_multi(routes, E, 4)
+    assert sorted(perm.tolist()) == list(range(N))
+    assert off.tolist() == [0, 2, 4, 6, 8]
+    batches = [perm[off[b]:off[b + 1]].tolist() for b in range(4)]
+
+    def partitions(items):
+        if not items:
+            yield []
+            return
+        first = items[0]
+        for other in items[1:]:
+            rest = [x for x in items[1:] if x != other]
+            for p in partitions(rest):
+                yield [[first, other]] + p
+
+    best = min(_eq2_sets(routes, E, p) for p in partitions(list(range(N))))
+    got = _eq2_sets(routes, E, batches)
+    assert best <= got
+    # each split's guard: never worse than the node's input split
+    assert (info[:, 5] <= info[:, 4]).all()
+    # the first split's objective is Eq. 2 over its two halves
+    assert info[0, 5] == _eq2_sets(routes, E, [perm[:4], perm[4:]])
+    for b, members in enumerate(batches):
+        ref = np.zeros((L, E), dtype=np.int64)
+        for i in members:
+            ref[np.arange(L), routes[i, :, 0]] += 1
+        assert np.array_equal(demand[b], ref)
+
+
+def test_multi_more_batches_than_tokens():
+    routes = _random_routes(3, 2, 4, 2, seed=44)
+    perm, off, demand, info = oracle.schedule_multi(routes, 4, 8)
+    assert sorted(perm.tolist()) == [0, 1, 2]
+    assert off.tolist() == [0, 0, 0, 0, 1, 1, 2, 2, 3]
+    # pre-order splits: (3 tokens, 8 batches) n1 = 1; (1, 4) n1 = 0; (0, 2)
+    # empty; (1, 2) n1 = 0; (2, 4) n1 = 1; (1, 2) and (1, 2) n1 = 0
+    assert info.shape == (7, 8)
+    assert info[2].tolist() == [0, 1, -1, -1, 0, 0, 0, 0]
+    assert info[:, 7].tolist() == [1, 0, 0, 0, 1, 0, 0]
+    for r in (1, 3, 5, 6):                       # one token: identity, L*k pairs
+        assert info[r].tolist() == [0, 1, -1, -1, 4, 4, 0, 0]
+    assert demand.sum() == 3 * 2 * 2
