@@ -48,6 +48,10 @@ def parse():
                    help="instead of the layer throughput, measure decode-sized batches of the "
                         "Mixtral-shaped layer (4 to 256 tokens, all 8 experts resident): "
                         "per-stage times and the expert weights' read bandwidth")
+    p.add_argument("--ways", action="store_true",
+                   help="instead of the layer throughput, measure B-way rebatching by "
+                        "recursive bisection (B = 2 to 64 batches of 64 tokens, Qwen-shaped "
+                        "24-layer predicted routes): time and active (layer, expert) pairs")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 counter_collection.csv files (FETCH_SIZE, "
                         "WRITE_SIZE) of a --copy-probe-mib run into the traffic file, then exit")
@@ -296,6 +300,64 @@ def decode_report(args):
     print(json.dumps(rec))
 
 
+def ways_report(args):
+    """B-way token scheduling (moe_schedule_multi) on Qwen-shaped predicted
+    routes: for B batches of 64 tokens, the time of one call (HIP events,
+    median of 7) and the active (layer, expert) pairs summed over the batches
+    (Eq. 2 generalised) for the input order cut into B contiguous batches and
+    for the scheduled batches. One JSON line."""
+    import torch
+    from paper_2410_17954_amd import ops, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.config(4)
+    L, E, k = cfg["L"], cfg["E"], cfg["k"]
+    per_batch = 64                   # decode-sized batches: not every expert is hit
+    out = []
+    for B in (2, 4, 8, 16, 64):
+        N = B * per_batch
+        routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], args.seed)
+        rt = torch.from_numpy(np.ascontiguousarray(routes, dtype=np.uint8)).to(dev)
+        ws = ops.workspace_tensor(ops.schedule_multi_workspace(N, L, E, k, B), dev)
+        perm = torch.empty(N, dtype=torch.int32, device=dev)
+        offs = torch.empty(B + 1, dtype=torch.int32, device=dev)
+        demand = torch.empty((B, L, E), dtype=torch.int32, device=dev)
+        info = torch.empty((B - 1, 8), dtype=torch.int64, device=dev)
+
+        def call():
+            ops.schedule_multi(rt, E, B, perm=perm, batch_offsets=offs, demand=demand, info=info,
+                               workspace=ws)
+
+        ts = []
+        for rep in range(args.warmup + 7):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(1000000)
+            e0.record()
+            call()
+            e1.record()
+            torch.cuda.synchronize()
+            if rep >= args.warmup:
+                ts.append(e0.elapsed_time(e1))
+        before = 0
+        for b in range(B):
+            r = routes[b * per_batch:(b + 1) * per_batch].astype(np.int64)
+            act = np.zeros((L, E), dtype=bool)
+            for l in range(L):
+                act[l, np.unique(r[:, l, :])] = True
+            before += int(act.sum())
+        after = int((demand.cpu().numpy() > 0).sum())
+        out.append({"batches": B, "tokens": N, "ms": round(float(np.median(ts)), 4),
+                    "active_pairs_input_order": before, "active_pairs_scheduled": after,
+                    "experts_per_layer_per_batch_input": round(before / (B * L), 2),
+                    "experts_per_layer_per_batch_scheduled": round(after / (B * L), 2)})
+    rec = {"metric": "B-way token scheduling: time and active (layer, expert) pairs",
+           "config": {"workload": f"Qwen1.5-MoE-shaped predicted routes: L={L}, E={E}, top-{k}, "
+                                  f"batches of {per_batch} tokens, keep {cfg['keep']}, "
+                                  f"zipf {cfg['zipf']}"},
+           "steps": out, "data": "synthetic"}
+    print(json.dumps(rec))
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -314,6 +376,9 @@ def main():
         return
     if args.decode:
         decode_report(args)
+        return
+    if args.ways:
+        ways_report(args)
         return
     import torch
     from paper_2410_17954_amd import ops, synth

@@ -5,6 +5,7 @@
  *
  *   moe_route       softmax top-k gating                        (Sec. 2.1)
  *   moe_schedule    balanced rebatching of two adjacent batches
+ *   moe_schedule_multi  the same into B batches by recursive bisection
  *                   by predicted routing path                   (Sec. 3.3, Eq. 2)
  *   moe_permute     expert-major grouping of (token, choice) pairs
  *   moe_expert_ffn  grouped SwiGLU experts over the resident
@@ -122,6 +123,39 @@ int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t E, int32_t
                  int64_t n1, int32_t max_iters, int32_t keep_original_if_worse,
                  int32_t* perm, int32_t* demand, int64_t* info,
                  void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_schedule_multi -- B-way rebatching by recursive bisection with
+ * moe_schedule (an extension: Sec. 3.3.1 states the problem, Eq. 2, for two
+ * batches). A node holds n tokens, in the order its parent's split left them,
+ * bound for b batches; b == 1 is a batch. Otherwise moe_schedule splits the
+ * node's tokens (re-indexed 0..n-1 in that order) with n1 = n*(b/2)/b
+ * (integer division): its batch 1, in perm order, becomes the left child with
+ * b/2 batches, its batch 2 the right child with b - b/2. The root holds all
+ * N tokens in index order and B batches; the batches are the leaves, left to
+ * right, so their sizes depend on N and B only.
+ *
+ * routes         [N,L,k] uint8   as for moe_schedule
+ * perm           [N] int32       the batches' token ids, batch 0 first
+ * batch_offsets  [B+1] int32     batch j is perm[batch_offsets[j] ..
+ *                                batch_offsets[j+1])
+ * demand         [B,L,E] int32   tokens of each batch using (l, e); may be NULL
+ * info           [B-1,8] int64   moe_schedule's info of each split in
+ *                                pre-order (medoids are node-local indices);
+ *                                a split of an empty node records
+ *                                {0, 1, -1, -1, 0, 0, 0, 0}; may be NULL
+ * All arrays are DEVICE memory owned by the caller; the workspace (size from
+ * moe_schedule_multi_workspace, 256-byte aligned) is scratch for the call.
+ * Runs B-1 two-way splits on `stream`, with no host synchronisation.
+ * Limits: those of moe_schedule, and 1 <= B <= 4096 (B > N gives empty
+ *   batches). Errors: MOE_ERR_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, or
+ *   the first error of a split (later splits are then not launched).
+ * ---------------------------------------------------------------------- */
+size_t moe_schedule_multi_workspace(int64_t N, int32_t L, int32_t E, int32_t k, int32_t B);
+int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, int32_t E, int32_t k,
+                       int32_t B, int32_t max_iters, int32_t keep_original_if_worse,
+                       int32_t* perm, int32_t* batch_offsets, int32_t* demand, int64_t* info,
+                       void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * moe_permute -- group the (token, choice) pairs of one batch by expert so

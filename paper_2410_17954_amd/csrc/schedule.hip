@@ -27,6 +27,7 @@
 #include "common.h"
 
 #include <algorithm>
+#include <vector>
 
 namespace moe {
 namespace {
@@ -1345,5 +1346,247 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
                                                cnt_orig, blkcnt, state, err, perm, demand, info);
   MOE_CHECK_LAUNCH();
 #undef MOE_TRY
+  return MOE_OK;
+}
+
+// ==================================================================== B ways
+// B-way rebatching by recursive bisection with the two-way scheduler above: a
+// node holds n tokens (a range of perm) bound for b batches; b == 1 is a batch,
+// otherwise the node's tokens, in their current order, are split with
+// n1 = n * (b / 2) / b and the two halves recurse into b / 2 and b - b / 2
+// batches. The host walks the tree in pre-order (the order of info's rows);
+// every step on the data is a kernel on the caller's stream.
+namespace moe {
+namespace {
+
+constexpr int32_t kMaxMultiBatches = 4096;
+
+struct MultiNode {
+  int64_t lo, n;
+  int32_t b;
+};
+
+// Nodes of the recursion in pre-order (sizes depend on N and B only).
+std::vector<MultiNode> multi_nodes(int64_t N, int32_t B) {
+  std::vector<MultiNode> out, stack{{0, N, B}};
+  while (!stack.empty()) {
+    const MultiNode v = stack.back();
+    stack.pop_back();
+    if (v.b == 1) continue;
+    out.push_back(v);
+    const int32_t bl = v.b / 2;
+    const int64_t n1 = v.n * bl / v.b;
+    stack.push_back({v.lo + n1, v.n - n1, v.b - bl});   // right after left
+    stack.push_back({v.lo, n1, bl});
+  }
+  return out;
+}
+
+struct MultiLayout {
+  size_t sub, routes, tmp, sub_perm, info, total;
+};
+
+MultiLayout multi_layout(int64_t N, int32_t L, int32_t E, int32_t k, int32_t B) {
+  MultiLayout m{};
+  size_t sub = 0;
+  for (const MultiNode& v : multi_nodes(N, B))
+    if (v.n >= 1) sub = std::max(sub, sch_layout(v.n, L, E, k).total);
+  size_t off = align_up(sub, 256);
+  m.sub = 0;
+  m.routes = off;
+  off = align_up(off + (size_t)N * L * k, 256);
+  m.tmp = off;
+  off = align_up(off + (size_t)N * 4, 256);
+  m.sub_perm = off;
+  off = align_up(off + (size_t)N * 4, 256);
+  m.info = off;                               // one info row when the caller passes none
+  off = align_up(off + 8 * sizeof(int64_t), 256);
+  m.total = off;
+  return m;
+}
+
+__global__ void sch_multi_iota(int64_t N, int32_t* __restrict__ ids) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < N) ids[i] = (int32_t)i;
+}
+
+// out[i, :] = routes[ids[i], :] for the n tokens of one node (row = L*k bytes)
+__global__ void sch_multi_gather(const uint8_t* __restrict__ routes, const int32_t* __restrict__ ids,
+                                 int64_t n, int64_t row, uint8_t* __restrict__ out) {
+  const int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (q >= n * row) return;
+  const int64_t i = q / row, c = q - i * row;
+  out[q] = routes[(int64_t)ids[i] * row + c];
+}
+
+// tmp[i] = ids[sub_perm[i]]: the node's tokens in the order its split left them
+__global__ void sch_multi_compose(const int32_t* __restrict__ ids, const int32_t* __restrict__ sub_perm,
+                                  int64_t n, int32_t* __restrict__ tmp) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < n) tmp[i] = ids[sub_perm[i]];
+}
+
+__global__ void sch_multi_copy(const int32_t* __restrict__ src, int64_t n, int32_t* __restrict__ dst) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
+// The info row of a split of an empty node: nothing to split.
+__global__ void sch_multi_info_empty(int64_t* __restrict__ info) {
+  const int q = threadIdx.x;
+  if (q < 8) info[q] = (q == 1) ? 1 : (q == 2 || q == 3) ? -1 : 0;
+}
+
+// offsets[j] for j = 0..B: descend the recursion to batch j's left edge.
+__global__ void sch_multi_offsets(int64_t N, int32_t B, int32_t* __restrict__ offsets) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j > B) return;
+  if (j == B) {
+    offsets[B] = (int32_t)N;
+    return;
+  }
+  int64_t lo = 0, n = N;
+  int32_t b = B, jj = j;
+  while (b > 1) {
+    const int32_t bl = b / 2;
+    const int64_t n1 = n * bl / b;
+    if (jj < bl) {
+      n = n1;
+      b = bl;
+    } else {
+      lo += n1;
+      n -= n1;
+      jj -= bl;
+      b -= bl;
+    }
+  }
+  offsets[j] = (int32_t)lo;
+}
+
+__global__ void sch_multi_zero(int64_t n, int32_t* __restrict__ p) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// demand[b, l, e] = tokens of batch b whose route uses (l, e); one block per
+// batch, counts in LDS when L*E fits (else straight to memory, zeroed first).
+// A token repeating an expert within a layer counts once.
+constexpr int kDemandLdsWords = 16384;
+template <bool LDS>
+__global__ void __launch_bounds__(1024)
+sch_multi_demand(const uint8_t* __restrict__ routes, const int32_t* __restrict__ perm,
+                 const int32_t* __restrict__ offsets, int32_t L, int32_t E, int32_t k,
+                 int32_t* __restrict__ demand) {
+  __shared__ int32_t h[LDS ? kDemandLdsWords : 1];
+  const int b = blockIdx.x;
+  const int64_t LE = (int64_t)L * E;
+  int32_t* const out = demand + (int64_t)b * LE;
+  if (LDS) {
+    for (int64_t q = threadIdx.x; q < LE; q += blockDim.x) h[q] = 0;
+    __syncthreads();
+  }
+  const int64_t lo = offsets[b], hi = offsets[b + 1];
+  const int64_t total = (hi - lo) * L;
+  for (int64_t q = threadIdx.x; q < total; q += blockDim.x) {
+    const int64_t p = lo + q / L;
+    const int l = (int)(q % L);
+    const uint8_t* r = routes + ((int64_t)perm[p] * L + l) * k;
+    for (int j = 0; j < k; ++j) {
+      bool seen = false;
+      for (int jj = 0; jj < j; ++jj) seen |= r[jj] == r[j];
+      if (seen || r[j] >= E) continue;
+      const int64_t cell = (int64_t)l * E + r[j];
+      if (LDS) atomicAdd(&h[cell], 1);
+      else atomicAdd(&out[cell], 1);
+    }
+  }
+  if (LDS) {
+    __syncthreads();
+    for (int64_t q = threadIdx.x; q < LE; q += blockDim.x) out[q] = h[q];
+  }
+}
+
+}  // namespace
+}  // namespace moe
+
+extern "C" size_t moe_schedule_multi_workspace(int64_t N, int32_t L, int32_t E, int32_t k,
+                                               int32_t B) {
+  if (N < 1 || L < 1 || E < 1 || k < 1 || B < 1 || B > moe::kMaxMultiBatches) return 0;
+  return moe::multi_layout(N, L, E, k, B).total;
+}
+
+extern "C" int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, int32_t E,
+                                  int32_t k, int32_t B, int32_t max_iters,
+                                  int32_t keep_original_if_worse, int32_t* perm,
+                                  int32_t* batch_offsets, int32_t* demand, int64_t* info,
+                                  void* workspace, size_t ws_bytes, void* stream) {
+  using namespace moe;
+  MOE_CHECK_ARG(routes && perm && batch_offsets);
+  MOE_CHECK_ARG(N >= 1 && L >= 1 && E >= 1 && E <= 256 && k >= 1 && k <= E);
+  MOE_CHECK_ARG(B >= 1 && B <= kMaxMultiBatches && max_iters >= 1);
+  MOE_CHECK_ARG(keep_original_if_worse == 0 || keep_original_if_worse == 1);
+  if (N >= ((int64_t)1 << 26) || (int64_t)L * E >= ((int64_t)1 << 24) ||
+      (int64_t)L * k >= ((int64_t)1 << 24))
+    return MOE_ERR_UNSUPPORTED;
+  const MultiLayout lay = multi_layout(N, L, E, k, B);
+  if (!workspace || ws_bytes < lay.total || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return MOE_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  void* sub_ws = ws + lay.sub;
+  const size_t sub_bytes = lay.routes;
+  auto* rt = reinterpret_cast<uint8_t*>(ws + lay.routes);
+  auto* tmp = reinterpret_cast<int32_t*>(ws + lay.tmp);
+  auto* sub_perm = reinterpret_cast<int32_t*>(ws + lay.sub_perm);
+  auto* info_scratch = reinterpret_cast<int64_t*>(ws + lay.info);
+  hipStream_t st = as_stream(stream);
+  const int64_t row = (int64_t)L * k;
+  if (ceil_div(N * row, 256) > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
+
+  sch_multi_iota<<<dim3((unsigned)ceil_div(N, 256)), dim3(256), 0, st>>>(N, perm);
+  MOE_CHECK_LAUNCH();
+  const std::vector<MultiNode> nodes = multi_nodes(N, B);
+  for (size_t q = 0; q < nodes.size(); ++q) {
+    const MultiNode& v = nodes[q];
+    int64_t* const info_row = info ? info + 8 * (int64_t)q : info_scratch;
+    if (v.n == 0) {
+      if (info) {
+        sch_multi_info_empty<<<dim3(1), dim3(64), 0, st>>>(info_row);
+        MOE_CHECK_LAUNCH();
+      }
+      continue;
+    }
+    int32_t* const ids = perm + v.lo;
+    const int32_t bl = v.b / 2;
+    const int64_t n1 = v.n * bl / v.b;
+    sch_multi_gather<<<dim3((unsigned)ceil_div(v.n * row, 256)), dim3(256), 0, st>>>(
+        routes, ids, v.n, row, rt);
+    MOE_CHECK_LAUNCH();
+    const int rc = moe_schedule(rt, v.n, L, E, k, n1, max_iters, keep_original_if_worse, sub_perm,
+                                nullptr, info_row, sub_ws, sub_bytes, stream);
+    if (rc != MOE_OK) return rc;
+    const dim3 g((unsigned)ceil_div(v.n, 256));
+    sch_multi_compose<<<g, dim3(256), 0, st>>>(ids, sub_perm, v.n, tmp);
+    MOE_CHECK_LAUNCH();
+    sch_multi_copy<<<g, dim3(256), 0, st>>>(tmp, v.n, ids);
+    MOE_CHECK_LAUNCH();
+  }
+  sch_multi_offsets<<<dim3((unsigned)ceil_div(B + 1, 256)), dim3(256), 0, st>>>(N, B,
+                                                                              batch_offsets);
+  MOE_CHECK_LAUNCH();
+  if (demand) {
+    const int64_t LE = (int64_t)L * E;
+    if (LE <= kDemandLdsWords) {
+      sch_multi_demand<true><<<dim3(B), dim3(1024), 0, st>>>(routes, perm, batch_offsets, L, E, k,
+                                                              demand);
+    } else {
+      const int64_t cells = (int64_t)B * LE;
+      if (ceil_div(cells, 256) > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
+      sch_multi_zero<<<dim3((unsigned)ceil_div(cells, 256)), dim3(256), 0, st>>>(cells, demand);
+      MOE_CHECK_LAUNCH();
+      sch_multi_demand<false><<<dim3(B), dim3(1024), 0, st>>>(routes, perm, batch_offsets, L, E,
+                                                               k, demand);
+    }
+    MOE_CHECK_LAUNCH();
+  }
   return MOE_OK;
 }

@@ -47,6 +47,9 @@ def load_library(path=None):
         "moe_route": (I32, [P, P, I32, I64, I64, I32, I32, P, I32, I32, P, P, P, P]),
         "moe_schedule_workspace": (SZ, [I64, I32, I32, I32]),
         "moe_schedule": (I32, [P, I64, I32, I32, I32, I64, I32, I32, P, P, P, P, SZ, P]),
+        "moe_schedule_multi_workspace": (SZ, [I64, I32, I32, I32, I32]),
+        "moe_schedule_multi": (I32, [P, I64, I32, I32, I32, I32, I32, I32, P, P, P, P, P, SZ,
+                                     P]),
         "moe_permute_workspace": (SZ, [I64, I32, I32]),
         "moe_permute": (I32, [P, I32, I64, I64, P, I64, P, I32, I32, P, P, P, P, P, SZ, P]),
         "moe_expert_ffn_workspace": (SZ, [I64, I64, I64, I32, I32]),
@@ -68,7 +71,8 @@ def load_library(path=None):
 
 def exported_symbols():
     return ["moe_abi_version", "moe_status_str", "moe_route", "moe_schedule_workspace",
-            "moe_schedule", "moe_permute_workspace", "moe_permute",
+            "moe_schedule", "moe_schedule_multi_workspace", "moe_schedule_multi",
+            "moe_permute_workspace", "moe_permute",
             "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_plec_order",
             "moe_plec_run", "moe_lru_run", "moe_load_experts"]
 
@@ -202,6 +206,40 @@ def schedule(routes, E, n1=None, max_iters=10, keep_original_if_worse=True,
                           _ptr(info), _ptr(ws), nbytes, _stream(stream))
     _check("moe_schedule", st)
     return perm, demand, info
+
+
+def schedule_multi_workspace(N, L, E, k, B):
+    return load_library().moe_schedule_multi_workspace(N, L, E, k, B)
+
+
+def schedule_multi(routes, E, B, max_iters=10, keep_original_if_worse=True, perm=None,
+                   batch_offsets=None, demand=None, info=None, workspace=None,
+                   want_demand=True, want_info=True, stream=None):
+    """moe_schedule_multi over routes uint8 [N, L, k] into B batches. Returns
+    (perm int32 [N], batch_offsets int32 [B+1], demand int32 [B, L, E] or None,
+    info int64 [B-1, 8] or None)."""
+    torch = _torch()
+    lib = load_library()
+    _dev(routes)
+    if routes.dtype != torch.uint8 or routes.dim() != 3:
+        raise TypeError("routes must be uint8 [N, L, k]")
+    N, L, k = routes.shape
+    dev = routes.device
+    if perm is None:
+        perm = torch.empty(N, dtype=torch.int32, device=dev)
+    if batch_offsets is None:
+        batch_offsets = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    if demand is None and want_demand:
+        demand = torch.empty((B, L, E), dtype=torch.int32, device=dev)
+    if info is None and want_info and B > 1:
+        info = torch.empty((B - 1, 8), dtype=torch.int64, device=dev)
+    ws, nbytes = _workspace(lib.moe_schedule_multi_workspace(N, L, E, k, B), dev, workspace)
+    st = lib.moe_schedule_multi(_ptr(routes), N, L, E, k, B, max_iters,
+                                1 if keep_original_if_worse else 0, _ptr(perm),
+                                _ptr(batch_offsets), _ptr(demand), _ptr(info), _ptr(ws), nbytes,
+                                _stream(stream))
+    _check("moe_schedule_multi", st)
+    return perm, batch_offsets, demand, info
 
 
 # --------------------------------------------------------------------- permute

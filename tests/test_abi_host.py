@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 14, names
+    assert len(names) == 16, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
@@ -48,6 +48,28 @@ def test_workspace_queries(lib):
     assert lib.moe_permute_workspace(4096, 2, 8) % 256 == 0
     assert lib.moe_expert_ffn_workspace(8192, 4096, 14336, 8, 1) >= 8192 * 14336 * 2
     assert lib.moe_schedule_workspace(8192, 32, 8, 2) > 8192 * 4 * 8
+    # the B-way workspace holds the largest split's plus a gathered copy of the routes
+    assert (lib.moe_schedule_multi_workspace(8192, 32, 8, 2, 4)
+            >= lib.moe_schedule_workspace(8192, 32, 8, 2) + 8192 * 32 * 2)
+    assert lib.moe_schedule_multi_workspace(8192, 32, 8, 2, 0) == 0
+    assert lib.moe_schedule_multi_workspace(8192, 32, 8, 2, 5000) == 0
+
+
+def test_schedule_multi_rejects_bad_arguments(lib):
+    S = None
+    ws = lib.moe_schedule_multi_workspace(16, 2, 8, 2, 4)
+    args = lambda N, E, k, B, perm=FAKE, off=FAKE, it=3, keep=1, nbytes=ws: lib.moe_schedule_multi(
+        FAKE, N, 2, E, k, B, it, keep, perm, off, S, S, FAKE, nbytes, S)
+    assert args(0, 8, 2, 4) == ops.MOE_ERR_ARG            # no tokens
+    assert args(16, 8, 2, 0) == ops.MOE_ERR_ARG           # no batches
+    assert args(16, 8, 2, 4097) == ops.MOE_ERR_ARG        # too many batches
+    assert args(16, 8, 9, 4) == ops.MOE_ERR_ARG           # k > E
+    assert args(16, 300, 2, 4) == ops.MOE_ERR_ARG         # E > 256
+    assert args(16, 8, 2, 4, perm=S) == ops.MOE_ERR_ARG   # missing output
+    assert args(16, 8, 2, 4, off=S) == ops.MOE_ERR_ARG
+    assert args(16, 8, 2, 4, it=0) == ops.MOE_ERR_ARG
+    assert args(16, 8, 2, 4, keep=2) == ops.MOE_ERR_ARG
+    assert args(16, 8, 2, 4, nbytes=ws - 1) == ops.MOE_ERR_WORKSPACE
 
 
 def test_route_rejects_bad_arguments(lib):

@@ -114,3 +114,48 @@ def test_long_paths_read_from_memory():
     # fit in LDS next to the column counts and are read from memory
     routes = synth.predicted_routes(3000, 32, 256, 2, 0.7, 1.0, seed=42)
     _check(routes, 256)
+
+
+# ----------------------------------------------------------------- B batches
+def _check_multi(routes, E, B, max_iters=10, keep=True):
+    routes = np.ascontiguousarray(routes, dtype=np.uint8)
+    perm, off, demand, info = ops.schedule_multi(to_dev(routes), E, B, max_iters=max_iters,
+                                                 keep_original_if_worse=keep)
+    rp, ro, rd, ri = oracle.schedule_multi(routes, E, B, max_iters, keep)
+    assert to_host(off).tolist() == ro.tolist()
+    if B > 1:
+        assert to_host(info).tolist() == ri.tolist()
+    assert np.array_equal(to_host(perm), rp)
+    assert np.array_equal(to_host(demand), rd)
+    return rp, ro, ri
+
+
+@pytest.mark.parametrize("N,L,E,k,B,s", [(64, 4, 8, 2, 4, 1.1), (1000, 8, 16, 2, 3, 1.0),
+                                         (777, 3, 64, 6, 5, 1.0), (4097, 2, 256, 4, 8, 0.5)])
+def test_multi_way_markov_routes(N, L, E, k, B, s):
+    routes = synth.predicted_routes(N, L, E, k, 0.7, s, seed=N + B)
+    _check_multi(routes, E, B)
+
+
+@pytest.mark.parametrize("B", [1, 2])
+def test_multi_way_reductions(B):
+    routes = synth.predicted_routes(301, 5, 8, 2, 0.6, 1.0, seed=51)
+    _check_multi(routes, 8, B)
+
+
+def test_multi_way_more_batches_than_tokens():
+    routes = synth.predicted_routes(3, 2, 4, 2, 0.5, 0.8, seed=44)
+    _check_multi(routes, 4, 8)
+
+
+def test_multi_way_no_guard_and_one_round():
+    routes = synth.predicted_routes(2000, 6, 8, 2, 0.5, 0.8, seed=52)
+    _check_multi(routes, 8, 4, max_iters=1, keep=False)
+
+
+def test_multi_way_mixtral_unit_four_batches():
+    cfg = synth.config(2)
+    routes = synth.predicted_routes(2 * cfg["T"], cfg["L"], cfg["E"], cfg["k"], cfg["keep"],
+                                    cfg["zipf"], seed=53)
+    rp, ro, ri = _check_multi(routes, cfg["E"], 4)
+    assert ro.tolist() == [0, 2048, 4096, 6144, 8192]
