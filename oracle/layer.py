@@ -1,6 +1,7 @@
 """The composed MoE layer of Sec. 2.1 (gate, expert evaluation, weighted sum),
 over one batch and one resident set, plus the dense FFN that a one-expert
-top-1 layer must reduce to (the pin of the whole composition)."""
+top-1 layer must reduce to (the pin of the whole composition), and a stack of
+such layers with a residual connection between them."""
 import numpy as np
 
 from .gating import route
@@ -32,3 +33,33 @@ def moe_layer(x, w_router, k, w_gate, w_up, w_down, bias=None, renormalize=True,
     return dict(logits=z, idx=idx, w=w, offsets=offsets, row_of_pair=rop,
                 pair_of_row=por, x_perm=xp, y_perm=yp, computed=computed,
                 y_shared=ys, y=y, incomplete=inc)
+
+
+def round_bf16(a):
+    """Round float64 values to the nearest bfloat16 value (8 significant bits,
+    ties to even), returned as float64. Normal range only (|a| >= 2^-126)."""
+    u = np.ascontiguousarray(a, dtype=np.float64).view(np.uint64)
+    drop = np.uint64(45)                         # 52 - 7 fraction bits dropped
+    lsb = (u >> drop) & np.uint64(1)
+    r = (u + (np.uint64(1) << np.uint64(44)) - np.uint64(1) + lsb) >> drop << drop
+    return r.view(np.float64)
+
+
+def moe_stack(h, layers, k, renormalize=True):
+    """A stack of MoE layers with a residual connection (the transformer blocks
+    of Sec. 2.1 with the attention half left out): h_{l+1} = h_l + y_l, y_l the
+    MoE layer's output on h_l. The state between layers is stored in bfloat16
+    (h_{l+1} rounded once), as the HIP path stores it.
+
+    layers: list of dicts with w_router [E, H], w_gate/w_up [S, F, H], w_down
+    [S, H, F] and optionally slot_of_expert [E]. Returns (h_L, inputs [L, n, H],
+    idx [L, n, k])."""
+    h = np.asarray(h, dtype=np.float64)
+    ins, idxs = [], []
+    for lay in layers:
+        ins.append(h)
+        out = moe_layer(h, lay["w_router"], k, lay["w_gate"], lay["w_up"], lay["w_down"],
+                        renormalize=renormalize, slot_of_expert=lay.get("slot_of_expert"))
+        idxs.append(out["idx"])
+        h = round_bf16(h + out["y"])
+    return h, np.stack(ins), np.stack(idxs)
