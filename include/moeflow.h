@@ -5,12 +5,15 @@
  *
  *   moe_route       softmax top-k gating                        (Sec. 2.1)
  *   moe_schedule    balanced rebatching of two adjacent batches
- *   moe_schedule_multi  the same into B batches by recursive bisection
  *                   by predicted routing path                   (Sec. 3.3, Eq. 2)
+ *   moe_schedule_multi  the same into B batches by recursive bisection
  *   moe_permute     expert-major grouping of (token, choice) pairs
  *   moe_expert_ffn  grouped SwiGLU experts over the resident
  *                   slots of the expert cache                   (Sec. 2.1, 3.4)
  *   moe_combine     gate-weighted sum of expert outputs         (Sec. 2.1)
+ *   moe_kv_gather   KV-cache Merge / Reindex row movement       (Sec. 3.3.3)
+ *   moe_kv_reindex  new batch and position of every token       (Sec. 3.3.3)
+ *   moe_stack_forward   a batch through L residual MoE layers   (Sec. 2.1)
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -156,6 +159,70 @@ int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, int32_t E, i
                        int32_t B, int32_t max_iters, int32_t keep_original_if_worse,
                        int32_t* perm, int32_t* batch_offsets, int32_t* demand, int64_t* info,
                        void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_kv_gather -- KV-cache Merge and the row movement of Reindex (Sec. 3.3.3).
+ * Rebatching moves tokens between batches; the KV state each token carries
+ * follows it. Merge aggregates the original batches' caches in global token
+ * order (source 0's tokens, then source 1's, ...); Reindex places global token
+ * index[p] at new position p.
+ *
+ * sources[b]        DEVICE pointer: source b's cache, [L, source_tokens[b], row_bytes]
+ *                   (the pointer array itself is HOST memory, n_sources <= 16)
+ * index [n_out]     DEVICE int32 global token ids, or NULL for the merge itself
+ *                   (then n_out must equal the total token count)
+ * dst               DEVICE [L, n_out, row_bytes]: dst[l][p] = merged[l][index[p]]
+ * err               DEVICE int32, set to 1 if an index is out of range (that row
+ *                   is not written); the caller clears it
+ * Rows move in 16-byte pieces when row_bytes and every pointer allow, else bytes.
+ * Errors: MOE_ERR_ARG (missing pointer, n_sources outside 1..16, sizes < 0).
+ * ---------------------------------------------------------------------- */
+int moe_kv_gather(const void* const* sources, const int64_t* source_tokens, int32_t n_sources,
+                  int64_t L, int64_t row_bytes, const int32_t* index, int64_t n_out, void* dst,
+                  int32_t* err, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_kv_reindex -- the index maps of Reindex (Sec. 3.3.3): new position p of
+ * batch b (batch_offsets[b] <= p < batch_offsets[b+1]) holds global token
+ * perm[p]; for every global token g, batch_of[g] = its new batch and pos_of[g]
+ * = its position there (either output may be NULL, not both).
+ * perm [N], batch_offsets [B+1] (as moe_schedule_multi writes them), batch_of
+ * and pos_of [N]: DEVICE int32. err as for moe_kv_gather (a perm entry outside
+ * 0..N-1). Limits: 1 <= N < 2^31, B >= 1.
+ * ---------------------------------------------------------------------- */
+int moe_kv_reindex(const int32_t* perm, int64_t N, const int32_t* batch_offsets, int32_t B,
+                   int32_t* batch_of, int32_t* pos_of, int32_t* err, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_stack_forward -- one batch through a stack of L MoE layers with a
+ * residual connection (Sec. 2.1's blocks, attention left out):
+ *   h <- h + MoE_l(h),  l = 0..L-1,
+ * each layer moe_route -> moe_permute -> moe_expert_ffn -> moe_combine with
+ * accumulate = 1 (so h is rounded to dtype once per layer).
+ *
+ * h [n_tokens, H]   DEVICE, updated in place; the batch is rows token_ids[0..T)
+ *                   (or rows 0..T when token_ids is NULL, then n_tokens == T)
+ * w_router, w_gate, w_up, w_down   HOST arrays of L DEVICE pointers: layer l's
+ *                   router [E, H] and expert slots [S, F, H], [S, F, H], [S, H, F]
+ * slot_of_expert    DEVICE int32 [L, E] (-1 = not resident: those choices are
+ *                   skipped) or NULL (every expert resident, S == E)
+ * h_trace           DEVICE [L, T, H] or NULL: the batch's state entering each layer
+ * idx_trace         DEVICE int32 [L, T, k] or NULL: each layer's top-k experts
+ * err               DEVICE int32, set to 1 on an out-of-range token id
+ * Runs on `stream` with no host synchronisation; the workspace comes from
+ * moe_stack_workspace (256-byte aligned). Limits: those of the four stages;
+ * H * element size a multiple of 16 and h, h_trace 16-byte aligned.
+ * Errors: MOE_ERR_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, or the first
+ * error of a stage (later layers are then not launched).
+ * ---------------------------------------------------------------------- */
+size_t moe_stack_workspace(int64_t T, int64_t H, int64_t F, int32_t E, int32_t k, int32_t dtype);
+int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64_t H,
+                      const int32_t* token_ids, int64_t T, int32_t L, int32_t E, int32_t k,
+                      int64_t F, const void* const* w_router, const void* const* w_gate,
+                      const void* const* w_up, const void* const* w_down,
+                      const int32_t* slot_of_expert, int32_t S, int32_t renormalize,
+                      void* h_trace, int32_t* idx_trace, int32_t* err, void* workspace,
+                      size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * moe_permute -- group the (token, choice) pairs of one batch by expert so

@@ -1,0 +1,162 @@
+// A batch through a stack of MoE layers (Sec. 2.1's transformer blocks with the
+// attention half left out): h <- h + MoE_l(h) for l = 0..L-1, each layer the
+// path route -> permute -> expert FFN -> combine, the residual added by the
+// combine's accumulate mode (one bf16 rounding of h per layer). The batch's
+// rows are gathered into a contiguous buffer once, run through every layer in
+// place, and scattered back, so the route step sees a dense [T, H] batch.
+#include "moeflow.h"
+#include "common.h"
+
+#include <algorithm>
+
+namespace moe {
+namespace {
+
+struct StackLayout {
+  size_t xb, idx, w, offs, rop, por, xp, yp, inc, pws, fws, total;
+  size_t pws_bytes, fws_bytes;
+};
+
+StackLayout stack_layout(int64_t T, int64_t H, int64_t F, int32_t E, int32_t k, int32_t dtype) {
+  const size_t elt = dtype == MOE_BF16 ? 2 : 4;
+  const int64_t P = T * k;
+  StackLayout s{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  s.xb = take((size_t)T * H * elt);
+  s.idx = take((size_t)P * 4);
+  s.w = take((size_t)P * 4);
+  s.offs = take((size_t)(E + 1) * 4);
+  s.rop = take((size_t)P * 4);
+  s.por = take((size_t)P * 4);
+  s.xp = take((size_t)P * H * elt);
+  s.yp = take((size_t)P * H * elt);
+  s.inc = take((size_t)T * 4);
+  s.pws_bytes = moe_permute_workspace(T, k, E);
+  s.pws = take(s.pws_bytes);
+  s.fws_bytes = moe_expert_ffn_workspace(P, H, F, E, dtype);
+  s.fws = take(s.fws_bytes);
+  s.total = o;
+  return s;
+}
+
+// dst row i = src row rows[i] (gather) or dst row rows[i] = src row i (scatter)
+template <bool SCATTER>
+__global__ void stack_rows_kernel(const char* __restrict__ src, char* __restrict__ dst,
+                                  const int32_t* __restrict__ rows, int64_t T, int64_t n_rows,
+                                  int64_t row_chunks, int32_t* __restrict__ err) {
+  const int64_t total = T * row_chunks;
+  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < total;
+       q += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = q / row_chunks, c = q - i * row_chunks;
+    const int64_t r = rows[i];
+    if (r < 0 || r >= n_rows) {
+      if (c == 0) atomicExch(err, 1);
+      continue;
+    }
+    const int64_t si = SCATTER ? i : r, di = SCATTER ? r : i;
+    reinterpret_cast<uint4*>(dst)[di * row_chunks + c] =
+        reinterpret_cast<const uint4*>(src)[si * row_chunks + c];
+  }
+}
+
+__global__ void stack_copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                  int64_t n) {
+  for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n;
+       q += (int64_t)gridDim.x * blockDim.x)
+    dst[q] = src[q];
+}
+
+}  // namespace
+}  // namespace moe
+
+extern "C" size_t moe_stack_workspace(int64_t T, int64_t H, int64_t F, int32_t E, int32_t k,
+                                      int32_t dtype) {
+  if (T < 1 || H < 1 || F < 1 || E < 1 || k < 1 || (dtype != MOE_BF16 && dtype != MOE_F32))
+    return 0;
+  return moe::stack_layout(T, H, F, E, k, dtype).total;
+}
+
+extern "C" int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64_t H,
+                                 const int32_t* token_ids, int64_t T, int32_t L, int32_t E,
+                                 int32_t k, int64_t F, const void* const* w_router,
+                                 const void* const* w_gate, const void* const* w_up,
+                                 const void* const* w_down, const int32_t* slot_of_expert,
+                                 int32_t S, int32_t renormalize, void* h_trace,
+                                 int32_t* idx_trace, int32_t* err, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  using namespace moe;
+  MOE_CHECK_ARG(h && w_router && w_gate && w_up && w_down && err);
+  MOE_CHECK_ARG(dtype == MOE_BF16 || dtype == MOE_F32);
+  MOE_CHECK_ARG(T >= 1 && n_tokens >= T && H >= 1 && F >= 1 && L >= 1);
+  MOE_CHECK_ARG(E >= 1 && E <= 256 && k >= 1 && k <= E && S >= 1);
+  MOE_CHECK_ARG(slot_of_expert || S == E);
+  MOE_CHECK_ARG(renormalize == 0 || renormalize == 1);
+  MOE_CHECK_ARG(token_ids || n_tokens == T);
+  const size_t elt = dtype == MOE_BF16 ? 2 : 4;
+  if ((H * (int64_t)elt) % 16 != 0 || (reinterpret_cast<uintptr_t>(h) & 15) ||
+      (reinterpret_cast<uintptr_t>(h_trace) & 15))
+    return MOE_ERR_UNSUPPORTED;                                  // 16-byte row copies
+  for (int32_t l = 0; l < L; ++l)
+    MOE_CHECK_ARG(w_router[l] && w_gate[l] && w_up[l] && w_down[l]);
+  const StackLayout lay = stack_layout(T, H, F, E, k, dtype);
+  if (!workspace || ws_bytes < lay.total || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return MOE_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t st = as_stream(stream);
+  const int64_t P = T * k;
+  const int64_t row_chunks = H * (int64_t)elt / 16;
+  const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(T * row_chunks, 256),
+                                                    16 * (int64_t)device_cu_count());
+  void* xb = token_ids ? static_cast<void*>(ws + lay.xb) : h;
+  auto* idx = reinterpret_cast<int32_t*>(ws + lay.idx);
+  auto* w = reinterpret_cast<float*>(ws + lay.w);
+  auto* offs = reinterpret_cast<int32_t*>(ws + lay.offs);
+  auto* rop = reinterpret_cast<int32_t*>(ws + lay.rop);
+  auto* por = reinterpret_cast<int32_t*>(ws + lay.por);
+  void* xp = ws + lay.xp;
+  void* yp = ws + lay.yp;
+  auto* inc = reinterpret_cast<int32_t*>(ws + lay.inc);
+
+  if (token_ids) {
+    stack_rows_kernel<false><<<dim3(grid), dim3(256), 0, st>>>(
+        static_cast<const char*>(h), static_cast<char*>(xb), token_ids, T, n_tokens, row_chunks,
+        err);
+    MOE_CHECK_LAUNCH();
+  }
+  int rc = MOE_OK;
+  for (int32_t l = 0; l < L && rc == MOE_OK; ++l) {
+    if (h_trace) {
+      stack_copy_kernel<<<dim3(grid), dim3(256), 0, st>>>(
+          static_cast<const uint4*>(xb),
+          reinterpret_cast<uint4*>(static_cast<char*>(h_trace) + (size_t)l * T * H * elt),
+          T * row_chunks);
+      MOE_CHECK_LAUNCH();
+    }
+    int32_t* const idx_l = idx_trace ? idx_trace + (int64_t)l * P : idx;
+    const int32_t* const slot_l = slot_of_expert ? slot_of_expert + (int64_t)l * E : nullptr;
+    rc = moe_route(xb, w_router[l], dtype, T, H, E, k, nullptr, 0, renormalize, nullptr, idx_l,
+                   w, stream);
+    if (rc != MOE_OK) break;
+    rc = moe_permute(xb, dtype, H, T, nullptr, T, idx_l, k, E, offs, rop, por, xp, ws + lay.pws,
+                     lay.pws_bytes, stream);
+    if (rc != MOE_OK) break;
+    rc = moe_expert_ffn(xp, dtype, P, H, F, offs, E, slot_l, S, w_gate[l], w_up[l], w_down[l], yp,
+                        ws + lay.fws, lay.fws_bytes, stream);
+    if (rc != MOE_OK) break;
+    rc = moe_combine(yp, dtype, H, P, nullptr, T, T, k, idx_l, w, rop, slot_l, E, nullptr, 1, xb,
+                     inc, stream);
+  }
+  if (rc != MOE_OK) return rc;
+  if (token_ids) {
+    stack_rows_kernel<true><<<dim3(grid), dim3(256), 0, st>>>(
+        static_cast<const char*>(xb), static_cast<char*>(h), token_ids, T, n_tokens, row_chunks,
+        err);
+    MOE_CHECK_LAUNCH();
+  }
+  return MOE_OK;
+}

@@ -47,6 +47,11 @@ def load_library(path=None):
         "moe_route": (I32, [P, P, I32, I64, I64, I32, I32, P, I32, I32, P, P, P, P]),
         "moe_schedule_workspace": (SZ, [I64, I32, I32, I32]),
         "moe_schedule": (I32, [P, I64, I32, I32, I32, I64, I32, I32, P, P, P, P, SZ, P]),
+        "moe_kv_gather": (I32, [P, P, I32, I64, I64, P, I64, P, P, P]),
+        "moe_kv_reindex": (I32, [P, I64, P, I32, P, P, P, P]),
+        "moe_stack_workspace": (SZ, [I64, I64, I64, I32, I32, I32]),
+        "moe_stack_forward": (I32, [P, I32, I64, I64, P, I64, I32, I32, I32, I64, P, P, P, P, P,
+                                    I32, I32, P, P, P, P, SZ, P]),
         "moe_schedule_multi_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "moe_schedule_multi": (I32, [P, I64, I32, I32, I32, I32, I32, I32, P, P, P, P, P, SZ,
                                      P]),
@@ -73,7 +78,8 @@ def exported_symbols():
     return ["moe_abi_version", "moe_status_str", "moe_route", "moe_schedule_workspace",
             "moe_schedule", "moe_schedule_multi_workspace", "moe_schedule_multi",
             "moe_permute_workspace", "moe_permute",
-            "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_plec_order",
+            "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_kv_gather",
+            "moe_kv_reindex", "moe_stack_workspace", "moe_stack_forward", "moe_plec_order",
             "moe_plec_run", "moe_lru_run", "moe_load_experts"]
 
 
@@ -240,6 +246,100 @@ def schedule_multi(routes, E, B, max_iters=10, keep_original_if_worse=True, perm
                                 _stream(stream))
     _check("moe_schedule_multi", st)
     return perm, batch_offsets, demand, info
+
+
+# ------------------------------------------------------------------- KV cache
+def kv_gather(sources, index=None, out=None, err=None, stream=None):
+    """moe_kv_gather. sources: list of device tensors [L, T_b, ...] (one per
+    original batch, same dtype and trailing shape); index int32 [n_out] or
+    None (the merge). Returns (out [L, n_out, ...], err int32 [1])."""
+    torch = _torch()
+    lib = load_library()
+    if not sources or len(sources) > 16:
+        raise ValueError("1 to 16 sources")
+    _dev(*sources, index)
+    L = sources[0].shape[0]
+    tail = tuple(sources[0].shape[2:])
+    for s_ in sources:
+        if s_.shape[0] != L or tuple(s_.shape[2:]) != tail or s_.dtype != sources[0].dtype:
+            raise ValueError("sources must share L, dtype and the trailing shape")
+        if not s_.is_contiguous():
+            raise ValueError("sources must be contiguous")
+    row_bytes = sources[0].element_size()
+    for d in tail:
+        row_bytes *= d
+    total = sum(s_.shape[1] for s_ in sources)
+    n_out = total if index is None else index.shape[0]
+    dev = sources[0].device
+    if out is None:
+        out = torch.empty((L, n_out) + tail, dtype=sources[0].dtype, device=dev)
+    if err is None:
+        err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ptrs = (ctypes.c_void_p * len(sources))(*[s_.data_ptr() for s_ in sources])
+    rows = (ctypes.c_int64 * len(sources))(*[s_.shape[1] for s_ in sources])
+    st = lib.moe_kv_gather(ptrs, rows, len(sources), L, row_bytes, _ptr(index), n_out,
+                           _ptr(out), _ptr(err), _stream(stream))
+    _check("moe_kv_gather", st)
+    return out, err
+
+
+def kv_reindex(perm, batch_offsets, batch_of=None, pos_of=None, err=None, stream=None):
+    """moe_kv_reindex. Returns (batch_of int32 [N], pos_of int32 [N], err)."""
+    torch = _torch()
+    lib = load_library()
+    _dev(perm, batch_offsets)
+    N = perm.shape[0]
+    B = batch_offsets.shape[0] - 1
+    dev = perm.device
+    if batch_of is None:
+        batch_of = torch.empty(N, dtype=torch.int32, device=dev)
+    if pos_of is None:
+        pos_of = torch.empty(N, dtype=torch.int32, device=dev)
+    if err is None:
+        err = torch.zeros(1, dtype=torch.int32, device=dev)
+    st = lib.moe_kv_reindex(_ptr(perm), N, _ptr(batch_offsets), B, _ptr(batch_of), _ptr(pos_of),
+                            _ptr(err), _stream(stream))
+    _check("moe_kv_reindex", st)
+    return batch_of, pos_of, err
+
+
+# ----------------------------------------------------------------------- stack
+def stack_workspace(T, H, F, E, k, dtype_code=MOE_BF16):
+    return load_library().moe_stack_workspace(T, H, F, E, k, dtype_code)
+
+
+def stack_forward(h, layers, k, token_ids=None, slot_of_expert=None, S=None, renormalize=True,
+                  h_trace=None, idx_trace=None, err=None, workspace=None, stream=None):
+    """moe_stack_forward: the batch (rows token_ids of h, or all rows) through
+    the layers, h updated in place. layers: list of (w_router [E,H], w_gate
+    [S,F,H], w_up [S,F,H], w_down [S,H,F]) device tensors. Returns (h, err)."""
+    torch = _torch()
+    lib = load_library()
+    _dev(h, token_ids, slot_of_expert, h_trace, idx_trace)
+    n_tokens, H = h.shape
+    T = token_ids.shape[0] if token_ids is not None else n_tokens
+    L = len(layers)
+    E = layers[0][0].shape[0]
+    Sw, F, _ = layers[0][1].shape
+    S = Sw if S is None else S
+    dt = _dtype_code(h)
+    for lay in layers:
+        _dev(*lay)
+        if (tuple(lay[0].shape) != (E, H) or tuple(lay[1].shape) != (Sw, F, H)
+                or tuple(lay[2].shape) != (Sw, F, H) or tuple(lay[3].shape) != (Sw, H, F)):
+            raise ValueError("every layer must be router [E,H], w_gate/w_up [S,F,H], w_down [S,H,F]")
+        if any(t.dtype != h.dtype or not t.is_contiguous() for t in lay):
+            raise ValueError("layer weights must be contiguous with the dtype of h")
+    if err is None:
+        err = torch.zeros(1, dtype=torch.int32, device=h.device)
+    arr = lambda j: (ctypes.c_void_p * L)(*[lay[j].data_ptr() for lay in layers])
+    ws, nbytes = _workspace(lib.moe_stack_workspace(T, H, F, E, k, dt), h.device, workspace)
+    st = lib.moe_stack_forward(_ptr(h), dt, n_tokens, H, _ptr(token_ids), T, L, E, k, F, arr(0),
+                               arr(1), arr(2), arr(3), _ptr(slot_of_expert), S,
+                               1 if renormalize else 0, _ptr(h_trace), _ptr(idx_trace), _ptr(err),
+                               _ptr(ws), nbytes, _stream(stream))
+    _check("moe_stack_forward", st)
+    return h, err
 
 
 # --------------------------------------------------------------------- permute

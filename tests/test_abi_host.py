@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 16, names
+    assert len(names) == 20, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
@@ -133,3 +133,26 @@ def test_plan_slots_host_rule():
     assert slot.tolist() == [0, -1, 1, 2, -1]
     assert ops.plan_slots(np.array([1, 2]), 0).tolist() == [-1, -1]
     assert ops.plan_slots(np.array([1, 2]), 5).tolist() == [0, 1]
+
+
+def test_kv_and_stack_reject_bad_arguments(lib):
+    S = None
+    one = (ctypes.c_int64 * 1)(10)
+    ptrs = (ctypes.c_void_p * 1)(0x1000)
+    # no sources, 17 sources, merge with n_out != total, missing err
+    assert lib.moe_kv_gather(ptrs, one, 0, 2, 64, S, 10, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_kv_gather(ptrs, one, 17, 2, 64, S, 10, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_kv_gather(ptrs, one, 1, 2, 64, S, 9, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_kv_gather(ptrs, one, 1, 2, 64, S, 10, FAKE, S, S) == ops.MOE_ERR_ARG
+    assert lib.moe_kv_reindex(FAKE, 0, FAKE, 2, FAKE, FAKE, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_kv_reindex(FAKE, 10, FAKE, 2, S, S, FAKE, S) == ops.MOE_ERR_ARG
+    w = (ctypes.c_void_p * 2)(0x1000, 0x1000)
+    ws = lib.moe_stack_workspace(16, 64, 64, 8, 2, 1)
+    call = lambda T=16, n=16, E=8, k=2, S_=8, slot=S, tok=S, nbytes=ws, wr=w: lib.moe_stack_forward(
+        FAKE, 1, n, 64, tok, T, 2, E, k, 64, wr, w, w, w, slot, S_, 1, S, S, FAKE, FAKE, nbytes, S)
+    assert call(T=0) == ops.MOE_ERR_ARG
+    assert call(n=20) == ops.MOE_ERR_ARG                  # n_tokens != T without token ids
+    assert call(k=9) == ops.MOE_ERR_ARG
+    assert call(S_=4) == ops.MOE_ERR_ARG                  # S < E needs a slot table
+    assert call(wr=(ctypes.c_void_p * 2)(0x1000, 0)) == ops.MOE_ERR_ARG
+    assert call(nbytes=ws - 1) == ops.MOE_ERR_WORKSPACE
