@@ -25,7 +25,7 @@ Modules and the passages they follow:
   cache     -- cross-layer slot planning, real-time correction and the LRU
                baseline of the expert cache engine (Sec. 3.4)
   layer     -- the composed MoE layer, the dense-FFN identity used as a pin, and
-               a residual stack of layers
+               a residual stack of pre-normalised layers
   kv        -- KV-cache Merge and Reindex of Sec. 3.3.3
 """
 from .gating import router_logits, topk_select, softmax, gate_weights, route
@@ -37,7 +37,7 @@ from .schedule import (route_bits, eq2_objective, signature_rank, hamming_to,
                        schedule_multi)
 from .slots import plan_slots
 from .cache import plec_order, plec_run, lru_run
-from .layer import moe_layer, dense_ffn, moe_stack, round_bf16
+from .layer import moe_layer, dense_ffn, moe_stack, round_bf16, rms_norm
 from .kv import kv_merge, kv_gather, kv_reindex
 
 __all__ = [
@@ -47,6 +47,6 @@ __all__ = [
     "cluster_distance_sums", "schedule", "batch_accuracy", "multi_batch_offsets",
     "schedule_multi", "plan_slots",
     "plec_order", "plec_run", "lru_run",
-    "moe_layer", "dense_ffn", "moe_stack", "round_bf16",
+    "moe_layer", "dense_ffn", "moe_stack", "round_bf16", "rms_norm",
     "kv_merge", "kv_gather", "kv_reindex",
 ]

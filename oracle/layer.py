@@ -45,21 +45,32 @@ def round_bf16(a):
     return r.view(np.float64)
 
 
-def moe_stack(h, layers, k, renormalize=True):
-    """A stack of MoE layers with a residual connection (the transformer blocks
-    of Sec. 2.1 with the attention half left out): h_{l+1} = h_l + y_l, y_l the
-    MoE layer's output on h_l. The state between layers is stored in bfloat16
-    (h_{l+1} rounded once), as the HIP path stores it.
+def rms_norm(h, weight=None, eps=1e-5):
+    """Root-mean-square normalisation of each row (the pre-norm of the MoE
+    blocks of Table 1's models): h / sqrt(mean(h^2) + eps) * weight."""
+    h = np.asarray(h, dtype=np.float64)
+    r = h / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps)
+    return r if weight is None else r * np.asarray(weight, dtype=np.float64)
+
+
+def moe_stack(h, layers, k, renormalize=True, pre_norm=False, eps=1e-5):
+    """A stack of MoE blocks with a residual connection (the transformer blocks
+    of Sec. 2.1 with the attention half left out): x_l = h_l, or with pre_norm
+    x_l = bf16(rms_norm(h_l, norm_l)); h_{l+1} = h_l + y_l, y_l the MoE layer's
+    output on x_l. The state between layers is stored in bfloat16 (h_{l+1}
+    rounded once), as the HIP path stores it.
 
     layers: list of dicts with w_router [E, H], w_gate/w_up [S, F, H], w_down
-    [S, H, F] and optionally slot_of_expert [E]. Returns (h_L, inputs [L, n, H],
-    idx [L, n, k])."""
+    [S, H, F], optionally slot_of_expert [E] and norm [H]. Returns (h_L,
+    states [L, n, H], inputs [L, n, H], idx [L, n, k])."""
     h = np.asarray(h, dtype=np.float64)
-    ins, idxs = [], []
+    states, ins, idxs = [], [], []
     for lay in layers:
-        ins.append(h)
-        out = moe_layer(h, lay["w_router"], k, lay["w_gate"], lay["w_up"], lay["w_down"],
+        states.append(h)
+        x = round_bf16(rms_norm(h, lay.get("norm"), eps)) if pre_norm else h
+        ins.append(x)
+        out = moe_layer(x, lay["w_router"], k, lay["w_gate"], lay["w_up"], lay["w_down"],
                         renormalize=renormalize, slot_of_expert=lay.get("slot_of_expert"))
         idxs.append(out["idx"])
         h = round_bf16(h + out["y"])
-    return h, np.stack(ins), np.stack(idxs)
+    return h, np.stack(states), np.stack(ins), np.stack(idxs)

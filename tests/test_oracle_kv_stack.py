@@ -74,7 +74,7 @@ def _stack_inputs(L, T=9, seed=5, E=None):
 
 def test_one_expert_top1_stack_is_the_dense_residual_stack():
     cfg, x, layers = _stack_inputs(3, E=1)
-    h, ins, idx = oracle.moe_stack(x, layers, 1)
+    h, states, ins, idx = oracle.moe_stack(x, layers, 1)
     ref = x.copy()
     for d in layers:                                # written out with numpy alone
         g = ref @ d["w_gate"][0].T
@@ -89,21 +89,41 @@ def test_zero_experts_leave_the_state_unchanged():
     cfg, x, layers = _stack_inputs(2)
     for d in layers:
         d["w_down"] = np.zeros_like(d["w_down"])
-    h, _, _ = oracle.moe_stack(x, layers, cfg["k"])
+    h, _, _, _ = oracle.moe_stack(x, layers, cfg["k"], pre_norm=True)
     assert np.array_equal(h, x)
 
 
 def test_tokens_are_independent_through_the_stack():
     cfg, x, layers = _stack_inputs(3, T=7)
-    h, _, idx = oracle.moe_stack(x, layers, cfg["k"])
+    h, _, _, idx = oracle.moe_stack(x, layers, cfg["k"], pre_norm=True)
     for t in (0, 3, 6):
-        ht, _, it = oracle.moe_stack(x[t:t + 1], layers, cfg["k"])
+        ht, _, _, it = oracle.moe_stack(x[t:t + 1], layers, cfg["k"], pre_norm=True)
         assert np.allclose(ht[0], h[t], rtol=0, atol=1e-12)
         assert np.array_equal(it[:, 0], idx[:, t])
 
 
 def test_stack_state_is_bf16_between_layers():
     cfg, x, layers = _stack_inputs(2)
-    h, ins, _ = oracle.moe_stack(x, layers, cfg["k"])
-    for a in (ins[1], h):
+    h, states, ins, _ = oracle.moe_stack(x, layers, cfg["k"], pre_norm=True)
+    for a in (states[1], ins[0], ins[1], h):
         assert np.array_equal(oracle.round_bf16(a), a)
+
+
+def test_rms_norm_closed_forms():
+    g = np.random.default_rng(6)
+    h = g.standard_normal((5, 64)) * 3
+    r = oracle.rms_norm(h, eps=0.0)
+    assert np.allclose((r * r).mean(axis=1), 1.0, rtol=1e-14)       # unit mean square
+    assert np.allclose(oracle.rms_norm(7.5 * h, eps=0.0), r, rtol=1e-14)   # scale-free
+    c = np.full((1, 16), -2.0)                                      # a constant row
+    w = np.arange(16, dtype=np.float64)
+    assert np.allclose(oracle.rms_norm(c, w, eps=0.25), -2.0 / np.sqrt(4.25) * w, rtol=1e-15)
+
+
+def test_pre_norm_keeps_the_stack_bounded():
+    # without the norm SwiGLU's growth compounds over layers; with it the
+    # input of every block has unit mean square
+    cfg, x, layers = _stack_inputs(4)
+    _, _, ins, _ = oracle.moe_stack(x * 10, layers, cfg["k"], pre_norm=True)
+    ms = (ins * ins).mean(axis=2)
+    assert np.allclose(ms, 1.0, rtol=1e-2)
