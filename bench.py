@@ -52,6 +52,12 @@ def parse():
                    help="instead of the layer throughput, measure B-way rebatching by "
                         "recursive bisection (B = 2 to 64 batches of 64 tokens, Qwen-shaped "
                         "24-layer predicted routes): time and active (layer, expert) pairs")
+    p.add_argument("--stack", action="store_true",
+                   help="instead of the one-layer throughput, run the dual-batch pipeline over "
+                        "the 32-layer Mixtral-shaped stack (8192-token units, KV caches merged "
+                        "and reindexed) with and without the scheduling stream overlapped")
+    p.add_argument("--stack-layers", type=int, default=32)
+    p.add_argument("--stack-units", type=int, default=3)
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 counter_collection.csv files (FETCH_SIZE, "
                         "WRITE_SIZE) of a --copy-probe-mib run into the traffic file, then exit")
@@ -358,6 +364,92 @@ def ways_report(args):
     print(json.dumps(rec))
 
 
+def stack_report(args):
+    """Dual-batch pipeline over a stack of MoE layers (one JSON line).
+
+    Units of 8192 tokens (two 4096-token batches) with 32-layer predicted
+    routes; each unit is rebatched by the token scheduler, its two original
+    batches' KV caches (Mixtral: 8 KV heads x 128 x K,V in bf16 = 4 KB per token
+    and layer) merged and reindexed into the new layout, and both new batches
+    run through the layer stack (RMS pre-normalised blocks, every expert of
+    every layer resident in HBM: 32 x 2.8 GB). Timed with and without the next
+    unit's scheduling and KV work on a second stream."""
+    import torch
+    from paper_2410_17954_amd import ops, pipeline, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.config(3)
+    H, E, F, k = cfg["H"], cfg["E"], cfg["F"], cfg["k"]
+    L = args.stack_layers
+    N = cfg["T"]                                   # one unit: two batches of N / 2
+    kv_row = 8 * 128 * 2 * 2
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+
+    def rnd(shape, scale):
+        t = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+        t.normal_(0.0, scale, generator=g)
+        return t
+
+    layers = [(rnd((E, H), 0.02), rnd((E, F, H), 0.02), rnd((E, F, H), 0.02),
+               rnd((E, H, F), 0.02)) for _ in range(L)]
+    n_units = 1 + args.stack_units
+
+    def make_units(seed0):
+        us = []
+        for u in range(n_units):
+            routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], seed0 + u)
+            us.append(pipeline.Unit(
+                h=rnd((N, H), 1.0),
+                routes=torch.from_numpy(np.ascontiguousarray(routes, dtype=np.uint8)).to(dev),
+                kv=[torch.randint(0, 256, (L, N // 2, kv_row), dtype=torch.uint8, device=dev,
+                                  generator=g) for _ in range(2)]))
+        return us
+
+    out = {}
+    state = {}
+    for overlap in (True, False):
+        units = make_units(args.seed * 1000)
+        pl = pipeline.DualBatchPipeline(layers, k, E, N, overlap=overlap)
+        pl.run(units[:1])                          # warm-up unit
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pl.run(units[1:])
+        torch.cuda.synchronize()
+        out[overlap] = time.perf_counter() - t0
+        hf = units[-1].h.float()
+        state[overlap] = (bool(torch.isfinite(hf).all().item()), float(hf.abs().mean().item()))
+        del units, pl
+    # the scheduling work of one unit alone (token scheduler + KV merge/reindex)
+    units = make_units(args.seed * 1000 + 7)
+    pl = pipeline.DualBatchPipeline(layers, k, E, N, overlap=False)
+    pl._plan(units[0])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    pl._plan(units[1])
+    e1.record()
+    torch.cuda.synchronize()
+    plan_ms = e0.elapsed_time(e1)
+    toks = args.stack_units * N
+    rec = {"metric": "dual-batch pipeline over a stack of MoE layers: tokens/s through all layers",
+           "config": {"workload": f"Mixtral-8x7B-shaped stack: {L} layers, H={H}, E={E}, F={F}, "
+                                  f"top-{k}, units of {N} tokens (2 batches of {N // 2}), "
+                                  f"32-layer predicted routes, KV rows of {kv_row} B per token "
+                                  f"and layer, every expert resident in HBM",
+                      "units_timed": args.stack_units},
+           "tokens_per_s_overlapped": round(toks / out[True], 1),
+           "tokens_per_s_in_order": round(toks / out[False], 1),
+           "ms_per_unit_overlapped": round(out[True] / args.stack_units * 1e3, 3),
+           "ms_per_unit_in_order": round(out[False] / args.stack_units * 1e3, 3),
+           "schedule_and_kv_ms_per_unit": round(plan_ms, 3),
+           "kv_bytes_moved_per_unit": 2 * L * N * kv_row,
+           "final_state_finite": state[True][0],
+           "final_state_abs_mean": round(state[True][1], 3),
+           "data": "synthetic"}
+    print(json.dumps(rec))
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -379,6 +471,9 @@ def main():
         return
     if args.ways:
         ways_report(args)
+        return
+    if args.stack:
+        stack_report(args)
         return
     import torch
     from paper_2410_17954_amd import ops, synth

@@ -194,11 +194,14 @@ int moe_kv_reindex(const int32_t* perm, int64_t N, const int32_t* batch_offsets,
                    int32_t* batch_of, int32_t* pos_of, int32_t* err, void* stream);
 
 /* ------------------------------------------------------------------------
- * moe_stack_forward -- one batch through a stack of L MoE layers with a
+ * moe_stack_forward -- one batch through a stack of L MoE blocks with a
  * residual connection (Sec. 2.1's blocks, attention left out):
- *   h <- h + MoE_l(h),  l = 0..L-1,
- * each layer moe_route -> moe_permute -> moe_expert_ffn -> moe_combine with
- * accumulate = 1 (so h is rounded to dtype once per layer).
+ *   x_l = h                                    (pre_norm = 0)
+ *   x_l = h / sqrt(mean(h^2) + eps) * norm_l   (pre_norm = 1: RMS pre-norm, as
+ *         in the MoE blocks of the models of Table 1; fp32, rounded once)
+ *   h <- h + MoE_l(x_l),  l = 0..L-1,
+ * each block moe_route -> moe_permute -> moe_expert_ffn on x_l, then
+ * moe_combine with accumulate = 1 into h (h is rounded once per layer).
  *
  * h [n_tokens, H]   DEVICE, updated in place; the batch is rows token_ids[0..T)
  *                   (or rows 0..T when token_ids is NULL, then n_tokens == T)
@@ -206,7 +209,10 @@ int moe_kv_reindex(const int32_t* perm, int64_t N, const int32_t* batch_offsets,
  *                   router [E, H] and expert slots [S, F, H], [S, F, H], [S, H, F]
  * slot_of_expert    DEVICE int32 [L, E] (-1 = not resident: those choices are
  *                   skipped) or NULL (every expert resident, S == E)
- * h_trace           DEVICE [L, T, H] or NULL: the batch's state entering each layer
+ * norm_weight       HOST array of L DEVICE pointers to [H] (dtype), or NULL
+ *                   (unit weights); must be NULL when pre_norm = 0
+ * h_trace           DEVICE [L, 2, T, H] or NULL: per layer the batch's state and
+ *                   the block's input x_l
  * idx_trace         DEVICE int32 [L, T, k] or NULL: each layer's top-k experts
  * err               DEVICE int32, set to 1 on an out-of-range token id
  * Runs on `stream` with no host synchronisation; the workspace comes from
@@ -221,6 +227,7 @@ int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64_t H,
                       int64_t F, const void* const* w_router, const void* const* w_gate,
                       const void* const* w_up, const void* const* w_down,
                       const int32_t* slot_of_expert, int32_t S, int32_t renormalize,
+                      int32_t pre_norm, const void* const* norm_weight, float eps,
                       void* h_trace, int32_t* idx_trace, int32_t* err, void* workspace,
                       size_t ws_bytes, void* stream);
 

@@ -1,9 +1,11 @@
-// A batch through a stack of MoE layers (Sec. 2.1's transformer blocks with the
-// attention half left out): h <- h + MoE_l(h) for l = 0..L-1, each layer the
-// path route -> permute -> expert FFN -> combine, the residual added by the
-// combine's accumulate mode (one bf16 rounding of h per layer). The batch's
-// rows are gathered into a contiguous buffer once, run through every layer in
-// place, and scattered back, so the route step sees a dense [T, H] batch.
+// A batch through a stack of MoE blocks (Sec. 2.1's transformer blocks with the
+// attention half left out): h <- h + MoE_l(x_l) for l = 0..L-1, x_l = h or,
+// with pre_norm, the RMS-normalised h (the pre-norm of the MoE blocks of the
+// models the paper runs); each block the path route -> permute -> expert FFN
+// -> combine, the residual added by the combine's accumulate mode (one
+// rounding of h per layer). The batch's rows are gathered into a contiguous
+// buffer once, run through every layer in place, and scattered back, so the
+// route step sees a dense [T, H] batch.
 #include "moeflow.h"
 #include "common.h"
 
@@ -13,7 +15,7 @@ namespace moe {
 namespace {
 
 struct StackLayout {
-  size_t xb, idx, w, offs, rop, por, xp, yp, inc, pws, fws, total;
+  size_t xb, xn, idx, w, offs, rop, por, xp, yp, inc, pws, fws, total;
   size_t pws_bytes, fws_bytes;
 };
 
@@ -28,6 +30,7 @@ StackLayout stack_layout(int64_t T, int64_t H, int64_t F, int32_t E, int32_t k, 
     return at;
   };
   s.xb = take((size_t)T * H * elt);
+  s.xn = take((size_t)T * H * elt);
   s.idx = take((size_t)P * 4);
   s.w = take((size_t)P * 4);
   s.offs = take((size_t)(E + 1) * 4);
@@ -64,6 +67,42 @@ __global__ void stack_rows_kernel(const char* __restrict__ src, char* __restrict
   }
 }
 
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return bf16_to_f32(v); }
+template <typename Tv> __device__ __forceinline__ Tv from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) {
+  return f32_to_bf16(v);
+}
+
+// x = h / sqrt(mean(h^2) + eps) * weight, one block per row (fp32 sum of
+// squares, one rounding of each output).
+template <typename Tv>
+__global__ void __launch_bounds__(256)
+stack_rms_norm_kernel(const Tv* __restrict__ h, const Tv* __restrict__ weight, int64_t T,
+                      int64_t H, float eps, Tv* __restrict__ x) {
+  __shared__ float part[256 / kWave];
+  const int64_t t = blockIdx.x;
+  if (t >= T) return;
+  const Tv* row = h + t * H;
+  float ss = 0.f;
+  for (int64_t c = threadIdx.x; c < H; c += blockDim.x) {
+    const float v = to_f32(row[c]);
+    ss += v * v;
+  }
+  for (int o = kWave / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+  if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int q = 0; q < (int)(blockDim.x / kWave); ++q) tot += part[q];
+  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+  for (int64_t c = threadIdx.x; c < H; c += blockDim.x) {
+    float v = to_f32(row[c]) * inv;
+    if (weight) v *= to_f32(weight[c]);
+    x[t * H + c] = from_f32<Tv>(v);
+  }
+}
+
 __global__ void stack_copy_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
                                   int64_t n) {
   for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n;
@@ -86,7 +125,8 @@ extern "C" int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64
                                  int32_t k, int64_t F, const void* const* w_router,
                                  const void* const* w_gate, const void* const* w_up,
                                  const void* const* w_down, const int32_t* slot_of_expert,
-                                 int32_t S, int32_t renormalize, void* h_trace,
+                                 int32_t S, int32_t renormalize, int32_t pre_norm,
+                                 const void* const* norm_weight, float eps, void* h_trace,
                                  int32_t* idx_trace, int32_t* err, void* workspace,
                                  size_t ws_bytes, void* stream) {
   using namespace moe;
@@ -96,13 +136,16 @@ extern "C" int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64
   MOE_CHECK_ARG(E >= 1 && E <= 256 && k >= 1 && k <= E && S >= 1);
   MOE_CHECK_ARG(slot_of_expert || S == E);
   MOE_CHECK_ARG(renormalize == 0 || renormalize == 1);
+  MOE_CHECK_ARG((pre_norm == 0 && !norm_weight) || (pre_norm == 1 && eps >= 0.f));
   MOE_CHECK_ARG(token_ids || n_tokens == T);
   const size_t elt = dtype == MOE_BF16 ? 2 : 4;
   if ((H * (int64_t)elt) % 16 != 0 || (reinterpret_cast<uintptr_t>(h) & 15) ||
       (reinterpret_cast<uintptr_t>(h_trace) & 15))
     return MOE_ERR_UNSUPPORTED;                                  // 16-byte row copies
   for (int32_t l = 0; l < L; ++l)
-    MOE_CHECK_ARG(w_router[l] && w_gate[l] && w_up[l] && w_down[l]);
+    MOE_CHECK_ARG(w_router[l] && w_gate[l] && w_up[l] && w_down[l] &&
+                  (!norm_weight || norm_weight[l]));
+  if (T > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
   const StackLayout lay = stack_layout(T, H, F, E, k, dtype);
   if (!workspace || ws_bytes < lay.total || (reinterpret_cast<uintptr_t>(workspace) & 255))
     return MOE_ERR_WORKSPACE;
@@ -113,6 +156,7 @@ extern "C" int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64
   const unsigned grid = (unsigned)std::min<int64_t>(ceil_div(T * row_chunks, 256),
                                                     16 * (int64_t)device_cu_count());
   void* xb = token_ids ? static_cast<void*>(ws + lay.xb) : h;
+  void* const xn = ws + lay.xn;
   auto* idx = reinterpret_cast<int32_t*>(ws + lay.idx);
   auto* w = reinterpret_cast<float*>(ws + lay.w);
   auto* offs = reinterpret_cast<int32_t*>(ws + lay.offs);
@@ -130,19 +174,36 @@ extern "C" int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64
   }
   int rc = MOE_OK;
   for (int32_t l = 0; l < L && rc == MOE_OK; ++l) {
-    if (h_trace) {
+    const void* xin = xb;                          // the block's input
+    if (pre_norm) {
+      const void* wn = norm_weight ? norm_weight[l] : nullptr;
+      if (dtype == MOE_BF16)
+        stack_rms_norm_kernel<uint16_t><<<dim3((unsigned)T), dim3(256), 0, st>>>(
+            static_cast<const uint16_t*>(xb), static_cast<const uint16_t*>(wn), T, H, eps,
+            static_cast<uint16_t*>(xn));
+      else
+        stack_rms_norm_kernel<float><<<dim3((unsigned)T), dim3(256), 0, st>>>(
+            static_cast<const float*>(xb), static_cast<const float*>(wn), T, H, eps,
+            static_cast<float*>(xn));
+      MOE_CHECK_LAUNCH();
+      xin = xn;
+    }
+    if (h_trace) {                                 // [l][0] the state, [l][1] the block's input
+      char* const tr = static_cast<char*>(h_trace) + (size_t)l * 2 * T * H * elt;
       stack_copy_kernel<<<dim3(grid), dim3(256), 0, st>>>(
-          static_cast<const uint4*>(xb),
-          reinterpret_cast<uint4*>(static_cast<char*>(h_trace) + (size_t)l * T * H * elt),
+          static_cast<const uint4*>(xb), reinterpret_cast<uint4*>(tr), T * row_chunks);
+      MOE_CHECK_LAUNCH();
+      stack_copy_kernel<<<dim3(grid), dim3(256), 0, st>>>(
+          static_cast<const uint4*>(xin), reinterpret_cast<uint4*>(tr + (size_t)T * H * elt),
           T * row_chunks);
       MOE_CHECK_LAUNCH();
     }
     int32_t* const idx_l = idx_trace ? idx_trace + (int64_t)l * P : idx;
     const int32_t* const slot_l = slot_of_expert ? slot_of_expert + (int64_t)l * E : nullptr;
-    rc = moe_route(xb, w_router[l], dtype, T, H, E, k, nullptr, 0, renormalize, nullptr, idx_l,
+    rc = moe_route(xin, w_router[l], dtype, T, H, E, k, nullptr, 0, renormalize, nullptr, idx_l,
                    w, stream);
     if (rc != MOE_OK) break;
-    rc = moe_permute(xb, dtype, H, T, nullptr, T, idx_l, k, E, offs, rop, por, xp, ws + lay.pws,
+    rc = moe_permute(xin, dtype, H, T, nullptr, T, idx_l, k, E, offs, rop, por, xp, ws + lay.pws,
                      lay.pws_bytes, stream);
     if (rc != MOE_OK) break;
     rc = moe_expert_ffn(xp, dtype, P, H, F, offs, E, slot_l, S, w_gate[l], w_up[l], w_down[l], yp,

@@ -51,7 +51,7 @@ def load_library(path=None):
         "moe_kv_reindex": (I32, [P, I64, P, I32, P, P, P, P]),
         "moe_stack_workspace": (SZ, [I64, I64, I64, I32, I32, I32]),
         "moe_stack_forward": (I32, [P, I32, I64, I64, P, I64, I32, I32, I32, I64, P, P, P, P, P,
-                                    I32, I32, P, P, P, P, SZ, P]),
+                                    I32, I32, I32, P, ctypes.c_float, P, P, P, P, SZ, P]),
         "moe_schedule_multi_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "moe_schedule_multi": (I32, [P, I64, I32, I32, I32, I32, I32, I32, P, P, P, P, P, SZ,
                                      P]),
@@ -309,10 +309,12 @@ def stack_workspace(T, H, F, E, k, dtype_code=MOE_BF16):
 
 
 def stack_forward(h, layers, k, token_ids=None, slot_of_expert=None, S=None, renormalize=True,
-                  h_trace=None, idx_trace=None, err=None, workspace=None, stream=None):
+                  pre_norm=False, norm_weights=None, eps=1e-5, h_trace=None, idx_trace=None,
+                  err=None, workspace=None, stream=None):
     """moe_stack_forward: the batch (rows token_ids of h, or all rows) through
     the layers, h updated in place. layers: list of (w_router [E,H], w_gate
-    [S,F,H], w_up [S,F,H], w_down [S,H,F]) device tensors. Returns (h, err)."""
+    [S,F,H], w_up [S,F,H], w_down [S,H,F]) device tensors; norm_weights: list
+    of [H] tensors or None (unit weights, with pre_norm). Returns (h, err)."""
     torch = _torch()
     lib = load_library()
     _dev(h, token_ids, slot_of_expert, h_trace, idx_trace)
@@ -333,11 +335,20 @@ def stack_forward(h, layers, k, token_ids=None, slot_of_expert=None, S=None, ren
     if err is None:
         err = torch.zeros(1, dtype=torch.int32, device=h.device)
     arr = lambda j: (ctypes.c_void_p * L)(*[lay[j].data_ptr() for lay in layers])
+    nw = None
+    if norm_weights is not None:
+        if not pre_norm or len(norm_weights) != L:
+            raise ValueError("norm_weights needs pre_norm and one [H] tensor per layer")
+        _dev(*norm_weights)
+        if any(tuple(w_.shape) != (H,) or w_.dtype != h.dtype for w_ in norm_weights):
+            raise ValueError("norm weights must be [H] with the dtype of h")
+        nw = (ctypes.c_void_p * L)(*[w_.data_ptr() for w_ in norm_weights])
     ws, nbytes = _workspace(lib.moe_stack_workspace(T, H, F, E, k, dt), h.device, workspace)
     st = lib.moe_stack_forward(_ptr(h), dt, n_tokens, H, _ptr(token_ids), T, L, E, k, F, arr(0),
                                arr(1), arr(2), arr(3), _ptr(slot_of_expert), S,
-                               1 if renormalize else 0, _ptr(h_trace), _ptr(idx_trace), _ptr(err),
-                               _ptr(ws), nbytes, _stream(stream))
+                               1 if renormalize else 0, 1 if pre_norm else 0, nw, float(eps),
+                               _ptr(h_trace), _ptr(idx_trace), _ptr(err), _ptr(ws), nbytes,
+                               _stream(stream))
     _check("moe_stack_forward", st)
     return h, err
 

@@ -148,11 +148,16 @@ def test_kv_and_stack_reject_bad_arguments(lib):
     assert lib.moe_kv_reindex(FAKE, 10, FAKE, 2, S, S, FAKE, S) == ops.MOE_ERR_ARG
     w = (ctypes.c_void_p * 2)(0x1000, 0x1000)
     ws = lib.moe_stack_workspace(16, 64, 64, 8, 2, 1)
-    call = lambda T=16, n=16, E=8, k=2, S_=8, slot=S, tok=S, nbytes=ws, wr=w: lib.moe_stack_forward(
-        FAKE, 1, n, 64, tok, T, 2, E, k, 64, wr, w, w, w, slot, S_, 1, S, S, FAKE, FAKE, nbytes, S)
+    call = (lambda T=16, n=16, E=8, k=2, S_=8, slot=S, tok=S, nbytes=ws, wr=w, pre=0, nw=S,
+            eps=1e-5: lib.moe_stack_forward(FAKE, 1, n, 64, tok, T, 2, E, k, 64, wr, w, w, w, slot,
+                                            S_, 1, pre, nw, eps, S, S, FAKE, FAKE, nbytes, S))
     assert call(T=0) == ops.MOE_ERR_ARG
     assert call(n=20) == ops.MOE_ERR_ARG                  # n_tokens != T without token ids
     assert call(k=9) == ops.MOE_ERR_ARG
     assert call(S_=4) == ops.MOE_ERR_ARG                  # S < E needs a slot table
     assert call(wr=(ctypes.c_void_p * 2)(0x1000, 0)) == ops.MOE_ERR_ARG
     assert call(nbytes=ws - 1) == ops.MOE_ERR_WORKSPACE
+    assert call(pre=0, nw=w) == ops.MOE_ERR_ARG            # norm weights without the norm
+    assert call(pre=1, eps=-1.0) == ops.MOE_ERR_ARG
+    assert call(pre=2) == ops.MOE_ERR_ARG
+    assert call(pre=1, nw=(ctypes.c_void_p * 2)(0x1000, 0)) == ops.MOE_ERR_ARG

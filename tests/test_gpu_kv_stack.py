@@ -64,41 +64,56 @@ def _layers(L, E, H, F, seed, S=None):
     return out
 
 
-def _check_layers(h_in, h_out_rows, trace, idx_trace, layers, k, slots=None):
-    """Layer l from the GPU's own input trace[l]; the state after it is trace[l+1]
-    (or the final rows)."""
+def _check_layers(h_in, h_out_rows, trace, idx_trace, layers, k, slots=None, norms=None,
+                  pre_norm=False, eps=1e-5):
+    """Layer l from the GPU's own input trace[l][1] (its state trace[l][0]); the
+    state after it is trace[l+1][0] (or the final rows)."""
     L = len(layers)
     for l in range(L):
-        x = vals(trace[l])
+        state = vals(trace[l][0])
+        x = vals(trace[l][1])
+        if pre_norm:            # the norm, within one bf16 step of the float64 value
+            ref_x = oracle.rms_norm(state, None if norms is None else synth.values(norms[l]), eps)
+            assert (np.abs(x - ref_x) <= 2.0 ** -7 * np.abs(ref_x) + 1e-6).all(), f"norm {l}"
+        else:
+            assert np.array_equal(x, state)
         wr, wg, wu, wd = (synth.values(a) for a in layers[l])
         ref = oracle.moe_layer(x, wr, k, wg, wu, wd,
                                slot_of_expert=None if slots is None else slots[l])
         assert np.array_equal(idx_trace[l], ref["idx"]), f"layer {l}: top-k"
-        nxt = vals(trace[l + 1]) if l + 1 < L else h_out_rows
-        want = x + ref["y"]
+        nxt = vals(trace[l + 1][0]) if l + 1 < L else h_out_rows
+        want = state + ref["y"]
         tol = 1e-2 * np.abs(ref["y"]).max() + 2.0 ** -8 * np.abs(want)
         assert (np.abs(nxt - want) <= tol).all(), f"layer {l}: state"
-    assert np.array_equal(vals(trace[0]), h_in)
+    assert np.array_equal(vals(trace[0][0]), h_in)
 
 
-@pytest.mark.parametrize("T,n", [(300, 300), (257, 611), (20, 64)])
-def test_stack_layer_by_layer(T, n):
+@pytest.mark.parametrize("T,n,pre_norm,with_w", [(300, 300, False, False),
+                                                 (257, 611, True, True),
+                                                 (20, 64, True, False),
+                                                 (129, 129, True, True)])
+def test_stack_layer_by_layer(T, n, pre_norm, with_w):
     L, E, H, F, k = 3, 8, 256, 512, 2
     lay = _layers(L, E, H, F, seed=T)
     g = np.random.default_rng(n)
-    h0 = synth.bf16_bits(g.standard_normal((n, H)).astype(np.float32))
+    h0 = synth.bf16_bits(g.standard_normal((n, H)).astype(np.float32) * np.float32(3))
     h = to_dev(h0)
     tok = None if T == n else np.sort(g.choice(n, size=T, replace=False)).astype(np.int32)
-    trace = torch.empty((L, T, H), dtype=torch.bfloat16, device="cuda:0")
+    norms = ([synth.bf16_bits((1 + 0.2 * g.standard_normal(H)).astype(np.float32))
+              for _ in range(L)] if with_w else None)
+    trace = torch.empty((L, 2, T, H), dtype=torch.bfloat16, device="cuda:0")
     itr = torch.empty((L, T, k), dtype=torch.int32, device="cuda:0")
     _, err = ops.stack_forward(h, [tuple(to_dev(a) for a in l_) for l_ in lay], k,
                                token_ids=None if tok is None else to_dev(tok),
+                               pre_norm=pre_norm,
+                               norm_weights=None if norms is None else [to_dev(w) for w in norms],
                                h_trace=trace, idx_trace=itr)
     torch.cuda.synchronize()
     assert to_host(err)[0] == 0
     rows = np.arange(n) if tok is None else tok
     hv = vals(h)
-    _check_layers(synth.values(h0)[rows], hv[rows], trace, to_host(itr), lay, k)
+    _check_layers(synth.values(h0)[rows], hv[rows], trace, to_host(itr), lay, k, norms=norms,
+                  pre_norm=pre_norm)
     rest = np.setdiff1d(np.arange(n), rows)
     assert np.array_equal(to_host(h)[rest], h0[rest])       # other rows untouched
 
@@ -112,7 +127,7 @@ def test_stack_with_a_resident_subset_per_layer():
     g = np.random.default_rng(10)
     h0 = synth.bf16_bits(g.standard_normal((T, H)).astype(np.float32))
     h = to_dev(h0)
-    trace = torch.empty((L, T, H), dtype=torch.bfloat16, device="cuda:0")
+    trace = torch.empty((L, 2, T, H), dtype=torch.bfloat16, device="cuda:0")
     itr = torch.empty((L, T, k), dtype=torch.int32, device="cuda:0")
     ops.stack_forward(h, [tuple(to_dev(a) for a in l_) for l_ in lay], k,
                       slot_of_expert=to_dev(slots), S=S, h_trace=trace, idx_trace=itr)
@@ -121,9 +136,9 @@ def test_stack_with_a_resident_subset_per_layer():
 
 
 def test_stack_full_shape_two_layers_sampled():
-    """Mixtral-shaped layers (H 4096, 8 experts of F 14336, top-2) over a
-    4096-token batch of an 8192-token unit; the oracle checks the first and
-    last row of every expert group and a seeded sample, layer by layer."""
+    """Mixtral-shaped pre-normalised blocks (H 4096, 8 experts of F 14336,
+    top-2) over a 4096-token batch of an 8192-token unit; the oracle checks a
+    seeded sample of tokens, layer by layer."""
     cfg = synth.config(2)
     E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
     L, n, T = 2, 8192, 4096
@@ -138,20 +153,23 @@ def test_stack_full_shape_two_layers_sampled():
     h = torch.randn((n, H), device=dev, generator=g).to(torch.bfloat16)
     h0 = to_host(h).copy()
     tok = torch.arange(1, n, 2, dtype=torch.int32, device=dev)          # the odd tokens
-    trace = torch.empty((L, T, H), dtype=torch.bfloat16, device=dev)
+    trace = torch.empty((L, 2, T, H), dtype=torch.bfloat16, device=dev)
     itr = torch.empty((L, T, k), dtype=torch.int32, device=dev)
-    ops.stack_forward(h, lay, k, token_ids=tok, h_trace=trace, idx_trace=itr)
+    ops.stack_forward(h, lay, k, token_ids=tok, pre_norm=True, h_trace=trace, idx_trace=itr)
     torch.cuda.synchronize()
     hv = vals(h)
     it = to_host(itr)
     sample = np.sort(np.random.default_rng(12).choice(T, size=20, replace=False))
     for l in range(L):
-        x = vals(trace[l])[sample]
+        state = vals(trace[l][0])[sample]
+        x = vals(trace[l][1])[sample]
+        ref_x = oracle.rms_norm(state)
+        assert (np.abs(x - ref_x) <= 2.0 ** -7 * np.abs(ref_x) + 1e-6).all()
         wr, wg, wu, wd = (synth.values(to_host(a)) for a in lay[l])
         ref = oracle.moe_layer(x, wr, k, wg, wu, wd)
         assert np.array_equal(it[l][sample], ref["idx"])
-        nxt = vals(trace[l + 1])[sample] if l + 1 < L else hv[1::2][sample]
-        want = x + ref["y"]
+        nxt = vals(trace[l + 1][0])[sample] if l + 1 < L else hv[1::2][sample]
+        want = state + ref["y"]
         tol = 1e-2 * np.abs(ref["y"]).max() + 2.0 ** -8 * np.abs(want)
         assert (np.abs(nxt - want) <= tol).all()
     assert np.array_equal(to_host(h)[0::2], h0[0::2])

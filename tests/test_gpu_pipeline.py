@@ -1,0 +1,79 @@
+"""The dual-batch pipeline (Sec. 3.3.4): with the next unit's scheduling on a
+second stream the results are bit-identical to running everything in order,
+each unit's new batches are the two-way schedule of its predicted routes, its
+KV caches are merged and reindexed like the oracle's, and its hidden states
+are what the layer stack gives for each new batch."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2410_17954_amd import ops, pipeline, synth
+from gpu_helpers import to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+def _setup(n_units=3, N=256, H=256, F=512, E=8, k=2, L=2, seed=0):
+    g = np.random.default_rng(seed)
+    layers = []
+    for l in range(L):
+        layers.append(tuple(to_dev(synth.bf16_bits(g.standard_normal(s).astype(np.float32)
+                                                   * np.float32(sc)))
+                            for s, sc in (((E, H), 0.05), ((E, F, H), 0.03), ((E, F, H), 0.03),
+                                          ((E, H, F), 0.03))))
+    units = []
+    for u in range(n_units):
+        h = synth.bf16_bits(g.standard_normal((N, H)).astype(np.float32))
+        routes = synth.predicted_routes(N, L, E, k, 0.7, 1.1, seed=100 + u)
+        kv = [g.integers(0, 256, size=(L, N // 2, 512), dtype=np.uint8) for _ in range(2)]
+        units.append((h, routes, kv))
+    return layers, units, (N, E, k)
+
+
+def _dev_units(units):
+    return [pipeline.Unit(h=to_dev(h), routes=to_dev(r), kv=[to_dev(c) for c in kv])
+            for h, r, kv in units]
+
+
+def test_overlapped_equals_in_order_and_the_parts():
+    layers, units, (N, E, k) = _setup()
+    res = {}
+    for overlap in (True, False):
+        us = _dev_units(units)
+        pl = pipeline.DualBatchPipeline(layers, k, E, N, overlap=overlap)
+        plans = pl.run(us)
+        torch.cuda.synchronize()
+        res[overlap] = ([to_host(u.h) for u in us], plans)
+    for a, b in zip(res[True][0], res[False][0]):
+        assert np.array_equal(a, b)
+    for pa, pb in zip(res[True][1], res[False][1]):
+        assert np.array_equal(to_host(pa.perm), to_host(pb.perm))
+        assert np.array_equal(to_host(pa.kv_new), to_host(pb.kv_new))
+    for (h0, routes, kv), hs, plan in zip(units, res[True][0], res[True][1]):
+        # the new batches: the two-way token scheduler on the predicted routes
+        rp, rd, _ = oracle.schedule(routes, E, N // 2)
+        assert np.array_equal(to_host(plan.perm), rp)
+        assert np.array_equal(to_host(plan.demand), rd)
+        # KV: merged in global order, then gathered into the new layout
+        assert np.array_equal(to_host(plan.kv_new), oracle.kv_gather(oracle.kv_merge(kv), rp))
+        b_of, p_of = oracle.kv_reindex(rp, [0, N // 2, N])
+        assert np.array_equal(to_host(plan.batch_of), b_of)
+        assert np.array_equal(to_host(plan.pos_of), p_of)
+        assert to_host(plan.err)[0] == 0
+        # hidden states: each new batch through the stack, called directly
+        h = to_dev(h0)
+        for lo, hi in ((0, N // 2), (N // 2, N)):
+            ops.stack_forward(h, layers, k, token_ids=to_dev(rp[lo:hi].astype(np.int32)),
+                              pre_norm=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(h), hs)
+
+
+def test_single_unit_and_no_kv():
+    layers, units, (N, E, k) = _setup(n_units=1, seed=3)
+    us = [pipeline.Unit(h=to_dev(h), routes=to_dev(r)) for h, r, _ in units]
+    plans = pipeline.DualBatchPipeline(layers, k, E, N).run(us)
+    torch.cuda.synchronize()
+    assert plans[0].kv_new is None
+    assert sorted(to_host(plans[0].perm).tolist()) == list(range(N))
