@@ -1382,6 +1382,25 @@ std::vector<MultiNode> multi_nodes(int64_t N, int32_t B) {
   return out;
 }
 
+// Batch boundaries on the host (the device kernel below computes the same).
+std::vector<int64_t> multi_offsets_host(int64_t N, int32_t B) {
+  std::vector<int64_t> off{0};
+  std::vector<std::pair<int64_t, int32_t>> stack{{N, B}};
+  while (!stack.empty()) {
+    const auto v = stack.back();
+    stack.pop_back();
+    if (v.second == 1) {
+      off.push_back(off.back() + v.first);
+      continue;
+    }
+    const int32_t bl = v.second / 2;
+    const int64_t n1 = v.first * bl / v.second;
+    stack.push_back({v.first - n1, v.second - bl});
+    stack.push_back({n1, bl});
+  }
+  return off;
+}
+
 struct MultiLayout {
   size_t sub, routes, tmp, sub_perm, info, total;
 };
@@ -1468,28 +1487,33 @@ __global__ void sch_multi_zero(int64_t n, int32_t* __restrict__ p) {
   if (i < n) p[i] = 0;
 }
 
-// demand[b, l, e] = tokens of batch b whose route uses (l, e); one block per
-// batch, counts in LDS when L*E fits (else straight to memory, zeroed first).
-// A token repeating an expert within a layer counts once.
+// demand[b, l, e] = tokens of batch b whose route uses (l, e). Block (c, b)
+// counts kDemandChunk tokens of batch b into an LDS histogram when L*E fits
+// (else straight into memory), then adds it to demand (zeroed first): many
+// blocks per batch keep the LDS atomics on the few (l, e) cells of small E
+// from serialising. A token repeating an expert within a layer counts once.
 constexpr int kDemandLdsWords = 16384;
+constexpr int kDemandChunk = 256;
 template <bool LDS>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(256)
 sch_multi_demand(const uint8_t* __restrict__ routes, const int32_t* __restrict__ perm,
                  const int32_t* __restrict__ offsets, int32_t L, int32_t E, int32_t k,
                  int32_t* __restrict__ demand) {
   __shared__ int32_t h[LDS ? kDemandLdsWords : 1];
-  const int b = blockIdx.x;
+  const int b = blockIdx.y;
   const int64_t LE = (int64_t)L * E;
   int32_t* const out = demand + (int64_t)b * LE;
+  const int64_t lo = offsets[b] + (int64_t)blockIdx.x * kDemandChunk;
+  const int64_t hi = min((int64_t)offsets[b + 1], lo + kDemandChunk);
+  if (lo >= hi) return;                                // uniform over the block
   if (LDS) {
     for (int64_t q = threadIdx.x; q < LE; q += blockDim.x) h[q] = 0;
     __syncthreads();
   }
-  const int64_t lo = offsets[b], hi = offsets[b + 1];
   const int64_t total = (hi - lo) * L;
   for (int64_t q = threadIdx.x; q < total; q += blockDim.x) {
-    const int64_t p = lo + q / L;
-    const int l = (int)(q % L);
+    const int64_t p = lo + q % (hi - lo);              // neighbouring threads: neighbouring tokens
+    const int l = (int)(q / (hi - lo));
     const uint8_t* r = routes + ((int64_t)perm[p] * L + l) * k;
     for (int j = 0; j < k; ++j) {
       bool seen = false;
@@ -1502,7 +1526,8 @@ sch_multi_demand(const uint8_t* __restrict__ routes, const int32_t* __restrict__
   }
   if (LDS) {
     __syncthreads();
-    for (int64_t q = threadIdx.x; q < LE; q += blockDim.x) out[q] = h[q];
+    for (int64_t q = threadIdx.x; q < LE; q += blockDim.x)
+      if (h[q]) atomicAdd(&out[q], h[q]);
   }
 }
 
@@ -1575,17 +1600,21 @@ extern "C" int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, i
   MOE_CHECK_LAUNCH();
   if (demand) {
     const int64_t LE = (int64_t)L * E;
-    if (LE <= kDemandLdsWords) {
-      sch_multi_demand<true><<<dim3(B), dim3(1024), 0, st>>>(routes, perm, batch_offsets, L, E, k,
-                                                              demand);
-    } else {
-      const int64_t cells = (int64_t)B * LE;
-      if (ceil_div(cells, 256) > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
-      sch_multi_zero<<<dim3((unsigned)ceil_div(cells, 256)), dim3(256), 0, st>>>(cells, demand);
-      MOE_CHECK_LAUNCH();
-      sch_multi_demand<false><<<dim3(B), dim3(1024), 0, st>>>(routes, perm, batch_offsets, L, E,
-                                                               k, demand);
-    }
+    const int64_t cells = (int64_t)B * LE;
+    if (ceil_div(cells, 256) > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
+    sch_multi_zero<<<dim3((unsigned)ceil_div(cells, 256)), dim3(256), 0, st>>>(cells, demand);
+    MOE_CHECK_LAUNCH();
+    // chunks of the largest batch (sizes depend on N and B only)
+    const std::vector<int64_t> off = multi_offsets_host(N, B);
+    int64_t largest = 0;
+    for (int32_t j = 0; j < B; ++j) largest = std::max(largest, off[j + 1] - off[j]);
+    const dim3 g((unsigned)std::max<int64_t>(1, ceil_div(largest, kDemandChunk)), (unsigned)B);
+    if (LE <= kDemandLdsWords)
+      sch_multi_demand<true><<<g, dim3(256), 0, st>>>(routes, perm, batch_offsets, L, E, k,
+                                                       demand);
+    else
+      sch_multi_demand<false><<<g, dim3(256), 0, st>>>(routes, perm, batch_offsets, L, E, k,
+                                                        demand);
     MOE_CHECK_LAUNCH();
   }
   return MOE_OK;

@@ -76,8 +76,9 @@ template <> __device__ __forceinline__ uint16_t from_f32<uint16_t>(float v) {
 }
 
 // x = h / sqrt(mean(h^2) + eps) * weight, one block per row (fp32 sum of
-// squares, one rounding of each output).
-template <typename Tv>
+// squares, one rounding of each output). VEC: bf16 rows read and written 8
+// values (16 bytes) at a time.
+template <typename Tv, bool VEC>
 __global__ void __launch_bounds__(256)
 stack_rms_norm_kernel(const Tv* __restrict__ h, const Tv* __restrict__ weight, int64_t T,
                       int64_t H, float eps, Tv* __restrict__ x) {
@@ -86,9 +87,23 @@ stack_rms_norm_kernel(const Tv* __restrict__ h, const Tv* __restrict__ weight, i
   if (t >= T) return;
   const Tv* row = h + t * H;
   float ss = 0.f;
-  for (int64_t c = threadIdx.x; c < H; c += blockDim.x) {
-    const float v = to_f32(row[c]);
-    ss += v * v;
+  if constexpr (VEC) {
+    const uint4* r4 = reinterpret_cast<const uint4*>(row);
+    for (int64_t c = threadIdx.x; c < H / 8; c += blockDim.x) {
+      const uint4 u = r4[c];
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float a = bf16_to_f32((uint16_t)(w[j] & 0xffff)), b = bf16_to_f32((uint16_t)(w[j] >> 16));
+        ss += a * a;
+        ss += b * b;
+      }
+    }
+  } else {
+    for (int64_t c = threadIdx.x; c < H; c += blockDim.x) {
+      const float v = to_f32(row[c]);
+      ss += v * v;
+    }
   }
   for (int o = kWave / 2; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
   if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = ss;
@@ -96,10 +111,33 @@ stack_rms_norm_kernel(const Tv* __restrict__ h, const Tv* __restrict__ weight, i
   float tot = 0.f;
   for (int q = 0; q < (int)(blockDim.x / kWave); ++q) tot += part[q];
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
-  for (int64_t c = threadIdx.x; c < H; c += blockDim.x) {
-    float v = to_f32(row[c]) * inv;
-    if (weight) v *= to_f32(weight[c]);
-    x[t * H + c] = from_f32<Tv>(v);
+  if constexpr (VEC) {
+    const uint4* r4 = reinterpret_cast<const uint4*>(row);
+    const uint4* w4 = reinterpret_cast<const uint4*>(weight);
+    uint4* x4 = reinterpret_cast<uint4*>(x + t * H);
+    for (int64_t c = threadIdx.x; c < H / 8; c += blockDim.x) {
+      const uint4 u = r4[c];
+      const uint4 g = weight ? w4[c] : make_uint4(0, 0, 0, 0);
+      const uint32_t in[4] = {u.x, u.y, u.z, u.w}, gw[4] = {g.x, g.y, g.z, g.w};
+      uint32_t o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float a = bf16_to_f32((uint16_t)(in[j] & 0xffff)) * inv;
+        float b = bf16_to_f32((uint16_t)(in[j] >> 16)) * inv;
+        if (weight) {
+          a *= bf16_to_f32((uint16_t)(gw[j] & 0xffff));
+          b *= bf16_to_f32((uint16_t)(gw[j] >> 16));
+        }
+        o[j] = (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+      }
+      x4[c] = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  } else {
+    for (int64_t c = threadIdx.x; c < H; c += blockDim.x) {
+      float v = to_f32(row[c]) * inv;
+      if (weight) v *= to_f32(weight[c]);
+      x[t * H + c] = from_f32<Tv>(v);
+    }
   }
 }
 
@@ -177,12 +215,18 @@ extern "C" int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64
     const void* xin = xb;                          // the block's input
     if (pre_norm) {
       const void* wn = norm_weight ? norm_weight[l] : nullptr;
-      if (dtype == MOE_BF16)
-        stack_rms_norm_kernel<uint16_t><<<dim3((unsigned)T), dim3(256), 0, st>>>(
+      // rows are 16-byte aligned (H * 2 a multiple of 16); the weight vector may not be
+      const bool vec = dtype == MOE_BF16 && (reinterpret_cast<uintptr_t>(wn) & 15) == 0;
+      if (vec)
+        stack_rms_norm_kernel<uint16_t, true><<<dim3((unsigned)T), dim3(256), 0, st>>>(
+            static_cast<const uint16_t*>(xb), static_cast<const uint16_t*>(wn), T, H, eps,
+            static_cast<uint16_t*>(xn));
+      else if (dtype == MOE_BF16)
+        stack_rms_norm_kernel<uint16_t, false><<<dim3((unsigned)T), dim3(256), 0, st>>>(
             static_cast<const uint16_t*>(xb), static_cast<const uint16_t*>(wn), T, H, eps,
             static_cast<uint16_t*>(xn));
       else
-        stack_rms_norm_kernel<float><<<dim3((unsigned)T), dim3(256), 0, st>>>(
+        stack_rms_norm_kernel<float, false><<<dim3((unsigned)T), dim3(256), 0, st>>>(
             static_cast<const float*>(xb), static_cast<const float*>(wn), T, H, eps,
             static_cast<float*>(xn));
       MOE_CHECK_LAUNCH();
