@@ -27,6 +27,7 @@ Modules and the passages they follow:
   layer     -- the composed MoE layer, the dense-FFN identity used as a pin, and
                a residual stack of pre-normalised layers
   kv        -- KV-cache Merge and Reindex of Sec. 3.3.3
+  rpp       -- forward pass of the routing path predictor of Sec. 3.2
 """
 from .gating import router_logits, topk_select, softmax, gate_weights, route
 from .permute import permute
@@ -39,6 +40,7 @@ from .slots import plan_slots
 from .cache import plec_order, plec_run, lru_run
 from .layer import moe_layer, dense_ffn, moe_stack, round_bf16, rms_norm
 from .kv import kv_merge, kv_gather, kv_reindex
+from . import rpp
 
 __all__ = [
     "router_logits", "topk_select", "softmax", "gate_weights", "route",
@@ -48,5 +50,5 @@ __all__ = [
     "schedule_multi", "plan_slots",
     "plec_order", "plec_run", "lru_run",
     "moe_layer", "dense_ffn", "moe_stack", "round_bf16", "rms_norm",
-    "kv_merge", "kv_gather", "kv_reindex",
+    "kv_merge", "kv_gather", "kv_reindex", "rpp",
 ]
