@@ -58,6 +58,10 @@ def parse():
                         "and reindexed) with and without the scheduling stream overlapped")
     p.add_argument("--stack-layers", type=int, default=32)
     p.add_argument("--stack-units", type=int, default=3)
+    p.add_argument("--rpp", action="store_true",
+                   help="instead of the layer throughput, time the routing path predictor's "
+                        "forward pass (16 sequences of 512 tokens, hidden 32, FFN 2048, random "
+                        "weights) with Mixtral-shaped and Qwen-shaped heads")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 counter_collection.csv files (FETCH_SIZE, "
                         "WRITE_SIZE) of a --copy-probe-mib run into the traffic file, then exit")
@@ -450,6 +454,61 @@ def stack_report(args):
     print(json.dumps(rec))
 
 
+def rpp_flops(dims, B, S):
+    """Algorithmic flops of one forward: every multiply-add counted as 2."""
+    d, dff, LE = dims["d_model"], dims["d_ff"], dims["L"] * dims["E"]
+    M = B * S
+    enc = dims["n_enc"] * M * (2 * d * 3 * d + 2 * d * d + 4 * d * dff + 4 * S * d)
+    causal_keys = (S + 1) / 2                      # mean keys per query under the causal mask
+    dec = dims["n_dec"] * M * (2 * d * 3 * d + 2 * d * d + 4 * causal_keys * d
+                               + 2 * d * d + 4 * d * d + 2 * d * d + 4 * S * d + 4 * d * dff)
+    return enc + dec + 2 * M * d * LE
+
+
+def rpp_report(args):
+    """Routing path predictor forward (one JSON line): tokens/s and float32
+    TFLOP/s, HIP events around one call, median of 7."""
+    import torch
+    from paper_2410_17954_amd import ops
+
+    dev = torch.device("cuda:0")
+    B, S = 16, 512
+    out = []
+    for name, L, E in (("Mixtral-8x7B heads", 32, 8), ("Qwen1.5-MoE heads", 24, 60)):
+        dims = dict(vocab=32000, d_model=32, n_heads=4, d_ff=2048, n_enc=3, n_dec=3, L=L, E=E,
+                    num_buckets=32, max_distance=128, eps=1e-6)
+        g = torch.Generator(device=dev)
+        g.manual_seed(args.seed)
+        w = torch.randn(ops.rpp_weights_count(dims), generator=g, device=dev) * 0.1
+        ids = torch.randint(0, 32000, (B, S), generator=g, device=dev, dtype=torch.int32)
+        ws = ops.workspace_tensor(ops.load_library().moe_rpp_workspace(
+            B, S, ops.ctypes.byref(ops.rpp_dims(dims))), dev)
+        probs = torch.empty((B, S, L, E), dtype=torch.float32, device=dev)
+        err = torch.zeros(1, dtype=torch.int32, device=dev)
+        ts = []
+        for rep in range(args.warmup + 7):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(1000000)
+            e0.record()
+            ops.rpp_forward(ids, w, dims, probs=probs, err=err, workspace=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            if rep >= args.warmup:
+                ts.append(e0.elapsed_time(e1))
+        ms = float(np.median(ts))
+        fl = rpp_flops(dims, B, S)
+        out.append({"heads": name, "L": L, "E": E, "ms": round(ms, 4),
+                    "tokens_per_s": round(B * S / (ms * 1e-3), 1),
+                    "gflop": round(fl / 1e9, 2), "tflops_fp32": round(fl / (ms * 1e-3) / 1e12, 2),
+                    "frac_of_fp32_peak": round(fl / (ms * 1e-3) / 1e12 / 157.3, 3),
+                    "weights_MB_fp32": round(ops.rpp_weights_count(dims) * 4 / 1e6, 2)})
+    rec = {"metric": "routing path predictor forward: tokens/s and float32 TFLOP/s",
+           "config": {"workload": f"T5-style predictor, 3+3 layers, hidden 32, 4 heads, FFN 2048, "
+                                  f"vocab 32000, {B} sequences x {S} tokens, random weights"},
+           "steps": out, "data": "synthetic"}
+    print(json.dumps(rec))
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -474,6 +533,9 @@ def main():
         return
     if args.stack:
         stack_report(args)
+        return
+    if args.rpp:
+        rpp_report(args)
         return
     import torch
     from paper_2410_17954_amd import ops, synth

@@ -14,6 +14,7 @@
  *   moe_kv_gather   KV-cache Merge / Reindex row movement       (Sec. 3.3.3)
  *   moe_kv_reindex  new batch and position of every token       (Sec. 3.3.3)
  *   moe_stack_forward   a batch through L residual MoE layers   (Sec. 2.1)
+ *   moe_rpp_forward routing path predictor forward pass         (Sec. 3.2)
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -230,6 +231,42 @@ int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64_t H,
                       int32_t pre_norm, const void* const* norm_weight, float eps,
                       void* h_trace, int32_t* idx_trace, int32_t* err, void* workspace,
                       size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_rpp_forward -- forward pass of the routing path predictor (Sec. 3.2): a
+ * T5-style encoder-decoder over B sequences of S token ids whose L heads give
+ * every token logits over the E experts of each MoE layer;
+ * probs = sigmoid(logits), laid out [B, S, L, E].
+ *   encoder   x = emb[ids]; per layer x += Attn(rms(x)) (bidirectional, T5
+ *             relative-position bias), x += W2 relu(W1 rms(x)); enc = rms(x)
+ *   decoder   y = emb[ids]; per layer y += Attn(rms(y)) (causal, its own
+ *             bias), y += CrossAttn(rms(y), enc), y += W2 relu(W1 rms(y));
+ *             logits = rms(y) . heads^T
+ *   rms(v) = v / sqrt(mean(v^2) + eps) * scale; attention without the
+ *   1/sqrt(d_kv) factor; relative buckets as T5's (num_buckets, max_distance
+ *   powers of two), the logarithmic ones evaluated exactly.
+ * weights  DEVICE float32, moe_rpp_weights_count(dims) values in this order
+ *          (linear layers [out, in]): emb [V,d]; enc_rel [nb,h]; per encoder
+ *          layer ln1 [d], q, k, v, o [d,d], ln2 [d], wi [dff,d], wo [d,dff];
+ *          enc_ln [d]; dec_rel [nb,h]; per decoder layer ln1 [d], q, k, v, o,
+ *          ln2 [d], cq, ck, cv, co [d,d], ln3 [d], wi [dff,d], wo [d,dff];
+ *          dec_ln [d]; heads [L*E, d]
+ * ids      DEVICE int32 [B, S]; an id outside 0..vocab-1 sets *err (DEVICE
+ *          int32, cleared by the caller) and embeds as zeros
+ * probs    DEVICE float32 [B, S, L, E]; logits the same or NULL
+ * Limits: d_model % n_heads == 0 with d_kv in {4, 8, 16, 32, 64};
+ *   2*S*d_kv*4 <= 64 KiB; num_buckets even; the bucket sizes powers of two.
+ * Errors: MOE_ERR_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE.
+ * ---------------------------------------------------------------------- */
+typedef struct moe_rpp_dims {
+  int32_t vocab, d_model, n_heads, d_ff, n_enc, n_dec, L, E, num_buckets, max_distance;
+  float eps;
+} moe_rpp_dims;
+size_t moe_rpp_weights_count(const moe_rpp_dims* dims);
+size_t moe_rpp_workspace(int32_t B, int32_t S, const moe_rpp_dims* dims);
+int moe_rpp_forward(const int32_t* ids, int32_t B, int32_t S, const moe_rpp_dims* dims,
+                    const float* weights, float* probs, float* logits, int32_t* err,
+                    void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * moe_permute -- group the (token, choice) pairs of one batch by expert so

@@ -52,6 +52,9 @@ def load_library(path=None):
         "moe_stack_workspace": (SZ, [I64, I64, I64, I32, I32, I32]),
         "moe_stack_forward": (I32, [P, I32, I64, I64, P, I64, I32, I32, I32, I64, P, P, P, P, P,
                                     I32, I32, I32, P, ctypes.c_float, P, P, P, P, SZ, P]),
+        "moe_rpp_weights_count": (SZ, [P]),
+        "moe_rpp_workspace": (SZ, [I32, I32, P]),
+        "moe_rpp_forward": (I32, [P, I32, I32, P, P, P, P, P, P, SZ, P]),
         "moe_schedule_multi_workspace": (SZ, [I64, I32, I32, I32, I32]),
         "moe_schedule_multi": (I32, [P, I64, I32, I32, I32, I32, I32, I32, P, P, P, P, P, SZ,
                                      P]),
@@ -79,7 +82,8 @@ def exported_symbols():
             "moe_schedule", "moe_schedule_multi_workspace", "moe_schedule_multi",
             "moe_permute_workspace", "moe_permute",
             "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_kv_gather",
-            "moe_kv_reindex", "moe_stack_workspace", "moe_stack_forward", "moe_plec_order",
+            "moe_kv_reindex", "moe_stack_workspace", "moe_stack_forward",
+            "moe_rpp_weights_count", "moe_rpp_workspace", "moe_rpp_forward", "moe_plec_order",
             "moe_plec_run", "moe_lru_run", "moe_load_experts"]
 
 
@@ -301,6 +305,50 @@ def kv_reindex(perm, batch_offsets, batch_of=None, pos_of=None, err=None, stream
                             _ptr(err), _stream(stream))
     _check("moe_kv_reindex", st)
     return batch_of, pos_of, err
+
+
+# ------------------------------------------------------------------------- RPP
+class RppDims(ctypes.Structure):
+    """moe_rpp_dims."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("vocab", "d_model", "n_heads", "d_ff", "n_enc",
+                                               "n_dec", "L", "E", "num_buckets",
+                                               "max_distance")] + [("eps", ctypes.c_float)]
+
+
+def rpp_dims(dims):
+    return RppDims(**{k: dims[k] for k in (n for n, _ in RppDims._fields_)})
+
+
+def rpp_weights_count(dims):
+    return load_library().moe_rpp_weights_count(ctypes.byref(rpp_dims(dims)))
+
+
+def rpp_forward(ids, weights, dims, probs=None, logits=None, err=None, workspace=None,
+                want_logits=False, stream=None):
+    """moe_rpp_forward. ids int32 [B, S]; weights float32 [n] (packed); dims a
+    dict of moe_rpp_dims fields. Returns (probs [B, S, L, E], logits or None, err)."""
+    torch = _torch()
+    lib = load_library()
+    _dev(ids, weights)
+    if ids.dtype != torch.int32 or ids.dim() != 2 or weights.dtype != torch.float32:
+        raise TypeError("ids int32 [B, S] and float32 weights")
+    B, S = ids.shape
+    g = rpp_dims(dims)
+    if weights.numel() != lib.moe_rpp_weights_count(ctypes.byref(g)):
+        raise ValueError("weights do not match the dimensions")
+    dev = ids.device
+    shape = (B, S, dims["L"], dims["E"])
+    if probs is None:
+        probs = torch.empty(shape, dtype=torch.float32, device=dev)
+    if logits is None and want_logits:
+        logits = torch.empty(shape, dtype=torch.float32, device=dev)
+    if err is None:
+        err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws, nbytes = _workspace(lib.moe_rpp_workspace(B, S, ctypes.byref(g)), dev, workspace)
+    st = lib.moe_rpp_forward(_ptr(ids), B, S, ctypes.byref(g), _ptr(weights), _ptr(probs),
+                             _ptr(logits), _ptr(err), _ptr(ws), nbytes, _stream(stream))
+    _check("moe_rpp_forward", st)
+    return probs, logits, err
 
 
 # ----------------------------------------------------------------------- stack

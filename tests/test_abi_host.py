@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 20, names
+    assert len(names) == 23, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
@@ -161,3 +161,25 @@ def test_kv_and_stack_reject_bad_arguments(lib):
     assert call(pre=1, eps=-1.0) == ops.MOE_ERR_ARG
     assert call(pre=2) == ops.MOE_ERR_ARG
     assert call(pre=1, nw=(ctypes.c_void_p * 2)(0x1000, 0)) == ops.MOE_ERR_ARG
+
+
+def test_rpp_weight_count_and_bad_arguments(lib):
+    dims = dict(vocab=32000, d_model=32, n_heads=4, d_ff=2048, n_enc=3, n_dec=3, L=32, E=8,
+                num_buckets=32, max_distance=128, eps=1e-6)
+    g = ops.rpp_dims(dims)
+    # the library's own count of the packed layout (7.43 MB in float32)
+    assert lib.moe_rpp_weights_count(ctypes.byref(g)) == 1856288
+    assert lib.moe_rpp_workspace(16, 512, ctypes.byref(g)) > 16 * 512 * 2048 * 4
+    S = None
+    ws = lib.moe_rpp_workspace(2, 8, ctypes.byref(g))
+    call = lambda B=2, S_=8, gg=g, nbytes=ws: lib.moe_rpp_forward(
+        FAKE, B, S_, ctypes.byref(gg), FAKE, FAKE, S, FAKE, FAKE, nbytes, S)
+    assert call(B=0) == ops.MOE_ERR_ARG
+    assert call(S_=0) == ops.MOE_ERR_ARG
+    bad = ops.rpp_dims(dict(dims, n_heads=5))           # d_model % n_heads != 0
+    assert lib.moe_rpp_weights_count(ctypes.byref(bad)) == 0
+    assert call(gg=bad) == ops.MOE_ERR_ARG
+    odd = ops.rpp_dims(dict(dims, max_distance=100))    # not a power of two
+    assert call(gg=odd, nbytes=lib.moe_rpp_workspace(2, 8, ctypes.byref(odd))) == \
+        ops.MOE_ERR_UNSUPPORTED
+    assert call(nbytes=ws - 1) == ops.MOE_ERR_WORKSPACE

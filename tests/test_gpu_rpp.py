@@ -1,0 +1,81 @@
+"""GPU parity of the routing-path-predictor forward (Sec. 3.2) against the
+float64 oracle: float32 arithmetic, so logits within 1e-4 * max|ref| (plus
+1e-5) and probabilities within 1e-5; the relative-position buckets are exact
+on both sides, so no bucket can differ."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import rpp as orpp
+from paper_2410_17954_amd import ops
+from gpu_helpers import to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+PAPER = dict(vocab=32000, d_model=32, n_heads=4, d_ff=2048, n_enc=3, n_dec=3, L=32, E=8,
+             num_buckets=32, max_distance=128, eps=1e-6)
+
+
+def _weights(dims, seed):
+    """Embeddings N(0, 1); each linear layer N(0, 1/fan_in); norm scales near 1."""
+    g = np.random.default_rng(seed)
+    w = g.standard_normal(orpp.n_weights(dims))
+    p = orpp.unpack(w, dims)                  # views: scale in place
+    d, dff = dims["d_model"], dims["d_ff"]
+    for lay in p["enc"] + p["dec"]:
+        for k, v in lay.items():
+            if k.startswith("ln"):
+                v[:] = 1.0 + 0.1 * v
+            else:
+                v *= 1.0 / np.sqrt(dff if k == "wo" else d)
+    for k in ("enc_ln", "dec_ln"):
+        p[k][:] = 1.0 + 0.1 * p[k]
+    p["heads"] *= 1.0 / np.sqrt(d)
+    return w.astype(np.float32)
+
+
+def _check(dims, B, S, seed, sample=None):
+    """GPU on all B sequences; the oracle on `sample` of them (sequences are
+    independent) or on all."""
+    w = _weights(dims, seed)
+    ids = np.random.default_rng(seed + 1).integers(0, dims["vocab"], size=(B, S)).astype(np.int32)
+    probs, logits, err = ops.rpp_forward(to_dev(ids), to_dev(w), dims, want_logits=True)
+    torch.cuda.synchronize()
+    assert to_host(err)[0] == 0
+    rows = np.arange(B) if sample is None else np.asarray(sample)
+    rp, rl = orpp.rpp_forward(ids[rows], w.astype(np.float64), dims)
+    gl = to_host(logits).astype(np.float64)[rows]
+    assert np.abs(gl - rl).max() <= 1e-4 * np.abs(rl).max() + 1e-5
+    assert np.abs(to_host(probs).astype(np.float64)[rows] - rp).max() <= 1e-5
+
+
+def test_small_dims_ragged_sequences():
+    dims = dict(vocab=50, d_model=16, n_heads=4, d_ff=32, n_enc=2, n_dec=2, L=3, E=5,
+                num_buckets=32, max_distance=128, eps=1e-6)
+    _check(dims, 3, 37, seed=1)
+
+
+def test_paper_dims_beyond_max_distance():
+    # 200 tokens: distances past 128 fall in the last buckets; 200 > one block of queries
+    _check(PAPER, 4, 200, seed=2)
+
+
+@pytest.mark.parametrize("h", [2, 1])
+def test_wider_attention_heads(h):
+    _check(dict(PAPER, vocab=500, n_heads=h, n_enc=1, n_dec=1, L=4, E=6), 2, 70, seed=3 + h)
+
+
+def test_scheduling_unit_of_8192_tokens():
+    # the bench's batch: 16 sequences of 512 tokens, Mixtral's 32 layers x 8 experts;
+    # the oracle checks the first and the last sequence
+    _check(PAPER, 16, 512, seed=5, sample=[0, 15])
+
+
+def test_out_of_range_ids_are_flagged():
+    dims = dict(PAPER, vocab=100, n_enc=1, n_dec=1, L=2, E=4)
+    w = _weights(dims, 6)
+    ids = np.array([[1, 2, 100], [-1, 5, 6]], dtype=np.int32)
+    probs, _, err = ops.rpp_forward(to_dev(ids), to_dev(w), dims)
+    torch.cuda.synchronize()
+    assert to_host(err)[0] == 1
+    assert np.isfinite(to_host(probs)).all()
