@@ -255,7 +255,7 @@ int moe_stack_forward(void* h, int32_t dtype, int64_t n_tokens, int64_t H,
  *          int32, cleared by the caller) and embeds as zeros
  * probs    DEVICE float32 [B, S, L, E]; logits the same or NULL
  * Limits: d_model % n_heads == 0 with d_kv in {4, 8, 16, 32, 64};
- *   2*S*d_kv*4 <= 64 KiB; num_buckets even; the bucket sizes powers of two.
+ *   (2*S*d_kv + 2*S)*4 bytes <= 64 KiB; num_buckets even; the bucket sizes powers of two.
  * Errors: MOE_ERR_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE.
  * ---------------------------------------------------------------------- */
 typedef struct moe_rpp_dims {

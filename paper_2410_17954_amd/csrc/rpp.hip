@@ -94,16 +94,22 @@ __global__ void rpp_embed(const int32_t* __restrict__ ids, int64_t M, int V, int
   x[q] = emb[(int64_t)id * d + c];
 }
 
-// out = x / sqrt(mean(x^2) + eps) * w, one thread per row
-__global__ void rpp_rmsnorm(const float* __restrict__ x, int64_t M, int d,
-                            const float* __restrict__ w, float eps, float* __restrict__ out) {
-  const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-  if (t >= M) return;
-  const float* r = x + t * d;
+// out = x / sqrt(mean(x^2) + eps) * w; 32 lanes per row (lane c takes columns
+// c, c + 32, ...), the sum of squares reduced across them in a fixed order.
+__global__ void __launch_bounds__(256)
+rpp_rmsnorm(const float* __restrict__ x, int64_t M, int d, const float* __restrict__ w,
+            float eps, float* __restrict__ out) {
+  const int64_t t = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 5;
+  const int lane = threadIdx.x & 31;
+  const bool live = t < M;
+  const float* r = x + (live ? t : 0) * d;
   float ss = 0.f;
-  for (int c = 0; c < d; ++c) ss += r[c] * r[c];
+  if (live)
+    for (int c = lane; c < d; c += 32) ss += r[c] * r[c];
+  for (int o = 16; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 32);
+  if (!live) return;
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int c = 0; c < d; ++c) out[t * d + c] = r[c] * inv * w[c];
+  for (int c = lane; c < d; c += 32) out[t * d + c] = r[c] * inv * w[c];
 }
 
 enum GemmMode { G_STORE = 0, G_ADD = 1, G_RELU = 2, G_SIGMOID = 3 };
@@ -168,11 +174,15 @@ rpp_gemm(const float* __restrict__ A, int64_t lda, const float* __restrict__ W, 
   }
 }
 
-// One thread per (sequence b, head h, query i): softmax over keys j of
-// q_i . k_j (+ bias of bucket(i - j)) with j <= i when causal, then the
-// weighted sum of v_j. Keys and values of (b, h) staged in LDS.
+// Attention of (sequence b, head h) for 64 queries per block: softmax over
+// keys j of q_i . k_j (+ the bias of distance i - j) with j <= i when causal,
+// then the weighted sum of v_j. Keys, values and the head's bias per distance
+// (2S - 1 values) are staged in LDS; each query's keys are split over kSplit
+// neighbouring lanes (key j goes to lane j mod kSplit), whose running softmax
+// states are merged with lane shuffles in a fixed order.
+constexpr int kAttQ = 64, kSplit = 4;
 template <int DK>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(kAttQ * kSplit)
 rpp_attention(const float* __restrict__ Q, int64_t ldq, const float* __restrict__ Kp,
               const float* __restrict__ Vp, int64_t ldkv, int S, int h_count,
               const float* __restrict__ rel, RelBuckets rb, int use_bias, int causal,
@@ -180,6 +190,7 @@ rpp_attention(const float* __restrict__ Q, int64_t ldq, const float* __restrict_
   extern __shared__ float kv_lds[];
   float* const ks = kv_lds;
   float* const vs = kv_lds + (size_t)S * DK;
+  float* const bt = vs + (size_t)S * DK;              // bias of distance n at bt[n + S - 1]
   const int h = blockIdx.y, b = blockIdx.z;
   const int64_t base = (int64_t)b * S;
   for (int q = threadIdx.x; q < S * DK; q += blockDim.x) {
@@ -187,33 +198,55 @@ rpp_attention(const float* __restrict__ Q, int64_t ldq, const float* __restrict_
     ks[q] = Kp[(base + j) * ldkv + h * DK + c];
     vs[q] = Vp[(base + j) * ldkv + h * DK + c];
   }
+  if (use_bias)
+    for (int q = threadIdx.x; q < 2 * S - 1; q += blockDim.x)
+      bt[q] = rel[rel_bucket(rb, q - (S - 1)) * h_count + h];
   __syncthreads();
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= S) return;
+  const int split = threadIdx.x % kSplit;
+  const int i = blockIdx.x * kAttQ + threadIdx.x / kSplit;
+  const bool live = i < S;
   float qv[DK], acc[DK];
 #pragma unroll
   for (int c = 0; c < DK; ++c) {
-    qv[c] = Q[(base + i) * ldq + h * DK + c];
+    qv[c] = live ? Q[(base + i) * ldq + h * DK + c] : 0.f;
     acc[c] = 0.f;
   }
   float mx = -INFINITY, den = 0.f;
-  const int jend = causal ? i + 1 : S;
-  for (int j = 0; j < jend; ++j) {
-    float s = 0.f;
+  const int jend = !live ? 0 : (causal ? i + 1 : S);
+  for (int j = split; j < jend; j += kSplit) {
+    float sc = 0.f;
 #pragma unroll
-    for (int c = 0; c < DK; ++c) s = fmaf(qv[c], ks[j * DK + c], s);
-    if (use_bias) s += rel[rel_bucket(rb, i - j) * h_count + h];
-    const float nm = fmaxf(mx, s);
-    const float scale = __expf(mx - nm), p = __expf(s - nm);
+    for (int c = 0; c < DK; ++c) sc = fmaf(qv[c], ks[j * DK + c], sc);
+    if (use_bias) sc += bt[i - j + S - 1];
+    const float nm = fmaxf(mx, sc);
+    const float scale = __expf(mx - nm), p = __expf(sc - nm);
     den = den * scale + p;
 #pragma unroll
     for (int c = 0; c < DK; ++c) acc[c] = fmaf(p, vs[j * DK + c], acc[c] * scale);
     mx = nm;
   }
+  // merge the kSplit states of a query (lanes 4q .. 4q+3): pairs at distance 1, then 2
+#pragma unroll
+  for (int o = 1; o < kSplit; o <<= 1) {
+    const float m2 = __shfl_xor(mx, o), d2 = __shfl_xor(den, o);
+    const float nm = fmaxf(mx, m2);
+    const float s1 = mx == -INFINITY ? 0.f : __expf(mx - nm);
+    const float s2 = m2 == -INFINITY ? 0.f : __expf(m2 - nm);
+    den = den * s1 + d2 * s2;
+#pragma unroll
+    for (int c = 0; c < DK; ++c) {
+      const float a2 = __shfl_xor(acc[c], o);
+      acc[c] = acc[c] * s1 + a2 * s2;
+    }
+    mx = nm;
+  }
+  if (!live || split != 0) return;
   const float inv = 1.0f / den;
 #pragma unroll
   for (int c = 0; c < DK; ++c) O[(base + i) * ldo + h * DK + c] = acc[c] * inv;
 }
+
+constexpr int kMlpRows = 32, kMlpChunk = 64, kMlpSplit = 8;   // fused feed-forward tiles
 
 struct RppOffsets {
   size_t emb, enc_rel, enc_ln, dec_rel, dec_ln, heads, total;
@@ -277,7 +310,7 @@ RppWs rpp_ws(int64_t M, const moe_rpp_dims& g) {
   w.o = take(M * d);
   w.qkv = take(M * 3 * d);
   w.kv = take(M * 2 * d);
-  w.hid = take(M * (size_t)g.d_ff);
+  w.hid = take(M * (size_t)std::max(g.d_ff, kMlpSplit * g.d_model));
   w.logits = take(M * (size_t)g.L * g.E);
   w.total = off;
   return w;
@@ -303,14 +336,122 @@ int gemm(hipStream_t st, const float* A, int64_t lda, const float* W, int64_t M,
   return hipGetLastError() == hipSuccess ? MOE_OK : MOE_ERR_HIP;
 }
 
+// Feed-forward block, fused: x[r] += W2 relu(W1 n[r]). Block (row tile, s)
+// takes 32 rows through the s-th of kMlpSplit parts of the hidden width, in
+// chunks of 64 through LDS (the hidden activations never leave the compute
+// unit), loading the next chunk's weights into registers while the current
+// one is used, and writes its partial output; rpp_mlp_sum adds the parts and
+// the residual in part order. D = d_model (a multiple of 8, <= 64).
+template <int D>
+__global__ void __launch_bounds__(256)
+rpp_mlp(const float* __restrict__ n, int64_t M, const float* __restrict__ W1,
+        const float* __restrict__ W2, int dff, float* __restrict__ part) {
+  __shared__ float Ns[kMlpRows][D + 1];
+  __shared__ float W1s[kMlpChunk][D + 1];             // hidden unit c of the chunk, its D inputs
+  __shared__ float Hs[kMlpRows][kMlpChunk + 1];
+  __shared__ float W2s[D][kMlpChunk + 1];             // output o, the chunk's hidden units
+  constexpr int OPT = D / 8;                          // outputs per thread
+  constexpr int PER = kMlpChunk * D / 256;            // weights of each matrix a thread moves
+  const int t = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.x * kMlpRows;
+  const int per_split = (dff + kMlpSplit - 1) / kMlpSplit;
+  const int fbeg = min(dff, (int)blockIdx.y * per_split);
+  const int fend = min(dff, fbeg + per_split);
+  for (int q = t; q < kMlpRows * D; q += 256) {
+    const int r = q / D, c = q % D;
+    Ns[r][c] = r0 + r < M ? n[(r0 + r) * D + c] : 0.f;
+  }
+  float w1r[PER], w2r[PER];
+  auto fetch = [&](int f0) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int q = t + 256 * u;
+      const int c = q / D, k = q % D;                 // W1 row f0 + c, column k
+      w1r[u] = f0 + c < fend ? W1[(int64_t)(f0 + c) * D + k] : 0.f;
+      const int o = q / kMlpChunk, kk = q % kMlpChunk;   // W2 row o, column f0 + kk
+      w2r[u] = f0 + kk < fend ? W2[(int64_t)o * dff + f0 + kk] : 0.f;
+    }
+  };
+  const int r = t >> 3;                               // this thread's row
+  const int c0 = (t & 7) * 8;                         // its 8 hidden units of a chunk
+  const int o0 = (t & 7) * OPT;                       // its output columns
+  float acc[OPT];
+#pragma unroll
+  for (int j = 0; j < OPT; ++j) acc[j] = 0.f;
+  if (fbeg < fend) fetch(fbeg);
+  for (int f0 = fbeg; f0 < fend; f0 += kMlpChunk) {
+    __syncthreads();                                  // the previous chunk is fully used
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int q = t + 256 * u;
+      W1s[q / D][q % D] = w1r[u];
+      W2s[q / kMlpChunk][q % kMlpChunk] = w2r[u];
+    }
+    __syncthreads();
+    if (f0 + kMlpChunk < fend) fetch(f0 + kMlpChunk);  // in flight during this chunk
+    float hv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) hv[j] = 0.f;
+#pragma unroll 8
+    for (int k = 0; k < D; ++k) {
+      const float a = Ns[r][k];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) hv[j] = fmaf(a, W1s[c0 + j][k], hv[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) Hs[r][c0 + j] = fmaxf(hv[j], 0.f);
+    __syncthreads();
+#pragma unroll 8
+    for (int k = 0; k < kMlpChunk; ++k) {
+      const float a = Hs[r][k];
+#pragma unroll
+      for (int j = 0; j < OPT; ++j) acc[j] = fmaf(a, W2s[o0 + j][k], acc[j]);
+    }
+  }
+  if (r0 + r < M) {
+    float* const out = part + ((int64_t)blockIdx.y * M + r0 + r) * D + o0;
+#pragma unroll
+    for (int j = 0; j < OPT; ++j) out[j] = acc[j];
+  }
+}
+
+// x += part[0] + part[1] + ... in part order
+__global__ void rpp_mlp_sum(const float* __restrict__ part, int64_t n, float* __restrict__ x) {
+  const int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (q >= n) return;
+  float v = part[q];
+#pragma unroll
+  for (int s = 1; s < kMlpSplit; ++s) v += part[s * n + q];
+  x[q] += v;
+}
+
+int mlp(hipStream_t st, const float* n, int64_t M, int d, const float* W1, const float* W2,
+        int dff, float* hid, float* x) {
+  // hid (M * dff floats) holds the kMlpSplit partial outputs (M * d each)
+  const dim3 grid((unsigned)ceil_div(M, kMlpRows), kMlpSplit);
+  switch (d) {
+    case 16: rpp_mlp<16><<<grid, dim3(256), 0, st>>>(n, M, W1, W2, dff, hid); break;
+    case 32: rpp_mlp<32><<<grid, dim3(256), 0, st>>>(n, M, W1, W2, dff, hid); break;
+    case 64: rpp_mlp<64><<<grid, dim3(256), 0, st>>>(n, M, W1, W2, dff, hid); break;
+    default: {                                        // other widths: two GEMMs via memory
+      int rc = gemm<G_RELU>(st, n, d, W1, M, dff, d, hid, dff);
+      if (rc != MOE_OK) return rc;
+      return gemm<G_ADD>(st, hid, dff, W2, M, d, dff, x, d);
+    }
+  }
+  if (hipGetLastError() != hipSuccess) return MOE_ERR_HIP;
+  rpp_mlp_sum<<<dim3((unsigned)ceil_div(M * d, 256)), dim3(256), 0, st>>>(hid, M * d, x);
+  return hipGetLastError() == hipSuccess ? MOE_OK : MOE_ERR_HIP;
+}
+
 int attention(hipStream_t st, int dk, const float* Q, int64_t ldq, const float* Kp,
               const float* Vp, int64_t ldkv, int B, int S, int h, const float* rel,
               const RelBuckets& rb, bool use_bias, bool causal, float* O, int64_t ldo) {
-  const dim3 grid((unsigned)ceil_div(S, 256), (unsigned)h, (unsigned)B);
-  const size_t lds = (size_t)2 * S * dk * sizeof(float);
-#define MOE_ATT(DKV)                                                                         \
-  rpp_attention<DKV><<<grid, dim3(256), lds, st>>>(Q, ldq, Kp, Vp, ldkv, S, h, rel, rb,     \
-                                                   use_bias ? 1 : 0, causal ? 1 : 0, O, ldo)
+  const dim3 grid((unsigned)ceil_div(S, kAttQ), (unsigned)h, (unsigned)B);
+  const size_t lds = ((size_t)2 * S * dk + 2 * S) * sizeof(float);
+#define MOE_ATT(DKV)                                                                          \
+  rpp_attention<DKV><<<grid, dim3(kAttQ * kSplit), lds, st>>>(                               \
+      Q, ldq, Kp, Vp, ldkv, S, h, rel, rb, use_bias ? 1 : 0, causal ? 1 : 0, O, ldo)
   switch (dk) {
     case 4: MOE_ATT(4); break;
     case 8: MOE_ATT(8); break;
@@ -345,7 +486,7 @@ extern "C" int moe_rpp_forward(const int32_t* ids, int32_t B, int32_t S, const m
   const int d = g.d_model, h = g.n_heads, dk = d / h;
   const int64_t M = (int64_t)B * S;
   if (M * std::max(g.d_ff, 3 * d) >= ((int64_t)1 << 31) / 4 ||
-      (size_t)2 * S * dk * sizeof(float) > 64 * 1024 || (size_t)S > 65535 * 256ull)
+      ((size_t)2 * S * dk + 2 * S) * sizeof(float) > 64 * 1024)
     return MOE_ERR_UNSUPPORTED;
   RelBuckets rb_enc{}, rb_dec{};
   if (!make_buckets(true, g.num_buckets, g.max_distance, &rb_enc) ||
@@ -362,7 +503,7 @@ extern "C" int moe_rpp_forward(const int32_t* ids, int32_t B, int32_t S, const m
   const RppOffsets wo = rpp_offsets(g);
   const float* W = weights;
   hipStream_t st = as_stream(stream);
-  const dim3 rows((unsigned)ceil_div(M, 256));
+  const dim3 rows((unsigned)ceil_div(M * 32, 256));      // 32 lanes per row
   const size_t dd = (size_t)d * d, df = (size_t)d * g.d_ff;
   int rc = MOE_OK;
 #define MOE_RC(expr)                  \
@@ -386,8 +527,7 @@ extern "C" int moe_rpp_forward(const int32_t* ids, int32_t B, int32_t S, const m
     MOE_RC(gemm<G_ADD>(st, o, d, wout, M, d, d, x, d));
     rpp_rmsnorm<<<rows, dim3(256), 0, st>>>(x, M, d, ln2, g.eps, n);
     MOE_CHECK_LAUNCH();
-    MOE_RC(gemm<G_RELU>(st, n, d, wi, M, g.d_ff, d, hid, g.d_ff));
-    MOE_RC(gemm<G_ADD>(st, hid, g.d_ff, wo2, M, d, g.d_ff, x, d));
+    MOE_RC(mlp(st, n, M, d, wi, wo2, g.d_ff, hid, x));
   }
   rpp_rmsnorm<<<rows, dim3(256), 0, st>>>(x, M, d, W + wo.enc_ln, g.eps, enc);
   MOE_CHECK_LAUNCH();
@@ -414,8 +554,7 @@ extern "C" int moe_rpp_forward(const int32_t* ids, int32_t B, int32_t S, const m
     MOE_RC(gemm<G_ADD>(st, o, d, cout, M, d, d, y, d));
     rpp_rmsnorm<<<rows, dim3(256), 0, st>>>(y, M, d, ln3, g.eps, n);
     MOE_CHECK_LAUNCH();
-    MOE_RC(gemm<G_RELU>(st, n, d, wi, M, g.d_ff, d, hid, g.d_ff));
-    MOE_RC(gemm<G_ADD>(st, hid, g.d_ff, wo2, M, d, g.d_ff, y, d));
+    MOE_RC(mlp(st, n, M, d, wi, wo2, g.d_ff, hid, y));
   }
   rpp_rmsnorm<<<rows, dim3(256), 0, st>>>(y, M, d, W + wo.dec_ln, g.eps, n);
   MOE_CHECK_LAUNCH();
