@@ -173,3 +173,28 @@ def test_stack_full_shape_two_layers_sampled():
         tol = 1e-2 * np.abs(ref["y"]).max() + 2.0 ** -8 * np.abs(want)
         assert (np.abs(nxt - want) <= tol).all()
     assert np.array_equal(to_host(h)[0::2], h0[0::2])
+
+
+def test_stack_float32():
+    # float32 state and weights: 16-byte rows of 4 values, the scalar norm path
+    L, E, H, F, k, T = 2, 8, 128, 256, 2, 97
+    g = np.random.default_rng(13)
+    lay = [tuple(g.standard_normal(s).astype(np.float32) * np.float32(sc)
+                 for s, sc in (((E, H), 0.05), ((E, F, H), 0.03), ((E, F, H), 0.03),
+                               ((E, H, F), 0.03))) for _ in range(L)]
+    h0 = g.standard_normal((T, H)).astype(np.float32)
+    h = to_dev(h0)
+    trace = torch.empty((L, 2, T, H), dtype=torch.float32, device="cuda:0")
+    itr = torch.empty((L, T, k), dtype=torch.int32, device="cuda:0")
+    ops.stack_forward(h, [tuple(to_dev(a) for a in l_) for l_ in lay], k, pre_norm=True,
+                      h_trace=trace, idx_trace=itr)
+    torch.cuda.synchronize()
+    tr, it, hv = to_host(trace).astype(np.float64), to_host(itr), to_host(h).astype(np.float64)
+    for l in range(L):
+        state, x = tr[l][0], tr[l][1]
+        assert np.allclose(x, oracle.rms_norm(state), rtol=1e-5, atol=1e-6)
+        wr, wg, wu, wd = (a.astype(np.float64) for a in lay[l])
+        ref = oracle.moe_layer(x, wr, k, wg, wu, wd)
+        assert np.array_equal(it[l], ref["idx"])
+        nxt = tr[l + 1][0] if l + 1 < L else hv
+        assert np.abs(nxt - (state + ref["y"])).max() <= 1e-4 * np.abs(ref["y"]).max() + 1e-5

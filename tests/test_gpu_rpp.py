@@ -79,3 +79,10 @@ def test_out_of_range_ids_are_flagged():
     torch.cuda.synchronize()
     assert to_host(err)[0] == 1
     assert np.isfinite(to_host(probs)).all()
+
+
+@pytest.mark.parametrize("d,h", [(64, 4), (24, 6)])
+def test_other_widths(d, h):
+    # d = 64: the fused feed-forward's widest tile; d = 24: two GEMMs through memory
+    dims = dict(PAPER, vocab=300, d_model=d, n_heads=h, d_ff=200, n_enc=2, n_dec=1, L=3, E=7)
+    _check(dims, 3, 45, seed=20 + d)

@@ -159,3 +159,9 @@ def test_multi_way_mixtral_unit_four_batches():
                                     cfg["zipf"], seed=53)
     rp, ro, ri = _check_multi(routes, cfg["E"], 4)
     assert ro.tolist() == [0, 2048, 4096, 6144, 8192]
+
+
+def test_multi_way_demand_too_large_for_lds():
+    # 70 layers x 256 experts: the per-batch demand counts go straight to memory
+    routes = synth.predicted_routes(300, 70, 256, 2, 0.7, 1.0, seed=54)
+    _check_multi(routes, 256, 3)
