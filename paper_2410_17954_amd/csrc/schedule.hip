@@ -568,6 +568,9 @@ __device__ void grid_sync(unsigned* bar, unsigned nblk, int32_t* err) {
   // needed -- those cost a serialised L2 operation per wave and block.
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  // One block (a few hundred tokens): the block barrier is the whole barrier;
+  // the arrival counter is never touched, so every call takes this branch.
+  if (nblk == 1) return;
   if (threadIdx.x == 0) {
     const unsigned arrived = atomicAdd(bar, 1u) + 1u;
     const unsigned target = (arrived + nblk - 1u) / nblk * nblk;
