@@ -645,6 +645,8 @@ def main():
             prev = base + 2
     st = {n: v / K for n, v in st.items()}
 
+    ceilings = measured_ceilings(torch, ops, dev)
+
     if args.copy_probe_mib > 0:
         src = torch.empty(args.copy_probe_mib * 2**20, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -674,6 +676,10 @@ def main():
         "combine": {"ms": st["combine"], "GB/s": bytes_comb / st["combine"] / 1e6,
                     "hbm_frac": bytes_comb / st["combine"] / 1e6 / PEAK_HBM_GBS},
     }
+    # the same fractions against what this chip measured (probe kernels, below)
+    for name in ("route", "permute", "combine"):
+        stages[name]["hbm_frac_measured"] = stages[name]["GB/s"] / ceilings["hbm_read_GBps"]
+    stages["expert_ffn"]["mfma_frac_measured"] = achieved / ceilings["mfma_bf16_TFLOPs"]
 
     out = {
         "metric": METRIC,
@@ -703,11 +709,55 @@ def main():
             "flop_per_launch": ffn_flops, "launch_ms": ffn_ms,
         },
         "stages": stages,
+        "measured_ceilings": ceilings,
         "setup_s": gen_s,
     }
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(inp, routes, cfg, args.cpu_seconds)
     print(json.dumps(out))
+
+
+def measured_ceilings(torch, ops, dev):
+    """What this GPU reaches in practice, measured after the timed region with
+    the library's probe kernels: a loop of dense bf16 32x32x16 MFMAs on every
+    SIMD (random operands that keep changing, no memory traffic), and one
+    streaming read of a 1 GiB buffer (larger than the last-level cache;
+    median of 5 passes)."""
+    lib = ops.load_library()
+    st = torch.cuda.current_stream().cuda_stream
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    src = torch.randn(8 * 64 * 8, generator=g, device=dev).to(torch.bfloat16)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    out_f = torch.empty(8 * cus * 256, dtype=torch.float32, device=dev)
+    out_u = torch.empty(8 * cus * 256, dtype=torch.int32, device=dev)
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(n):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    iters = 256
+    flops = lib.moe_probe_mfma_bf16(ops._ptr(src), iters, ops._ptr(out_f), out_f.numel(), st)
+    if flops <= 0:
+        raise RuntimeError("moe_probe_mfma_bf16 failed")
+    ms = timed(lambda: lib.moe_probe_mfma_bf16(ops._ptr(src), iters, ops._ptr(out_f),
+                                               out_f.numel(), st), 5)
+    buf = torch.ones(2 ** 30, dtype=torch.uint8, device=dev)
+    rms = timed(lambda: lib.moe_probe_read(ops._ptr(buf), buf.numel(), ops._ptr(out_u),
+                                           out_u.numel(), st), 5)
+    return {"mfma_bf16_TFLOPs": flops / (ms * 1e-3) / 1e12,
+            "hbm_read_GBps": buf.numel() / (rms * 1e-3) / 1e9,
+            "probes": "moe_probe_mfma_bf16 (4 waves per SIMD, 8 MFMA chains, "
+                      f"{iters} rounds), moe_probe_read (1 GiB, one pass)"}
 
 
 def measured_traffic():

@@ -269,6 +269,22 @@ int moe_rpp_forward(const int32_t* ids, int32_t B, int32_t S, const moe_rpp_dims
                     void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Measured ceilings (for roofline reports; not part of the method):
+ * moe_probe_mfma_bf16 runs iters (a multiple of 4) rounds of 8 independent
+ * 32x32x16 bf16 MFMAs per wave, 4 waves per SIMD on every compute unit, with
+ * operands taken from src (DEVICE, >= 8 x 64 x 8 bf16 values, cycled so they
+ * keep changing) and one float per thread written to out (DEVICE, out_len >=
+ * 1024 x compute units); returns the flops launched (negative on error).
+ * moe_probe_read reads `bytes` (a multiple of 16, 16-byte aligned DEVICE
+ * memory) once with one 16-byte load per lane, grid-stride, and writes one
+ * word per thread to out (out_len >= 2048 x compute units).
+ * ---------------------------------------------------------------------- */
+int64_t moe_probe_mfma_bf16(const void* src, int64_t iters, float* out, int32_t out_len,
+                            void* stream);
+int moe_probe_read(const void* src, int64_t bytes, uint32_t* out, int32_t out_len,
+                   void* stream);
+
+/* ------------------------------------------------------------------------
  * moe_permute -- group the (token, choice) pairs of one batch by expert so
  * that every expert sees its tokens as one contiguous block of rows.
  *

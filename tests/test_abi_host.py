@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 23, names
+    assert len(names) == 25, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
