@@ -283,17 +283,22 @@ constexpr int kSmallCols = 16 * kSmallNT;
 constexpr int kSmallU = 4;                       // K steps of 32 loaded per batch
 constexpr int kSmallWaves = 4;
 
-template <int EPI, int MT>
+// MTMAX = 1: the experts of list1 (at most 16 rows); MTMAX = 2: those of list1
+// and then those of list2 (17 to 32 rows, two row tiles) in one launch, each
+// unit taking the body for its row tiles (the branch is uniform per block).
+template <int EPI, int MTMAX>
 __global__ void __launch_bounds__(64 * kSmallWaves)
 ffn_small_bf16(const uint16_t* __restrict__ A, int64_t K, const uint16_t* __restrict__ B0,
                const uint16_t* __restrict__ B1, int64_t F, int64_t H,
                const int32_t* __restrict__ offsets, const int32_t* __restrict__ slot,
-               int64_t max_rows, const int32_t* __restrict__ list, uint16_t* __restrict__ C) {
+               int64_t max_rows, const int32_t* __restrict__ list1,
+               const int32_t* __restrict__ list2, uint16_t* __restrict__ C) {
   constexpr int NB = EPI == 0 ? 2 : 1;           // gate and up, or down
-  __shared__ f32x4_t part[kSmallWaves][MT][kSmallNT][NB][kWave];
+  __shared__ f32x4_t part[kSmallWaves][MTMAX][kSmallNT][NB][kWave];
   const int64_t N_out = EPI == 0 ? F : H;        // a multiple of kSmallCols (fast path)
   const int ncb = (int)(N_out / kSmallCols);
-  const int64_t units = (int64_t)list[0] * ncb;
+  const int64_t units1 = (int64_t)list1[0] * ncb;
+  const int64_t units = units1 + (MTMAX == 2 ? (int64_t)list2[0] * ncb : 0);
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
   const int r = lane & 15;                       // A row / B column of this lane
@@ -306,9 +311,8 @@ ffn_small_bf16(const uint16_t* __restrict__ A, int64_t K, const uint16_t* __rest
   const uint32_t b_off = (uint32_t)(((int64_t)r * K + kq) * 2);
   // units (expert, column block) in order, the grid striding over them: at any
   // time the blocks work on neighbouring columns
-  for (int64_t unit = blockIdx.x; unit < units; unit += gridDim.x) {
-    const int li = (int)(unit / ncb), cb = (int)(unit % ncb);
-    const int e = list[1 + li];
+  auto run_unit = [&](auto mt_c, int e, int cb) {
+    constexpr int MT = decltype(mt_c)::value;
     const int s = slot ? slot[e] : e;
     int64_t lo = offsets[e], hi = offsets[e + 1];
     lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
@@ -405,6 +409,14 @@ ffn_small_bf16(const uint16_t* __restrict__ A, int64_t K, const uint16_t* __rest
         }
     }
     __syncthreads();                               // part is rewritten by the next unit
+  };
+  for (int64_t unit = blockIdx.x; unit < units; unit += gridDim.x) {
+    if (MTMAX == 1 || unit < units1) {
+      run_unit(std::integral_constant<int, 1>{}, list1[1 + (int)(unit / ncb)], (int)(unit % ncb));
+    } else if constexpr (MTMAX == 2) {
+      const int64_t u = unit - units1;
+      run_unit(std::integral_constant<int, 2>{}, list2[1 + (int)(u / ncb)], (int)(u % ncb));
+    }
   }
 }
 
@@ -1056,14 +1068,13 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
           claim, tail, partial, pieces, ab);
       MOE_CHECK_LAUNCH();
     }
-    if (few) {
+    if (few && !mid) {
       ffn_small_bf16<0, 1><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list1, ab);
+          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, ab);
       MOE_CHECK_LAUNCH();
-    }
-    if (mid) {
+    } else if (mid) {
       ffn_small_bf16<0, 2><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list2, ab);
+          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, ab);
       MOE_CHECK_LAUNCH();
     }
     if (big) {
@@ -1072,14 +1083,13 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
           claim + 8, tail + kTailWords, partial, pieces, yb);
       MOE_CHECK_LAUNCH();
     }
-    if (few) {
+    if (few && !mid) {
       ffn_small_bf16<1, 1><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list1, yb);
+          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, yb);
       MOE_CHECK_LAUNCH();
-    }
-    if (mid) {
+    } else if (mid) {
       ffn_small_bf16<1, 2><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list2, yb);
+          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, yb);
       MOE_CHECK_LAUNCH();
     }
     return MOE_OK;
