@@ -1126,6 +1126,410 @@ sch_fin_scatter(int N, int n1, int LE, int trivial, const int32_t* __restrict__ 
   }
 }
 
+// ---------------------------------------------------------------- one block
+// Up to kSmallN tokens whose packed paths fit in LDS (decode-sized units and
+// the small nodes of a B-way split): every step in one block and one launch,
+// all state in LDS. Same results as the multi-kernel path, step for step:
+// signature order by a bitonic sort under the lowest-differing-bit rule, m1
+// and m2, then per round the delta histogram, the threshold with the tie
+// quota taken in signature order, the batch-1 column counts, and both
+// centroids as (distance sum, signature rank) minima; the guard and outputs.
+// Per-token sums are spread over (token, word) items with LDS atomics, so the
+// work of a few tokens still runs on all waves of the block; a centroid
+// candidate is one 32-bit key (sum << 10 | rank) reduced with DPP moves, and
+// the sort's in-wave stages exchange through lane shuffles, not LDS.
+constexpr int kSmallN = kSel;
+constexpr int kSmallRankBits = 10;               // signature rank < kSmallN
+constexpr int kSmallMaxLk = 2048;                // sums < kSmallN * 2 L k fit 22 bits
+constexpr int kSmallPre = 8;                     // 16-byte route pieces in flight per thread
+constexpr size_t kSmallMaxLds = 140 * 1024;
+static_assert(kSmallN <= (1 << kSmallRankBits), "rank field");
+static_assert((int64_t)kSmallN * 2 * kSmallMaxLk <= (1ll << (32 - kSmallRankBits)), "sum field");
+
+struct SmallLds {
+  size_t bits, cnt_all, cnt1, cnt_orig, hist, idx, rank, ones, dbin, in1, sall, s1, skey, stok,
+      total;
+};
+
+__host__ __device__ inline size_t small_align(size_t v) { return (v + 15) & ~(size_t)15; }
+
+__host__ __device__ inline SmallLds small_lds(int N, int W, int LE, int nbins) {
+  int NP = 1;
+  while (NP < N) NP <<= 1;
+  SmallLds o{};
+  size_t p = 0;
+  o.bits = p;     p = small_align(p + (size_t)N * W * 8);
+  o.cnt_all = p;  p = small_align(p + (size_t)LE * 4);
+  o.cnt1 = p;     p = small_align(p + (size_t)LE * 4);
+  o.cnt_orig = p; p = small_align(p + (size_t)LE * 4);
+  o.hist = p;     p = small_align(p + (size_t)nbins * 4);
+  o.idx = p;      p = small_align(p + (size_t)N * 4);
+  o.rank = p;     p = small_align(p + (size_t)N * 4);
+  o.ones = p;     p = small_align(p + (size_t)N * 4);
+  o.dbin = p;     p = small_align(p + (size_t)N * 4);
+  o.in1 = p;      p = small_align(p + (size_t)N * 4);
+  o.sall = p;     p = small_align(p + (size_t)N * 4);
+  o.s1 = p;       p = small_align(p + (size_t)N * 4);
+  o.skey = p;     p = small_align(p + (size_t)(NP >= 128 ? NP : 0) * 8);
+  o.stok = p;     p = small_align(p + (size_t)(NP >= 128 ? NP : 0) * 4);
+  o.total = p;
+  return o;
+}
+
+// DPP move within rows of 16 lanes (lanes without a source keep `old`)
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t small_dpp(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWS, 0xf, false);
+}
+
+// Minimum over the wave (every lane active), in every lane: row_shr 1, 2, 4, 8
+// within rows of 16, then row 15 into rows 1 and 3, row 31 into rows 2 and 3.
+__device__ __forceinline__ uint32_t small_wave_min(uint32_t v) {
+  v = min(v, small_dpp<0x111, 0xf>(~0u, v));
+  v = min(v, small_dpp<0x112, 0xf>(~0u, v));
+  v = min(v, small_dpp<0x114, 0xf>(~0u, v));
+  v = min(v, small_dpp<0x118, 0xf>(~0u, v));
+  v = min(v, small_dpp<0x142, 0xa>(~0u, v));
+  v = min(v, small_dpp<0x143, 0xc>(~0u, v));
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, kWave - 1);
+}
+
+// Inclusive prefix sum over the wave (every lane active), same moves.
+__device__ __forceinline__ int small_wave_scan(int v) {
+  v += (int)small_dpp<0x111, 0xf>(0u, (uint32_t)v);
+  v += (int)small_dpp<0x112, 0xf>(0u, (uint32_t)v);
+  v += (int)small_dpp<0x114, 0xf>(0u, (uint32_t)v);
+  v += (int)small_dpp<0x118, 0xf>(0u, (uint32_t)v);
+  v += (int)small_dpp<0x142, 0xa>(0u, (uint32_t)v);
+  v += (int)small_dpp<0x143, 0xc>(0u, (uint32_t)v);
+  return v;
+}
+
+// Block-wide minima of two keys at once (all kSel threads call it).
+__device__ __forceinline__ void small_block_min2(uint32_t& a, uint32_t& b, uint32_t* red) {
+  constexpr int NWv = kSel / kWave;
+  a = small_wave_min(a);
+  b = small_wave_min(b);
+  if (lane_id() == 0) {
+    red[threadIdx.x / kWave] = a;
+    red[NWv + threadIdx.x / kWave] = b;
+  }
+  __syncthreads();
+  uint32_t ra = red[0], rb = red[NWv];
+#pragma unroll
+  for (int w = 1; w < NWv; ++w) {
+    ra = min(ra, red[w]);
+    rb = min(rb, red[NWv + w]);
+  }
+  __syncthreads();
+  a = ra;
+  b = rb;
+}
+
+// Block-wide exclusive scan; the block total goes to *total.
+__device__ __forceinline__ int small_block_scan(int v, int* total, int* red) {
+  constexpr int NWv = kSel / kWave;
+  const int inc = small_wave_scan(v);
+  if (lane_id() == kWave - 1) red[threadIdx.x / kWave] = inc;
+  __syncthreads();
+  const int me = threadIdx.x / kWave;
+  int base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NWv; ++w) {
+    const int x = red[w];
+    base += w < me ? x : 0;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - v;
+}
+
+__global__ void __launch_bounds__(kSel)
+sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W, int n1,
+          int max_iters, int keep, int nbins, int32_t* __restrict__ perm,
+          int32_t* __restrict__ demand, int64_t* __restrict__ info) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char s_lds[];
+  __shared__ uint32_t s_red[2 * kSel / kWave];
+  __shared__ int s_t, s_below;
+  const int LE = L * E, Lk = L * k, NW = N * W, tid = threadIdx.x;
+  const SmallLds o = small_lds(N, W, LE, nbins);
+  uint64_t* const bits = reinterpret_cast<uint64_t*>(s_lds + o.bits);
+  uint32_t* const bits32 = reinterpret_cast<uint32_t*>(s_lds + o.bits);
+  int* const cnt_all = reinterpret_cast<int*>(s_lds + o.cnt_all);
+  int* const cnt1 = reinterpret_cast<int*>(s_lds + o.cnt1);
+  int* const cnt_orig = reinterpret_cast<int*>(s_lds + o.cnt_orig);
+  int* const hist = reinterpret_cast<int*>(s_lds + o.hist);
+  int* const idx = reinterpret_cast<int*>(s_lds + o.idx);
+  int* const rank = reinterpret_cast<int*>(s_lds + o.rank);
+  int* const ones = reinterpret_cast<int*>(s_lds + o.ones);
+  int* const dbin = reinterpret_cast<int*>(s_lds + o.dbin);
+  int* const in1 = reinterpret_cast<int*>(s_lds + o.in1);
+  int* const sall = reinterpret_cast<int*>(s_lds + o.sall);
+  int* const s1 = reinterpret_cast<int*>(s_lds + o.s1);
+  uint64_t* const skey = reinterpret_cast<uint64_t*>(s_lds + o.skey);
+  int* const stok = reinterpret_cast<int*>(s_lds + o.stok);
+  int* const s_redi = reinterpret_cast<int*>(s_red);
+
+  for (int q = tid; q < 2 * NW; q += kSel) bits32[q] = 0;
+  for (int c = tid; c < LE; c += kSel) {
+    cnt_all[c] = 0;
+    cnt_orig[c] = 0;
+  }
+  for (int i = tid; i < N; i += kSel) {
+    ones[i] = 0;
+    sall[i] = 0;
+    dbin[i] = 0;
+  }
+  __syncthreads();
+
+  // paths: bit l*E+e of token i for each id e < E of its route; a bit set for
+  // the first time counts once towards |r_i| and its column
+  int my_ones = 0;
+  auto set_bit = [&](int tok, int l, int e) {
+    if (e >= E) return;
+    const int col = l * E + e;
+    const uint32_t m = 1u << (col & 31);
+    if (atomicOr(&bits32[tok * 2 * W + (col >> 5)], m) & m) return;
+    ++my_ones;
+    atomicAdd(&ones[tok], 1);
+    atomicAdd(&cnt_all[col], 1);
+    if (tok < n1) atomicAdd(&cnt_orig[col], 1);
+  };
+  const int64_t nbytes = (int64_t)N * Lk;
+  const int64_t npiece = (reinterpret_cast<uintptr_t>(routes) & 15) ? 0 : nbytes / 16;
+  for (int64_t q0 = 0; q0 < npiece; q0 += (int64_t)kSmallPre * kSel) {
+    u32x4_t v[kSmallPre];
+#pragma unroll
+    for (int u = 0; u < kSmallPre; ++u) {
+      const int64_t q = q0 + (int64_t)u * kSel + tid;
+      if (q < npiece) v[u] = reinterpret_cast<const u32x4_t*>(routes)[q];
+    }
+#pragma unroll
+    for (int u = 0; u < kSmallPre; ++u) {
+      const int64_t q = q0 + (int64_t)u * kSel + tid;
+      if (q < npiece) {
+        int tok = (int)(q * 16 / Lk);
+        int pos = (int)(q * 16 - (int64_t)tok * Lk);
+        int l = pos / k, j = pos - l * k;
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+          set_bit(tok, l, (int)((v[u][c >> 2] >> (8 * (c & 3))) & 0xff));
+          if (++j == k) {
+            j = 0;
+            if (++l == L) {
+              l = 0;
+              ++tok;
+            }
+          }
+        }
+      }
+    }
+  }
+  for (int64_t q = npiece * 16 + tid; q < nbytes; q += kSel) {
+    const int tok = (int)(q / Lk), pos = (int)(q - (int64_t)tok * Lk);
+    set_bit(tok, pos / k, routes[q]);
+  }
+  int tot_all = 0;
+  (void)small_block_scan(my_ones, &tot_all, s_redi);  // its barriers publish bits and counts
+
+  // per token: sum over its columns of cnt[]; accumulated into out[] (zeroed)
+  auto col_sums = [&](const int* cnt, int* out) {
+    for (int q = tid; q < NW; q += kSel) {
+      const int lo = (q % W) * 64;
+      int sum = 0;
+      for (uint64_t x = bits[q]; x; x &= x - 1) sum += cnt[lo + __builtin_ctzll(x)];
+      if (sum) atomicAdd(&out[q / W], sum);
+    }
+  };
+  col_sums(cnt_all, sall);
+
+  // signature order: bitonic sort of (key, token), one element per thread.
+  // The key is word 0 bit-reversed and inverted, so ascending keys follow the
+  // lowest-differing-bit rule on word 0; equal keys compare the later words
+  // the same way, then the index. Padding (token -1) sorts last.
+  int NP = 1;
+  while (NP < N) NP <<= 1;
+  auto before = [&](uint64_t ka, int ta, uint64_t kb, int tb) {
+    if (ta < 0) return false;
+    if (tb < 0) return true;
+    if (ka != kb) return ka < kb;
+    for (int w = 1; w < W; ++w) {
+      const uint64_t x = bits[ta * W + w] ^ bits[tb * W + w];
+      if (x) return (bits[ta * W + w] & lowbit(x)) != 0;
+    }
+    return ta < tb;
+  };
+  uint64_t key = ~0ull;
+  int tk = -1;
+  if (tid < N) {
+    key = ~__builtin_bitreverse64(bits[tid * W]);
+    tk = tid;
+  }
+  for (int kk = 2; kk <= NP; kk <<= 1)
+    for (int j = kk >> 1; j > 0; j >>= 1) {
+      uint64_t pk;
+      int pt;
+      if (j < kWave) {
+        pk = __shfl_xor(key, j, kWave);
+        pt = __shfl_xor(tk, j, kWave);
+      } else {                                   // NP >= 128 here
+        if (tid < NP) {
+          skey[tid] = key;
+          stok[tid] = tk;
+        }
+        __syncthreads();
+        pk = tid < NP ? skey[tid ^ j] : key;
+        pt = tid < NP ? stok[tid ^ j] : tk;
+        __syncthreads();
+      }
+      // the lower position of an ascending pair keeps the element that comes first
+      const bool asc = (tid & kk) == 0, low = (tid & j) == 0;
+      const bool pfirst = before(pk, pt, key, tk);
+      if (asc == low ? pfirst : !pfirst) {
+        key = pk;
+        tk = pt;
+      }
+    }
+  if (tid < N) {
+    idx[tid] = tk;
+    rank[tk] = tid;
+  }
+  __syncthreads();
+
+  // m1: least total distance; m2: farthest from m1 (ties to the lower rank)
+  auto pack = [](int64_t v, int r) { return ((uint32_t)v << kSmallRankBits) | (uint32_t)r; };
+  uint32_t c1 = ~0u, c2 = ~0u;
+  for (int i = tid; i < N; i += kSel)
+    c1 = min(c1, pack((int64_t)N * ones[i] + tot_all - 2 * (int64_t)sall[i], rank[i]));
+  small_block_min2(c1, c2, s_red);
+  int m1 = idx[c1 & (kSmallN - 1)];
+  for (int q = tid; q < NW; q += kSel) {
+    const int d = __popcll(bits[q] ^ bits[m1 * W + q % W]);
+    if (d) atomicAdd(&dbin[q / W], d);
+  }
+  __syncthreads();
+  c1 = ~0u;
+  c2 = ~0u;
+  for (int i = tid; i < N; i += kSel)
+    if (i != m1) c1 = min(c1, pack(2 * Lk - dbin[i], rank[i]));
+  small_block_min2(c1, c2, s_red);
+  int m2 = idx[c1 & (kSmallN - 1)];
+
+  const int off = 2 * Lk;                        // delta in [-2Lk, 2Lk]
+  int iters = 0, converged = 0, med0 = -1, med1 = -1;
+  for (int it = 1; it <= max_iters; ++it) {
+    iters = it;
+    for (int b = tid; b < nbins; b += kSel) hist[b] = 0;
+    for (int i = tid; i < N; i += kSel) {
+      dbin[i] = off;
+      s1[i] = 0;
+    }
+    for (int col = tid; col < LE; col += kSel) cnt1[col] = 0;
+    __syncthreads();
+    for (int q = tid; q < NW; q += kSel) {
+      const int w = q % W;
+      const uint64_t x = bits[q];
+      const int d = __popcll(x ^ bits[m1 * W + w]) - __popcll(x ^ bits[m2 * W + w]);
+      if (d) atomicAdd(&dbin[q / W], d);
+    }
+    __syncthreads();
+    for (int i = tid; i < N; i += kSel) atomicAdd(&hist[dbin[i]], 1);
+    __syncthreads();
+    // threshold bin t: fewer than n1 tokens lie below it, at least n1 up to it
+    const int per = (nbins + kSel - 1) / kSel;
+    const int b0 = min(nbins, tid * per), b1 = min(nbins, b0 + per);
+    int mine = 0;
+    for (int b = b0; b < b1; ++b) mine += hist[b];
+    int total = 0;
+    const int below = small_block_scan(mine, &total, s_redi);
+    if (below < n1 && below + mine >= n1) {
+      int cum = below;
+      for (int b = b0; b < b1; ++b) {
+        if (cum + hist[b] >= n1) {
+          s_t = b;
+          s_below = cum;
+          break;
+        }
+        cum += hist[b];
+      }
+    }
+    __syncthreads();
+    const int t = s_t, quota = n1 - s_below;
+    // ties at t go to batch 1 in signature order, up to the quota
+    const int tok = tid < N ? idx[tid] : -1;
+    const int tie = tok >= 0 && dbin[tok] == t ? 1 : 0;
+    const int tpos = small_block_scan(tie, &total, s_redi);
+    if (tok >= 0) in1[tok] = (dbin[tok] < t || (tie && tpos < quota)) ? 1 : 0;
+    __syncthreads();
+    int my1 = 0;
+    for (int q = tid; q < NW; q += kSel)
+      if (in1[q / W]) {
+        const int lo = (q % W) * 64;
+        uint64_t x = bits[q];
+        my1 += __popcll(x);
+        for (; x; x &= x - 1) atomicAdd(&cnt1[lo + __builtin_ctzll(x)], 1);
+      }
+    int tot1 = 0;
+    (void)small_block_scan(my1, &tot1, s_redi);   // its barriers publish cnt1
+    col_sums(cnt1, s1);
+    __syncthreads();
+    med0 = m1;
+    med1 = m2;
+    uint32_t a1 = ~0u, a2 = ~0u;
+    for (int i = tid; i < N; i += kSel) {
+      if (in1[i])
+        a1 = min(a1, pack((int64_t)n1 * ones[i] + tot1 - 2 * (int64_t)s1[i], rank[i]));
+      else
+        a2 = min(a2, pack((int64_t)(N - n1) * ones[i] + (tot_all - tot1) -
+                              2 * (int64_t)(sall[i] - s1[i]), rank[i]));
+    }
+    small_block_min2(a1, a2, s_red);
+    const int n1m = idx[a1 & (kSmallN - 1)];
+    const int n2m = idx[a2 & (kSmallN - 1)];
+    if (n1m == m1 && n2m == m2) {
+      converged = 1;
+      break;
+    }
+    m1 = n1m;
+    m2 = n2m;
+  }
+
+  // Eq. 2 before and after, the guard
+  int ob = 0, oa = 0;
+  for (int col = tid; col < LE; col += kSel) {
+    ob += (cnt_orig[col] > 0) + (cnt_all[col] - cnt_orig[col] > 0);
+    oa += (cnt1[col] > 0) + (cnt_all[col] - cnt1[col] > 0);
+  }
+  int obj_before = 0, obj_after = 0;
+  (void)small_block_scan(ob, &obj_before, s_redi);
+  (void)small_block_scan(oa, &obj_after, s_redi);
+  const bool use_orig = keep && obj_after > obj_before;
+  if (use_orig) obj_after = obj_before;
+
+  // perm: batch 1 in ascending index, then batch 2
+  const int f = tid < N ? (use_orig ? (tid < n1 ? 1 : 0) : in1[tid]) : 0;
+  int nb1 = 0;
+  const int pos = small_block_scan(f, &nb1, s_redi);
+  if (tid < N) perm[f ? pos : nb1 + (tid - pos)] = tid;
+  if (demand)
+    for (int col = tid; col < LE; col += kSel) {
+      const int c = use_orig ? cnt_orig[col] : cnt1[col];
+      demand[col] = c;
+      demand[LE + col] = cnt_all[col] - c;
+    }
+  if (tid == 0) {
+    info[0] = iters;
+    info[1] = converged;
+    info[2] = med0;
+    info[3] = med1;
+    info[4] = obj_before;
+    info[5] = obj_after;
+    info[6] = use_orig ? 1 : 0;
+    info[7] = n1;
+  }
+}
+
 struct SchLayout {
   size_t bits, bits_s, key0, key1, key2, skey0, skey1, skey2, sidx, part, ones, ones_s, rank, order, delta,
       in1, cnt, cnt_orig, hist, hpart, tot, state, cand, cand8, blkcnt, bar, total;
@@ -1245,6 +1649,19 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   do { if ((expr) != hipSuccess) return MOE_ERR_HIP; } while (0)
 
   const bool trivial = (n1 == 0 || n1 == N);
+  if (!trivial && N <= kSmallN && (int64_t)L * k < kSmallMaxLk) {
+    const size_t slds = small_lds((int)N, (int)W, (int)LE, nbins).total;
+    if (slds <= kSmallMaxLds &&
+        hipFuncSetAttribute(reinterpret_cast<const void*>(&sch_small),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)slds) == hipSuccess) {
+      sch_small<<<dim3(1), dim3(kSel), slds, st>>>(routes, (int)N, L, E, k, (int)W, (int)n1,
+                                                   max_iters, keep_original_if_worse, nbins, perm,
+                                                   demand, info);
+      MOE_CHECK_LAUNCH();
+      return MOE_OK;
+    }
+    (void)hipGetLastError();
+  }
 
   sch_init<<<dim3((unsigned)std::min<int64_t>(64, ceil_div(std::max(2 * nbins, 2 * LE), kT))), blk,
              0, st>>>(hist, 2 * nbins, cnt_orig, cnt, 2 * LE, tot, cand8, bar, err, state);
