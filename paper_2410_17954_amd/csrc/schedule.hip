@@ -1143,8 +1143,15 @@ constexpr int kSmallRankBits = 10;               // signature rank < kSmallN
 constexpr int kSmallMaxLk = 2048;                // sums < kSmallN * 2 L k fit 22 bits
 constexpr int kSmallPre = 8;                     // 16-byte route pieces in flight per thread
 constexpr size_t kSmallMaxLds = 140 * 1024;
+constexpr int kSmallBatch = 64;                  // nodes per launch (one block each)
 static_assert(kSmallN <= (1 << kSmallRankBits), "rank field");
 static_assert((int64_t)kSmallN * 2 * kSmallMaxLk <= (1ll << (32 - kSmallRankBits)), "sum field");
+
+// The nodes of one launch: block b splits the n[b] tokens at perm[lo[b] ...]
+// with n1[b] in batch 1 and writes info row row[b].
+struct SmallNodes {
+  int32_t lo[kSmallBatch], n[kSmallBatch], n1[kSmallBatch], row[kSmallBatch];
+};
 
 struct SmallLds {
   size_t bits, cnt_all, cnt1, cnt_orig, hist, idx, rank, ones, dbin, in1, sall, s1, skey, stok,
@@ -1245,14 +1252,27 @@ __device__ __forceinline__ int small_block_scan(int v, int* total, int* red) {
   return base + inc - v;
 }
 
+// ids_in == 0: token i of the node is routes row i, and perm[lo + j] receives
+// the node-local index of the token at position j of the split (batch 1, then
+// batch 2, each ascending). ids_in == 1: token i is routes row perm[lo + i],
+// and the same positions receive those row ids (the node's tokens reordered
+// in place). demand (single node only) and info may be null.
 __global__ void __launch_bounds__(kSel)
-sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W, int n1,
-          int max_iters, int keep, int nbins, int32_t* __restrict__ perm,
-          int32_t* __restrict__ demand, int64_t* __restrict__ info) {
+sch_small(const uint8_t* __restrict__ routes, const SmallNodes nodes, int ids_in, int L, int E,
+          int k, int W, int max_iters, int keep, int nbins, int32_t* __restrict__ perm,
+          int32_t* __restrict__ demand, int64_t* __restrict__ info_rows) {
   extern __shared__ __attribute__((aligned(16))) unsigned char s_lds[];
   __shared__ uint32_t s_red[2 * kSel / kWave];
   __shared__ int s_t, s_below;
-  const int LE = L * E, Lk = L * k, NW = N * W, tid = threadIdx.x;
+  const int tid = threadIdx.x;
+  const int N = nodes.n[blockIdx.x], n1 = nodes.n1[blockIdx.x], lo = nodes.lo[blockIdx.x];
+  int64_t* const info = info_rows ? info_rows + 8 * (int64_t)nodes.row[blockIdx.x] : nullptr;
+  if (N == 0) {                                  // an empty node: nothing to split
+    if (info && tid < 8) info[tid] = (tid == 1) ? 1 : (tid == 2 || tid == 3) ? -1 : 0;
+    return;
+  }
+  const bool trivial = n1 == 0 || n1 == N;
+  const int LE = L * E, Lk = L * k, NW = N * W;
   const SmallLds o = small_lds(N, W, LE, nbins);
   uint64_t* const bits = reinterpret_cast<uint64_t*>(s_lds + o.bits);
   uint32_t* const bits32 = reinterpret_cast<uint32_t*>(s_lds + o.bits);
@@ -1270,6 +1290,9 @@ sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
   uint64_t* const skey = reinterpret_cast<uint64_t*>(s_lds + o.skey);
   int* const stok = reinterpret_cast<int*>(s_lds + o.stok);
   int* const s_redi = reinterpret_cast<int*>(s_red);
+  int* const gid = s1;                           // routes row of each token until the rounds
+  const int my_id = tid < N ? (ids_in ? perm[lo + tid] : tid) : -1;
+  if (tid < N) gid[tid] = my_id;
 
   for (int q = tid; q < 2 * NW; q += kSel) bits32[q] = 0;
   for (int c = tid; c < LE; c += kSel) {
@@ -1296,21 +1319,36 @@ sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
     atomicAdd(&cnt_all[col], 1);
     if (tok < n1) atomicAdd(&cnt_orig[col], 1);
   };
+  // 16-byte pieces when rows allow it: the node's rows back to back (ids_in
+  // == 0), or whole rows of 16-byte multiples (ids_in == 1); else bytes
   const int64_t nbytes = (int64_t)N * Lk;
-  const int64_t npiece = (reinterpret_cast<uintptr_t>(routes) & 15) ? 0 : nbytes / 16;
+  const bool aligned = (reinterpret_cast<uintptr_t>(routes) & 15) == 0;
+  const int64_t npiece = !aligned ? 0 : !ids_in ? nbytes / 16 : (Lk % 16 == 0 ? nbytes / 16 : 0);
+  const int ppr = Lk / 16;                       // pieces per row (ids_in, Lk % 16 == 0)
+  auto piece_at = [&](int64_t q, int& tok, int& pos) -> const u32x4_t* {
+    if (!ids_in) {
+      tok = (int)(q * 16 / Lk);
+      pos = (int)(q * 16 - (int64_t)tok * Lk);
+      return reinterpret_cast<const u32x4_t*>(routes) + q;
+    }
+    tok = (int)(q / ppr);
+    pos = (int)(q - (int64_t)tok * ppr) * 16;
+    return reinterpret_cast<const u32x4_t*>(routes + (int64_t)gid[tok] * Lk + pos);
+  };
   for (int64_t q0 = 0; q0 < npiece; q0 += (int64_t)kSmallPre * kSel) {
     u32x4_t v[kSmallPre];
 #pragma unroll
     for (int u = 0; u < kSmallPre; ++u) {
       const int64_t q = q0 + (int64_t)u * kSel + tid;
-      if (q < npiece) v[u] = reinterpret_cast<const u32x4_t*>(routes)[q];
+      int tok, pos;
+      if (q < npiece) v[u] = *piece_at(q, tok, pos);
     }
 #pragma unroll
     for (int u = 0; u < kSmallPre; ++u) {
       const int64_t q = q0 + (int64_t)u * kSel + tid;
       if (q < npiece) {
-        int tok = (int)(q * 16 / Lk);
-        int pos = (int)(q * 16 - (int64_t)tok * Lk);
+        int tok, pos;
+        (void)piece_at(q, tok, pos);
         int l = pos / k, j = pos - l * k;
 #pragma unroll
         for (int c = 0; c < 16; ++c) {
@@ -1328,7 +1366,7 @@ sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
   }
   for (int64_t q = npiece * 16 + tid; q < nbytes; q += kSel) {
     const int tok = (int)(q / Lk), pos = (int)(q - (int64_t)tok * Lk);
-    set_bit(tok, pos / k, routes[q]);
+    set_bit(tok, pos / k, routes[(int64_t)gid[tok] * Lk + pos]);
   }
   int tot_all = 0;
   (void)small_block_scan(my_ones, &tot_all, s_redi);  // its barriers publish bits and counts
@@ -1344,155 +1382,162 @@ sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
   };
   col_sums(cnt_all, sall);
 
-  // signature order: bitonic sort of (key, token), one element per thread.
-  // The key is word 0 bit-reversed and inverted, so ascending keys follow the
-  // lowest-differing-bit rule on word 0; equal keys compare the later words
-  // the same way, then the index. Padding (token -1) sorts last.
-  int NP = 1;
-  while (NP < N) NP <<= 1;
-  auto before = [&](uint64_t ka, int ta, uint64_t kb, int tb) {
-    if (ta < 0) return false;
-    if (tb < 0) return true;
-    if (ka != kb) return ka < kb;
-    for (int w = 1; w < W; ++w) {
-      const uint64_t x = bits[ta * W + w] ^ bits[tb * W + w];
-      if (x) return (bits[ta * W + w] & lowbit(x)) != 0;
-    }
-    return ta < tb;
-  };
-  uint64_t key = ~0ull;
-  int tk = -1;
-  if (tid < N) {
-    key = ~__builtin_bitreverse64(bits[tid * W]);
-    tk = tid;
-  }
-  for (int kk = 2; kk <= NP; kk <<= 1)
-    for (int j = kk >> 1; j > 0; j >>= 1) {
-      uint64_t pk;
-      int pt;
-      if (j < kWave) {
-        pk = __shfl_xor(key, j, kWave);
-        pt = __shfl_xor(tk, j, kWave);
-      } else {                                   // NP >= 128 here
-        if (tid < NP) {
-          skey[tid] = key;
-          stok[tid] = tk;
-        }
-        __syncthreads();
-        pk = tid < NP ? skey[tid ^ j] : key;
-        pt = tid < NP ? stok[tid ^ j] : tk;
-        __syncthreads();
-      }
-      // the lower position of an ascending pair keeps the element that comes first
-      const bool asc = (tid & kk) == 0, low = (tid & j) == 0;
-      const bool pfirst = before(pk, pt, key, tk);
-      if (asc == low ? pfirst : !pfirst) {
-        key = pk;
-        tk = pt;
-      }
-    }
-  if (tid < N) {
-    idx[tid] = tk;
-    rank[tk] = tid;
-  }
-  __syncthreads();
-
-  // m1: least total distance; m2: farthest from m1 (ties to the lower rank)
-  auto pack = [](int64_t v, int r) { return ((uint32_t)v << kSmallRankBits) | (uint32_t)r; };
-  uint32_t c1 = ~0u, c2 = ~0u;
-  for (int i = tid; i < N; i += kSel)
-    c1 = min(c1, pack((int64_t)N * ones[i] + tot_all - 2 * (int64_t)sall[i], rank[i]));
-  small_block_min2(c1, c2, s_red);
-  int m1 = idx[c1 & (kSmallN - 1)];
-  for (int q = tid; q < NW; q += kSel) {
-    const int d = __popcll(bits[q] ^ bits[m1 * W + q % W]);
-    if (d) atomicAdd(&dbin[q / W], d);
-  }
-  __syncthreads();
-  c1 = ~0u;
-  c2 = ~0u;
-  for (int i = tid; i < N; i += kSel)
-    if (i != m1) c1 = min(c1, pack(2 * Lk - dbin[i], rank[i]));
-  small_block_min2(c1, c2, s_red);
-  int m2 = idx[c1 & (kSmallN - 1)];
-
-  const int off = 2 * Lk;                        // delta in [-2Lk, 2Lk]
-  int iters = 0, converged = 0, med0 = -1, med1 = -1;
-  for (int it = 1; it <= max_iters; ++it) {
-    iters = it;
-    for (int b = tid; b < nbins; b += kSel) hist[b] = 0;
-    for (int i = tid; i < N; i += kSel) {
-      dbin[i] = off;
-      s1[i] = 0;
-    }
-    for (int col = tid; col < LE; col += kSel) cnt1[col] = 0;
+  int iters = 0, converged = 1, med0 = -1, med1 = -1;
+  if (trivial) {                                 // one batch empty: the input split stands
+    for (int i = tid; i < N; i += kSel) in1[i] = i < n1 ? 1 : 0;
+    for (int col = tid; col < LE; col += kSel) cnt1[col] = cnt_orig[col];
     __syncthreads();
+  } else {
+    // signature order: bitonic sort of (key, token), one element per thread.
+    // The key is word 0 bit-reversed and inverted, so ascending keys follow the
+    // lowest-differing-bit rule on word 0; equal keys compare the later words
+    // the same way, then the index. Padding (token -1) sorts last.
+    int NP = 1;
+    while (NP < N) NP <<= 1;
+    auto before = [&](uint64_t ka, int ta, uint64_t kb, int tb) {
+      if (ta < 0) return false;
+      if (tb < 0) return true;
+      if (ka != kb) return ka < kb;
+      for (int w = 1; w < W; ++w) {
+        const uint64_t x = bits[ta * W + w] ^ bits[tb * W + w];
+        if (x) return (bits[ta * W + w] & lowbit(x)) != 0;
+      }
+      return ta < tb;
+    };
+    uint64_t key = ~0ull;
+    int tk = -1;
+    if (tid < N) {
+      key = ~__builtin_bitreverse64(bits[tid * W]);
+      tk = tid;
+    }
+    for (int kk = 2; kk <= NP; kk <<= 1)
+      for (int j = kk >> 1; j > 0; j >>= 1) {
+        uint64_t pk;
+        int pt;
+        if (j < kWave) {
+          pk = __shfl_xor(key, j, kWave);
+          pt = __shfl_xor(tk, j, kWave);
+        } else {                                   // NP >= 128 here
+          if (tid < NP) {
+            skey[tid] = key;
+            stok[tid] = tk;
+          }
+          __syncthreads();
+          pk = tid < NP ? skey[tid ^ j] : key;
+          pt = tid < NP ? stok[tid ^ j] : tk;
+          __syncthreads();
+        }
+        // the lower position of an ascending pair keeps the element that comes first
+        const bool asc = (tid & kk) == 0, low = (tid & j) == 0;
+        const bool pfirst = before(pk, pt, key, tk);
+        if (asc == low ? pfirst : !pfirst) {
+          key = pk;
+          tk = pt;
+        }
+      }
+    if (tid < N) {
+      idx[tid] = tk;
+      rank[tk] = tid;
+    }
+    __syncthreads();
+
+    // m1: least total distance; m2: farthest from m1 (ties to the lower rank)
+    auto pack = [](int64_t v, int r) { return ((uint32_t)v << kSmallRankBits) | (uint32_t)r; };
+    uint32_t c1 = ~0u, c2 = ~0u;
+    for (int i = tid; i < N; i += kSel)
+      c1 = min(c1, pack((int64_t)N * ones[i] + tot_all - 2 * (int64_t)sall[i], rank[i]));
+    small_block_min2(c1, c2, s_red);
+    int m1 = idx[c1 & (kSmallN - 1)];
     for (int q = tid; q < NW; q += kSel) {
-      const int w = q % W;
-      const uint64_t x = bits[q];
-      const int d = __popcll(x ^ bits[m1 * W + w]) - __popcll(x ^ bits[m2 * W + w]);
+      const int d = __popcll(bits[q] ^ bits[m1 * W + q % W]);
       if (d) atomicAdd(&dbin[q / W], d);
     }
     __syncthreads();
-    for (int i = tid; i < N; i += kSel) atomicAdd(&hist[dbin[i]], 1);
-    __syncthreads();
-    // threshold bin t: fewer than n1 tokens lie below it, at least n1 up to it
-    const int per = (nbins + kSel - 1) / kSel;
-    const int b0 = min(nbins, tid * per), b1 = min(nbins, b0 + per);
-    int mine = 0;
-    for (int b = b0; b < b1; ++b) mine += hist[b];
-    int total = 0;
-    const int below = small_block_scan(mine, &total, s_redi);
-    if (below < n1 && below + mine >= n1) {
-      int cum = below;
-      for (int b = b0; b < b1; ++b) {
-        if (cum + hist[b] >= n1) {
-          s_t = b;
-          s_below = cum;
-          break;
+    c1 = ~0u;
+    c2 = ~0u;
+    for (int i = tid; i < N; i += kSel)
+      if (i != m1) c1 = min(c1, pack(2 * Lk - dbin[i], rank[i]));
+    small_block_min2(c1, c2, s_red);
+    int m2 = idx[c1 & (kSmallN - 1)];
+
+    const int off = 2 * Lk;                        // delta in [-2Lk, 2Lk]
+    converged = 0;
+    for (int it = 1; it <= max_iters; ++it) {
+      iters = it;
+      for (int b = tid; b < nbins; b += kSel) hist[b] = 0;
+      for (int i = tid; i < N; i += kSel) {
+        dbin[i] = off;
+        s1[i] = 0;
+      }
+      for (int col = tid; col < LE; col += kSel) cnt1[col] = 0;
+      __syncthreads();
+      for (int q = tid; q < NW; q += kSel) {
+        const int w = q % W;
+        const uint64_t x = bits[q];
+        const int d = __popcll(x ^ bits[m1 * W + w]) - __popcll(x ^ bits[m2 * W + w]);
+        if (d) atomicAdd(&dbin[q / W], d);
+      }
+      __syncthreads();
+      for (int i = tid; i < N; i += kSel) atomicAdd(&hist[dbin[i]], 1);
+      __syncthreads();
+      // threshold bin t: fewer than n1 tokens lie below it, at least n1 up to it
+      const int per = (nbins + kSel - 1) / kSel;
+      const int b0 = min(nbins, tid * per), b1 = min(nbins, b0 + per);
+      int mine = 0;
+      for (int b = b0; b < b1; ++b) mine += hist[b];
+      int total = 0;
+      const int below = small_block_scan(mine, &total, s_redi);
+      if (below < n1 && below + mine >= n1) {
+        int cum = below;
+        for (int b = b0; b < b1; ++b) {
+          if (cum + hist[b] >= n1) {
+            s_t = b;
+            s_below = cum;
+            break;
+          }
+          cum += hist[b];
         }
-        cum += hist[b];
       }
-    }
-    __syncthreads();
-    const int t = s_t, quota = n1 - s_below;
-    // ties at t go to batch 1 in signature order, up to the quota
-    const int tok = tid < N ? idx[tid] : -1;
-    const int tie = tok >= 0 && dbin[tok] == t ? 1 : 0;
-    const int tpos = small_block_scan(tie, &total, s_redi);
-    if (tok >= 0) in1[tok] = (dbin[tok] < t || (tie && tpos < quota)) ? 1 : 0;
-    __syncthreads();
-    int my1 = 0;
-    for (int q = tid; q < NW; q += kSel)
-      if (in1[q / W]) {
-        const int lo = (q % W) * 64;
-        uint64_t x = bits[q];
-        my1 += __popcll(x);
-        for (; x; x &= x - 1) atomicAdd(&cnt1[lo + __builtin_ctzll(x)], 1);
+      __syncthreads();
+      const int t = s_t, quota = n1 - s_below;
+      // ties at t go to batch 1 in signature order, up to the quota
+      const int tok = tid < N ? idx[tid] : -1;
+      const int tie = tok >= 0 && dbin[tok] == t ? 1 : 0;
+      const int tpos = small_block_scan(tie, &total, s_redi);
+      if (tok >= 0) in1[tok] = (dbin[tok] < t || (tie && tpos < quota)) ? 1 : 0;
+      __syncthreads();
+      int my1 = 0;
+      for (int q = tid; q < NW; q += kSel)
+        if (in1[q / W]) {
+          const int lo = (q % W) * 64;
+          uint64_t x = bits[q];
+          my1 += __popcll(x);
+          for (; x; x &= x - 1) atomicAdd(&cnt1[lo + __builtin_ctzll(x)], 1);
+        }
+      int tot1 = 0;
+      (void)small_block_scan(my1, &tot1, s_redi);   // its barriers publish cnt1
+      col_sums(cnt1, s1);
+      __syncthreads();
+      med0 = m1;
+      med1 = m2;
+      uint32_t a1 = ~0u, a2 = ~0u;
+      for (int i = tid; i < N; i += kSel) {
+        if (in1[i])
+          a1 = min(a1, pack((int64_t)n1 * ones[i] + tot1 - 2 * (int64_t)s1[i], rank[i]));
+        else
+          a2 = min(a2, pack((int64_t)(N - n1) * ones[i] + (tot_all - tot1) -
+                                2 * (int64_t)(sall[i] - s1[i]), rank[i]));
       }
-    int tot1 = 0;
-    (void)small_block_scan(my1, &tot1, s_redi);   // its barriers publish cnt1
-    col_sums(cnt1, s1);
-    __syncthreads();
-    med0 = m1;
-    med1 = m2;
-    uint32_t a1 = ~0u, a2 = ~0u;
-    for (int i = tid; i < N; i += kSel) {
-      if (in1[i])
-        a1 = min(a1, pack((int64_t)n1 * ones[i] + tot1 - 2 * (int64_t)s1[i], rank[i]));
-      else
-        a2 = min(a2, pack((int64_t)(N - n1) * ones[i] + (tot_all - tot1) -
-                              2 * (int64_t)(sall[i] - s1[i]), rank[i]));
+      small_block_min2(a1, a2, s_red);
+      const int n1m = idx[a1 & (kSmallN - 1)];
+      const int n2m = idx[a2 & (kSmallN - 1)];
+      if (n1m == m1 && n2m == m2) {
+        converged = 1;
+        break;
+      }
+      m1 = n1m;
+      m2 = n2m;
     }
-    small_block_min2(a1, a2, s_red);
-    const int n1m = idx[a1 & (kSmallN - 1)];
-    const int n2m = idx[a2 & (kSmallN - 1)];
-    if (n1m == m1 && n2m == m2) {
-      converged = 1;
-      break;
-    }
-    m1 = n1m;
-    m2 = n2m;
   }
 
   // Eq. 2 before and after, the guard
@@ -1511,14 +1556,14 @@ sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
   const int f = tid < N ? (use_orig ? (tid < n1 ? 1 : 0) : in1[tid]) : 0;
   int nb1 = 0;
   const int pos = small_block_scan(f, &nb1, s_redi);
-  if (tid < N) perm[f ? pos : nb1 + (tid - pos)] = tid;
+  if (tid < N) perm[lo + (f ? pos : nb1 + (tid - pos))] = my_id;
   if (demand)
     for (int col = tid; col < LE; col += kSel) {
       const int c = use_orig ? cnt_orig[col] : cnt1[col];
       demand[col] = c;
       demand[LE + col] = cnt_all[col] - c;
     }
-  if (tid == 0) {
+  if (info && tid == 0) {
     info[0] = iters;
     info[1] = converged;
     info[2] = med0;
@@ -1528,6 +1573,29 @@ sch_small(const uint8_t* __restrict__ routes, int N, int L, int E, int k, int W,
     info[6] = use_orig ? 1 : 0;
     info[7] = n1;
   }
+}
+
+// LDS bytes of the one-block path for a node of n tokens, 0 if it does not
+// take that path.
+inline size_t small_fit(int64_t n, int L, int E, int k) {
+  if (n > kSmallN || (int64_t)L * k >= kSmallMaxLk) return 0;
+  const size_t b = small_lds((int)n, (L * E + 63) / 64, L * E, 4 * L * k + 1).total;
+  return b <= kSmallMaxLds ? b : 0;
+}
+
+// sch_small over the first `count` nodes of the table (lds: the largest
+// small_fit among them).
+inline hipError_t small_launch(const uint8_t* routes, const SmallNodes& nodes, int count,
+                               int ids_in, int L, int E, int k, int max_iters, int keep,
+                               size_t lds, int32_t* perm, int32_t* demand, int64_t* info,
+                               hipStream_t st) {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&sch_small),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  sch_small<<<dim3(count), dim3(kSel), lds, st>>>(routes, nodes, ids_in, L, E, k,
+                                                  (L * E + 63) / 64, max_iters, keep,
+                                                  4 * L * k + 1, perm, demand, info);
+  return hipGetLastError();
 }
 
 struct SchLayout {
@@ -1649,18 +1717,14 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
   do { if ((expr) != hipSuccess) return MOE_ERR_HIP; } while (0)
 
   const bool trivial = (n1 == 0 || n1 == N);
-  if (!trivial && N <= kSmallN && (int64_t)L * k < kSmallMaxLk) {
-    const size_t slds = small_lds((int)N, (int)W, (int)LE, nbins).total;
-    if (slds <= kSmallMaxLds &&
-        hipFuncSetAttribute(reinterpret_cast<const void*>(&sch_small),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)slds) == hipSuccess) {
-      sch_small<<<dim3(1), dim3(kSel), slds, st>>>(routes, (int)N, L, E, k, (int)W, (int)n1,
-                                                   max_iters, keep_original_if_worse, nbins, perm,
-                                                   demand, info);
-      MOE_CHECK_LAUNCH();
+  if (const size_t slds = small_fit(N, L, E, k)) {
+    SmallNodes one{};
+    one.n[0] = (int32_t)N;
+    one.n1[0] = (int32_t)n1;
+    if (small_launch(routes, one, 1, 0, L, E, k, max_iters, keep_original_if_worse, slds, perm,
+                     demand, info, st) == hipSuccess)
       return MOE_OK;
-    }
-    (void)hipGetLastError();
+    (void)hipGetLastError();                     // nothing ran: take the general path
   }
 
   sch_init<<<dim3((unsigned)std::min<int64_t>(64, ceil_div(std::max(2 * nbins, 2 * LE), kT))), blk,
@@ -1783,12 +1847,12 @@ constexpr int32_t kMaxMultiBatches = 4096;
 
 struct MultiNode {
   int64_t lo, n;
-  int32_t b;
+  int32_t b, depth;
 };
 
 // Nodes of the recursion in pre-order (sizes depend on N and B only).
 std::vector<MultiNode> multi_nodes(int64_t N, int32_t B) {
-  std::vector<MultiNode> out, stack{{0, N, B}};
+  std::vector<MultiNode> out, stack{{0, N, B, 0}};
   while (!stack.empty()) {
     const MultiNode v = stack.back();
     stack.pop_back();
@@ -1796,8 +1860,8 @@ std::vector<MultiNode> multi_nodes(int64_t N, int32_t B) {
     out.push_back(v);
     const int32_t bl = v.b / 2;
     const int64_t n1 = v.n * bl / v.b;
-    stack.push_back({v.lo + n1, v.n - n1, v.b - bl});   // right after left
-    stack.push_back({v.lo, n1, bl});
+    stack.push_back({v.lo + n1, v.n - n1, v.b - bl, v.depth + 1});   // right after left
+    stack.push_back({v.lo, n1, bl, v.depth + 1});
   }
   return out;
 }
@@ -1989,20 +2053,12 @@ extern "C" int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, i
 
   sch_multi_iota<<<dim3((unsigned)ceil_div(N, 256)), dim3(256), 0, st>>>(N, perm);
   MOE_CHECK_LAUNCH();
-  const std::vector<MultiNode> nodes = multi_nodes(N, B);
-  for (size_t q = 0; q < nodes.size(); ++q) {
-    const MultiNode& v = nodes[q];
+  // one node through the general two-way path: its routes gathered, split,
+  // its range of perm composed with the split's order
+  auto multi_split = [&](const MultiNode& v, size_t q) -> int {
     int64_t* const info_row = info ? info + 8 * (int64_t)q : info_scratch;
-    if (v.n == 0) {
-      if (info) {
-        sch_multi_info_empty<<<dim3(1), dim3(64), 0, st>>>(info_row);
-        MOE_CHECK_LAUNCH();
-      }
-      continue;
-    }
     int32_t* const ids = perm + v.lo;
-    const int32_t bl = v.b / 2;
-    const int64_t n1 = v.n * bl / v.b;
+    const int64_t n1 = v.n * (v.b / 2) / v.b;
     sch_multi_gather<<<dim3((unsigned)ceil_div(v.n * row, 256)), dim3(256), 0, st>>>(
         routes, ids, v.n, row, rt);
     MOE_CHECK_LAUNCH();
@@ -2014,6 +2070,55 @@ extern "C" int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, i
     MOE_CHECK_LAUNCH();
     sch_multi_copy<<<g, dim3(256), 0, st>>>(tmp, v.n, ids);
     MOE_CHECK_LAUNCH();
+    return MOE_OK;
+  };
+  // The nodes of one depth are disjoint ranges of perm, each depending only
+  // on its parent: a level's nodes that fit the one-block path run as one
+  // launch (a block per node, tokens reordered in place), the others one
+  // after another.
+  const std::vector<MultiNode> nodes = multi_nodes(N, B);
+  int32_t depth_max = 0;
+  for (const MultiNode& v : nodes) depth_max = std::max(depth_max, v.depth);
+  for (int32_t d = 0; d <= depth_max && !nodes.empty(); ++d) {
+    SmallNodes tab{};
+    int count = 0;
+    size_t lds = 0;
+    auto flush = [&]() -> int {
+      if (count == 0) return MOE_OK;
+      if (small_launch(routes, tab, count, 1, L, E, k, max_iters, keep_original_if_worse, lds,
+                       perm, nullptr, info, st) != hipSuccess)
+        return MOE_ERR_HIP;
+      count = 0;
+      lds = 0;
+      return MOE_OK;
+    };
+    for (size_t q = 0; q < nodes.size(); ++q) {
+      const MultiNode& v = nodes[q];
+      if (v.depth != d) continue;
+      if (const size_t b = small_fit(v.n, L, E, k)) {
+        tab.lo[count] = (int32_t)v.lo;
+        tab.n[count] = (int32_t)v.n;
+        tab.n1[count] = (int32_t)(v.n * (v.b / 2) / v.b);
+        tab.row[count] = (int32_t)q;
+        lds = std::max(lds, b);
+        if (++count == kSmallBatch) {
+          const int rc = flush();
+          if (rc != MOE_OK) return rc;
+        }
+        continue;
+      }
+      if (v.n == 0) {                            // an empty node: its info row only
+        if (info) {
+          sch_multi_info_empty<<<dim3(1), dim3(64), 0, st>>>(info + 8 * (int64_t)q);
+          MOE_CHECK_LAUNCH();
+        }
+        continue;
+      }
+      const int rc = multi_split(v, q);
+      if (rc != MOE_OK) return rc;
+    }
+    const int rc = flush();
+    if (rc != MOE_OK) return rc;
   }
   sch_multi_offsets<<<dim3((unsigned)ceil_div(B + 1, 256)), dim3(256), 0, st>>>(N, B,
                                                                               batch_offsets);

@@ -165,3 +165,39 @@ def test_multi_way_demand_too_large_for_lds():
     # 70 layers x 256 experts: the per-batch demand counts go straight to memory
     routes = synth.predicted_routes(300, 70, 256, 2, 0.7, 1.0, seed=54)
     _check_multi(routes, 256, 3)
+
+
+def test_multi_way_many_small_nodes_per_level():
+    # 200 batches of 15 tokens: the deepest levels hold more than 64 nodes,
+    # each level's small nodes run as several launches of one block per node
+    routes = synth.predicted_routes(3000, 4, 16, 2, 0.7, 1.0, seed=55)
+    _check_multi(routes, 16, 200)
+
+
+def test_multi_way_level_mixing_small_and_large_nodes():
+    # 2300 tokens into 5 batches: the first level holds a 920-token node (one
+    # block) beside a 1380-token node (general path); rows of 16 bytes
+    routes = synth.predicted_routes(2300, 8, 64, 2, 0.7, 1.0, seed=56)
+    _check_multi(routes, 64, 5)
+
+
+def test_unaligned_routes():
+    # routes starting one byte past an aligned address: byte loads throughout
+    import torch
+    N, L, E, k = 300, 8, 64, 2
+    routes = np.ascontiguousarray(synth.predicted_routes(N, L, E, k, 0.7, 1.0, seed=57),
+                                  dtype=np.uint8)
+    buf = torch.empty(N * L * k + 1, dtype=torch.uint8, device="cuda:0")
+    rt = buf[1:].view(N, L, k)
+    rt.copy_(torch.from_numpy(routes))
+    assert rt.data_ptr() % 16 != 0
+    perm, demand, info = ops.schedule(rt, E)
+    rp, rd, ri = oracle.schedule(routes, E)
+    assert to_host(info).tolist() == ri.tolist()
+    assert np.array_equal(to_host(perm), rp)
+    assert np.array_equal(to_host(demand), rd)
+    perm, off, demand, info = ops.schedule_multi(rt, E, 6)
+    rp, ro, rd, ri = oracle.schedule_multi(routes, E, 6)
+    assert to_host(info).tolist() == ri.tolist()
+    assert np.array_equal(to_host(perm), rp)
+    assert np.array_equal(to_host(demand), rd)
