@@ -21,9 +21,11 @@
 //            they repeat or max_iters rounds
 //   finish   Eq. 2 before/after from the column counts, the optional guard,
 //            perm by stable compaction, demand, info.
-// All ties go to the lower signature rank. The rounds run in one cooperative
-// launch over tokens laid out in signature order (a per-phase launch sequence
-// covers shapes beyond its limits); nothing is read back to the host.
+// All ties go to the lower signature rank. Up to 1024 tokens whose paths fit
+// in LDS run every step in one block (sch_small); otherwise the rounds run in
+// one cooperative launch over tokens laid out in signature order (a per-phase
+// launch sequence covers shapes beyond its limits). Nothing is read back to
+// the host.
 #include "common.h"
 
 #include <algorithm>
@@ -1838,8 +1840,8 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
 // node holds n tokens (a range of perm) bound for b batches; b == 1 is a batch,
 // otherwise the node's tokens, in their current order, are split with
 // n1 = n * (b / 2) / b and the two halves recurse into b / 2 and b - b / 2
-// batches. The host walks the tree in pre-order (the order of info's rows);
-// every step on the data is a kernel on the caller's stream.
+// batches. Info rows follow the tree's pre-order; the host walks it level by
+// level, and every step on the data is a kernel on the caller's stream.
 namespace moe {
 namespace {
 
