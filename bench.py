@@ -62,6 +62,10 @@ def parse():
                    help="instead of the layer throughput, time the routing path predictor's "
                         "forward pass (16 sequences of 512 tokens, hidden 32, FFN 2048, random "
                         "weights) with Mixtral-shaped and Qwen-shaped heads")
+    p.add_argument("--sched-sweep", action="store_true",
+                   help="instead of the layer throughput, time the two-way token scheduler on "
+                        "Mixtral-shaped 32-layer predicted routes from 1024 to 2^20 tokens: "
+                        "us per call, Eq. 2 before and after, effective GB/s")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 counter_collection.csv files (FETCH_SIZE, "
                         "WRITE_SIZE) of a --copy-probe-mib run into the traffic file, then exit")
@@ -368,6 +372,61 @@ def ways_report(args):
     print(json.dumps(rec))
 
 
+def sched_sweep_report(args):
+    """Two-way token scheduler (moe_schedule) from 1024 to 2^20 tokens on
+    Mixtral-shaped predicted routes (32 layers, 8 experts, top-2; the first N
+    tokens of one 2^20-token draw), n1 = N / 2. Per size: the call's time (HIP
+    events, median of 5 after 2 warm-ups, launches queued behind a short wait),
+    rounds, Eq. 2 before and after, and an effective rate over the bytes the
+    algorithm must move: one read of the routes, one write of perm, and
+    (5 + 3 * rounds) passes over the packed paths (their write, the signature
+    order, the input split's counts, m1, m2, then per round the deltas, the
+    batch-1 counts and the centroid sums). One JSON line."""
+    import torch
+    from paper_2410_17954_amd import ops, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.config(3)
+    L, E, k = cfg["L"], cfg["E"], cfg["k"]
+    W = (L * E + 63) // 64
+    Nmax = 1 << 20
+    routes = synth.predicted_routes(Nmax, L, E, k, cfg["keep"], cfg["zipf"], args.seed)
+    rt_all = torch.from_numpy(np.ascontiguousarray(routes, dtype=np.uint8)).to(dev)
+    out = []
+    for lg in (10, 12, 13, 14, 16, 18, 20):
+        N = 1 << lg
+        rt = rt_all[:N]
+        ws = ops.workspace_tensor(ops.schedule_workspace(N, L, E, k), dev)
+        perm = torch.empty(N, dtype=torch.int32, device=dev)
+        demand = torch.empty((2, L, E), dtype=torch.int32, device=dev)
+        info = torch.empty(8, dtype=torch.int64, device=dev)
+        ts = []
+        for rep in range(2 + 5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(1000000)
+            e0.record()
+            ops.schedule(rt, E, perm=perm, demand=demand, info=info, workspace=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            if rep >= 2:
+                ts.append(e0.elapsed_time(e1))
+        ms = float(np.median(ts))
+        inf = info.cpu().numpy()
+        iters = int(inf[0])
+        nbytes = N * L * k + 4 * N + (5 + 3 * iters) * N * W * 8
+        out.append({"tokens": N, "us": round(ms * 1e3, 1), "rounds": iters,
+                    "converged": int(inf[1]), "obj_before": int(inf[4]),
+                    "obj_after": int(inf[5]), "used_original": int(inf[6]),
+                    "algorithmic_MB": round(nbytes / 1e6, 3),
+                    "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                    "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)})
+    rec = {"metric": "two-way token scheduling: time per call and effective bandwidth by size",
+           "config": {"workload": f"Mixtral-shaped predicted routes: L={L}, E={E}, top-{k}, "
+                                  f"keep {cfg['keep']}, zipf {cfg['zipf']}; n1 = N / 2"},
+           "steps": out, "data": "synthetic"}
+    print(json.dumps(rec))
+
+
 def stack_report(args):
     """Dual-batch pipeline over a stack of MoE layers (one JSON line).
 
@@ -534,6 +593,9 @@ def main():
     if args.stack:
         stack_report(args)
         return
+    if args.sched_sweep:
+        sched_sweep_report(args)
+        return
     if args.rpp:
         rpp_report(args)
         return
@@ -629,21 +691,40 @@ def main():
     def span(ev, a, b):
         return ev[a].elapsed_time(ev[b])
 
-    st = {n: 0.0 for n in stage_names}
-    ffn_launch_ms = []
-    for ev in events:
-        st["schedule"] += span(ev, 0, 1)
-        st["route"] += span(ev, 1, 2)
+    def stage_ms(ev, ffn_launch_ms=None):
+        t = {n: 0.0 for n in stage_names}
+        t["schedule"] = span(ev, 0, 1)
+        t["route"] = span(ev, 1, 2)
         prev = 2
         for b in range(2):
             base = 3 + 3 * b
-            st["permute"] += span(ev, prev, base)
+            t["permute"] += span(ev, prev, base)
             d = span(ev, base, base + 1)
-            st["expert_ffn"] += d
-            ffn_launch_ms.append(d)
-            st["combine"] += span(ev, base + 1, base + 2)
+            t["expert_ffn"] += d
+            if ffn_launch_ms is not None:
+                ffn_launch_ms.append(d)
+            t["combine"] += span(ev, base + 1, base + 2)
             prev = base + 2
-    st = {n: v / K for n, v in st.items()}
+        return t
+
+    ffn_launch_ms = []
+    per_step = [stage_ms(ev, ffn_launch_ms) for ev in events]
+    st = {n: sum(t[n] for t in per_step) / K for n in stage_names}
+
+    # Outside the timed region: the same step with every cache cold (a 512 MB
+    # write before each step evicts the last-level cache), launches queued
+    # behind a short wait so that host time is not counted; median of 5.
+    flush = torch.empty(512 * 2 ** 20 // 4, dtype=torch.float32, device=dev)
+    cold = []
+    for rep in range(5):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(9)]
+        torch.cuda._sleep(3000000)
+        flush.fill_(float(rep))
+        step(ev)
+        torch.cuda.synchronize()
+        cold.append(stage_ms(ev))
+    st_cold = {n: float(np.median([t[n] for t in cold])) for n in stage_names}
+    del flush
 
     ceilings = measured_ceilings(torch, ops, dev)
 
@@ -709,6 +790,7 @@ def main():
             "flop_per_launch": ffn_flops, "launch_ms": ffn_ms,
         },
         "stages": stages,
+        "stages_cold_ms": {n: round(v, 4) for n, v in st_cold.items()},
         "measured_ceilings": ceilings,
         "setup_s": gen_s,
     }

@@ -315,6 +315,125 @@ sch_rank_sum(const int32_t* __restrict__ part, int ngroups, int N, int32_t* __re
   if (r < N) order[r] = i;                        // always: the chunk counts add up to a permutation
 }
 
+// Merge passes for large N (the rank above costs N lower bounds per chunk):
+// sorted runs of R tokens become runs of 2R. Block b writes outputs
+// [b T, b T + T) of the pass, T = min(kMergeTile, 2R) so that a block stays
+// inside one pair of runs. Two threads find where the block's first and
+// one-past-last outputs split the pair (merge path: a binary search along the
+// diagonal), the two pieces are staged in LDS, and each thread merges T / 256
+// consecutive outputs after the same search inside LDS.
+constexpr int kMergeTile = 2048;
+constexpr int kMergeBT = 256;
+constexpr int kMergeRankMaxChunks = 256;         // beyond: merge passes
+
+__device__ __forceinline__ SKey skey_at(const uint64_t* __restrict__ s0,
+                                        const uint64_t* __restrict__ s1,
+                                        const uint64_t* __restrict__ s2,
+                                        const int32_t* __restrict__ si, int64_t p) {
+  return SKey{s0[p], s1[p], s2[p], si[p]};
+}
+
+__global__ void __launch_bounds__(kMergeBT)
+sch_merge_pass(const uint64_t* __restrict__ s0, const uint64_t* __restrict__ s1,
+               const uint64_t* __restrict__ s2, const int32_t* __restrict__ si,
+               const uint64_t* __restrict__ bits, int N, int W, int R, uint64_t* __restrict__ d0,
+               uint64_t* __restrict__ d1, uint64_t* __restrict__ d2, int32_t* __restrict__ di) {
+  __shared__ uint64_t a0[kMergeTile], a1[kMergeTile], a2[kMergeTile];
+  __shared__ int32_t ai[kMergeTile];
+  __shared__ int32_t s_src[kMergeTile];          // merged order: staged position per output
+  __shared__ int s_lo[2], s_hi[2], s_cut[2];
+  const int tid = threadIdx.x;
+  const int T = min(kMergeTile, 2 * R);
+  const int o0 = blockIdx.x * T;                 // first output of the block
+  const int ps = o0 / (2 * R) * (2 * R);         // the pair's first position
+  const int nA = min(R, N - ps);
+  const int nB = max(0, min(R, N - ps - R));
+  const int aS = ps, bS = ps + nA;
+  const int dbeg = o0 - ps, dend = min(dbeg + T, nA + nB);
+  // The split of diagonal d is the first a in [max(0, d - nB), min(d, nA)]
+  // with !(A[a] < B[d - 1 - a]) (the end if none). Threads 0..127 search
+  // diagonal dbeg, 128..255 dend: each round probes 128 evenly spaced a and
+  // keeps the gap between the last true and the first false probe.
+  static_assert(kMergeBT == 256, "two groups of 128 probes");
+  if (tid < 2) {
+    const int d = tid ? dend : dbeg;
+    s_lo[tid] = max(0, d - nB);
+    s_hi[tid] = min(d, nA);
+  }
+  __syncthreads();
+  const int g = tid >> 7, t = tid & 127;
+  const int dg = g ? dend : dbeg;
+  while (s_lo[0] < s_hi[0] || s_lo[1] < s_hi[1]) {   // the same values in every thread
+    const int lo = s_lo[g], hi = s_hi[g], len = hi - lo;
+    if (tid < 2) s_cut[tid] = 128;
+    __syncthreads();
+    if (len > 0) {
+      const int a = lo + (int)(((int64_t)t * len) >> 7);
+      if (!key_less(skey_at(s0, s1, s2, si, aS + a), skey_at(s0, s1, s2, si, bS + dg - 1 - a),
+                    bits, W, N))
+        atomicMin(&s_cut[g], t);
+    }
+    __syncthreads();
+    if (len > 0 && t == 0) {
+      const int c = s_cut[g];
+      s_lo[g] = c == 0 ? lo : lo + (int)(((int64_t)(c - 1) * len) >> 7) + 1;
+      s_hi[g] = c == 128 ? hi : lo + (int)(((int64_t)c * len) >> 7);
+    }
+    __syncthreads();
+  }
+  const int ja0 = s_lo[0];
+  const int na = s_lo[1] - ja0;                  // A elements in the tile, then B
+  const int tot = dend - dbeg;
+  const int nb = tot - na;
+  const int jb0 = dbeg - ja0;
+  for (int p = threadIdx.x; p < tot; p += kMergeBT) {
+    const int g = p < na ? aS + ja0 + p : bS + jb0 + (p - na);
+    a0[p] = s0[g];
+    a1[p] = s1[g];
+    a2[p] = s2[g];
+    ai[p] = si[g];
+  }
+  __syncthreads();
+  auto at = [&](int p) { return SKey{a0[p], a1[p], a2[p], ai[p]}; };
+  const int per = T / kMergeBT;
+  const int t0 = threadIdx.x * per;
+  if (t0 < tot) {
+    int lo = max(0, t0 - nb), hi = min(t0, na);
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (key_less(at(mid), at(na + t0 - 1 - mid), bits, W, N))
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    int ia = lo, ib = t0 - lo;
+    for (int u = 0; u < per && t0 + u < tot; ++u) {
+      const bool take_a = ib >= nb || (ia < na && key_less(at(ia), at(na + ib), bits, W, N));
+      s_src[t0 + u] = take_a ? ia++ : na + ib++;
+    }
+  }
+  __syncthreads();
+  // the tile's outputs in order: coalesced stores
+  for (int p = threadIdx.x; p < tot; p += kMergeBT) {
+    const int src = s_src[p];
+    d0[o0 + p] = a0[src];
+    d1[o0 + p] = a1[src];
+    d2[o0 + p] = a2[src];
+    di[o0 + p] = ai[src];
+  }
+}
+
+// rank[order[r]] = r from the fully sorted token ids.
+__global__ void __launch_bounds__(kT)
+sch_rank_sorted(const int32_t* __restrict__ sorted, int N, int32_t* __restrict__ rank,
+                int32_t* __restrict__ order) {
+  const int r = blockIdx.x * kT + threadIdx.x;
+  if (r >= N) return;
+  const int i = sorted[r];
+  order[r] = i;
+  rank[i] = r;
+}
+
 // Paths and path sizes in signature order, word-major: bits_s[w][r] is word w
 // of the token at signature position r.
 __global__ void __launch_bounds__(kT)
@@ -541,7 +660,7 @@ constexpr int kCoopT = 256;
 constexpr int kCoopMaxLE = 8192;
 constexpr int kCoopMaxBins = 4096;
 constexpr int kCoopMaxBlocks = 1024;
-constexpr int kCoopMaxPPT = 4;
+constexpr int kCoopMaxPPT = 16;
 constexpr size_t kCoopMaxLds = 160 * 1024 - 2048;   // dynamic LDS limit (static part aside)
 constexpr unsigned kSpinBound = 1u << 20;
 
@@ -1747,11 +1866,30 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
     sch_sort_chunks<<<dim3(nchunks), dim3(kSortT), 0, st>>>(key0, key1, key2, bits, n, W, skey0,
                                                             skey1, skey2, sidx);
     MOE_CHECK_LAUNCH();
-    sch_merge_rank<<<dim3((unsigned)ceil_div(N, kMergeT), ngroups), dim3(kMergeT), 0, st>>>(
-        key0, key1, key2, bits, n, W, nchunks, skey0, skey1, skey2, sidx, part);
-    MOE_CHECK_LAUNCH();
-    sch_rank_sum<<<grid, blk, 0, st>>>(part, ngroups, n, rank, order);
-    MOE_CHECK_LAUNCH();
+    if (nchunks <= kMergeRankMaxChunks) {
+      sch_merge_rank<<<dim3((unsigned)ceil_div(N, kMergeT), ngroups), dim3(kMergeT), 0, st>>>(
+          key0, key1, key2, bits, n, W, nchunks, skey0, skey1, skey2, sidx, part);
+      MOE_CHECK_LAUNCH();
+      sch_rank_sum<<<grid, blk, 0, st>>>(part, ngroups, n, rank, order);
+      MOE_CHECK_LAUNCH();
+    } else {
+      // merge passes, ping-ponging between the sorted keys and the (now
+      // unused) unsorted keys with part as the id buffer
+      uint64_t *a0 = skey0, *a1 = skey1, *a2 = skey2, *b0 = key0, *b1 = key1, *b2 = key2;
+      int32_t *ai = sidx, *bi = part;
+      for (int64_t R = kChunk; R < N; R *= 2) {
+        const int64_t T = std::min<int64_t>(kMergeTile, 2 * R);
+        sch_merge_pass<<<dim3((unsigned)ceil_div(N, T)), dim3(kMergeBT), 0, st>>>(
+            a0, a1, a2, ai, bits, n, W, (int)R, b0, b1, b2, bi);
+        MOE_CHECK_LAUNCH();
+        std::swap(a0, b0);
+        std::swap(a1, b1);
+        std::swap(a2, b2);
+        std::swap(ai, bi);
+      }
+      sch_rank_sorted<<<grid, blk, 0, st>>>(ai, n, rank, order);
+      MOE_CHECK_LAUNCH();
+    }
     if (coop_shapes(N, L, E, k)) {
       sch_repack<<<grid, blk, 0, st>>>(bits, ones, order, n, W, bits_s, ones_s);
       MOE_CHECK_LAUNCH();
@@ -1760,7 +1898,7 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
           1, std::min<int64_t>({(int64_t)cus, ceil_div(N, kCoopT), (int64_t)kCoopMaxBlocks}));
       const int ppt = (int)ceil_div(ceil_div(N, nb), kCoopT);
       if (ppt <= kCoopMaxPPT) {
-        const int ppt_t = ppt <= 1 ? 1 : (ppt <= 2 ? 2 : 4);
+        const int ppt_t = ppt <= 1 ? 1 : ppt <= 2 ? 2 : ppt <= 4 ? 4 : ppt <= 8 ? 8 : 16;
         const int Lk = L * k;
         const bool bits_lds = coop_lds(LE, nbins, W, Lk, ppt_t, true, false).total <= kCoopMaxLds;
         const bool rt_lds = E <= 255 &&
@@ -1770,9 +1908,11 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
                     2 * L * k, bits_lds ? 1 : 0, rt_lds ? 1 : 0, E, k, Lk, L, in1, hist, hpart, cnt,
                     cnt_orig, tot, cand8, bar, err, state};
         void* args[] = {&ca};
-        const void* fn = ppt_t == 1 ? reinterpret_cast<const void*>(&sch_coop<1>)
+        const void* fn = ppt_t == 1   ? reinterpret_cast<const void*>(&sch_coop<1>)
                          : ppt_t == 2 ? reinterpret_cast<const void*>(&sch_coop<2>)
-                                      : reinterpret_cast<const void*>(&sch_coop<4>);
+                         : ppt_t == 4 ? reinterpret_cast<const void*>(&sch_coop<4>)
+                         : ppt_t == 8 ? reinterpret_cast<const void*>(&sch_coop<8>)
+                                      : reinterpret_cast<const void*>(&sch_coop<16>);
         if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) ==
                 hipSuccess &&
             hipLaunchCooperativeKernel(fn, dim3(nb), dim3(kCoopT), args, (unsigned)lds, st) ==

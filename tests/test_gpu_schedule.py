@@ -201,3 +201,72 @@ def test_unaligned_routes():
     assert to_host(info).tolist() == ri.tolist()
     assert np.array_equal(to_host(perm), rp)
     assert np.array_equal(to_host(demand), rd)
+
+
+def test_two_way_million_tokens_properties():
+    # 2^20 Mixtral-shaped tokens, beyond the oracle's reach: check what holds at
+    # any size. perm is batch 1 then batch 2, each ascending; demand is the
+    # batches' column counts; Eq. 2 before and after match them; the split is
+    # the balanced threshold of delta = d(i, m1) - d(i, m2); after convergence
+    # each medoid attains its batch's least distance sum.
+    N, L, E, k = 1 << 20, 32, 8, 2
+    base = synth.predicted_routes(1 << 17, L, E, k, 0.7, 1.1, seed=58)
+    pick = np.random.default_rng(59).permutation(N) % base.shape[0]
+    routes = np.ascontiguousarray(base[pick], dtype=np.uint8)
+    n1 = N // 2
+    perm, demand, info = ops.schedule(to_dev(routes), E, n1=n1)
+    perm, demand, info = to_host(perm), to_host(demand), to_host(info)
+    iters, conv, m1, m2, ob, oa, used, n1_out = (int(v) for v in info)
+    assert n1_out == n1 and 1 <= iters <= 10 and conv in (0, 1)
+    assert np.array_equal(np.sort(perm), np.arange(N))
+    b1, b2 = perm[:n1], perm[n1:]
+    assert np.all(np.diff(b1) > 0) and np.all(np.diff(b2) > 0)
+    cols = (np.arange(L)[None, :, None] * E + routes.astype(np.int64)).reshape(N, L * k)
+
+    def counts(tokens):
+        return np.bincount(cols[tokens].ravel(), minlength=L * E)
+
+    c1, c2 = counts(b1), counts(b2)
+    assert np.array_equal(demand.reshape(2, -1), np.stack([c1, c2]))
+    assert oa == int((c1 > 0).sum() + (c2 > 0).sum())
+    o1, o2 = counts(np.arange(n1)), counts(np.arange(n1, N))
+    assert ob == int((o1 > 0).sum() + (o2 > 0).sum())
+    assert oa <= ob
+    if used:
+        assert np.array_equal(perm, np.arange(N)) and oa == ob
+        return
+    # packed paths as 0/1 rows; Hamming distances to the two medoids
+    bits = np.zeros((N, L * E), dtype=np.uint8)
+    np.put_along_axis(bits, cols, 1, axis=1)
+    assert 0 <= m1 < N and 0 <= m2 < N
+    d1 = (bits != bits[m1]).sum(axis=1, dtype=np.int64)
+    d2 = (bits != bits[m2]).sum(axis=1, dtype=np.int64)
+    delta = d1 - d2
+    assert delta[b1].max() <= delta[b2].min()
+    if conv:
+        ones = bits.sum(axis=1, dtype=np.int64)
+        for members, cnt, m in ((b1, c1, m1), (b2, c2, m2)):
+            s = len(members) * ones[members] + ones[members].sum() \
+                - 2 * cnt[cols[members]].sum(axis=1)
+            assert m in set(members[s == s.min()].tolist())
+
+
+def test_merge_passes_and_eight_positions_per_thread():
+    # 300000 tokens: the signature order comes from merge passes over the
+    # sorted 512-token chunks (586 chunks), and the round loop holds eight
+    # positions per thread
+    routes = synth.predicted_routes(300000, 3, 16, 2, 0.7, 1.0, seed=60)
+    _check(routes, 16)
+
+
+def test_sixteen_positions_per_thread():
+    routes = synth.predicted_routes(600000, 3, 16, 2, 0.7, 1.0, seed=61)
+    _check(routes, 16)
+
+
+def test_merge_passes_with_ties_on_later_words():
+    # 140000 tokens drawn from 3000 paths of 4 words each: the merges meet
+    # equal first three words and decide on the fourth, then on the index
+    base = synth.predicted_routes(3000, 2, 128, 2, 0.7, 1.0, seed=62)
+    pick = np.random.default_rng(63).integers(0, 3000, size=140000)
+    _check(base[pick], 128)
