@@ -66,6 +66,10 @@ def parse():
                    help="instead of the layer throughput, time the two-way token scheduler on "
                         "Mixtral-shaped 32-layer predicted routes from 1024 to 2^20 tokens: "
                         "us per call, Eq. 2 before and after, effective GB/s")
+    p.add_argument("--deepseek", action="store_true",
+                   help="instead of the Mixtral-shaped layer, time the DeepSeek-V2-Lite-shaped "
+                        "one: 32768 tokens scheduled into two batches by 26-layer predicted "
+                        "routes, 48 of 64 experts resident per batch, two shared experts")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 counter_collection.csv files (FETCH_SIZE, "
                         "WRITE_SIZE) of a --copy-probe-mib run into the traffic file, then exit")
@@ -427,6 +431,181 @@ def sched_sweep_report(args):
     print(json.dumps(rec))
 
 
+def deepseek_report(args):
+    """DeepSeek-V2-Lite-shaped layer (H 2048, 64 routed experts of width 1408,
+    top-6, two shared experts as one FFN of width 2816): one step schedules
+    32768 tokens into two batches of 16384 by 26-layer predicted routes,
+    routes all of them (router bias toward each token's predicted layer-0
+    experts, so that prediction and routing mostly agree), then per batch
+    permutes, runs the 48 resident experts (the batch's 48 most demanded by
+    prediction; the slot tables and slot weights are set up once, before the
+    timed region, as the expert cache would hold them), gathers the batch for
+    the shared experts, runs them, and combines. Tokens/s, per-stage HIP-event
+    times and rates (routed and shared FFN against the bf16 MFMA peak). One
+    JSON line."""
+    import torch
+    from paper_2410_17954_amd import ops, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.config(5)
+    N, H, E, F, k, L, S = (cfg[n] for n in ("T", "H", "E", "F", "k", "L", "S"))
+    n_s = cfg["n_shared"]
+    inp = synth.layer_inputs(cfg, args.seed, T=N)
+    routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], args.seed)
+    bias = synth.route_boost_bias(routes, 0, E, cfg["boost"], inp.get("bias"))
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    x, wr, bias_d, routes_d = up(inp["x"]), up(inp["w_router"]), up(bias), up(routes)
+    W = {n: up(inp[n]) for n in ("w_gate", "w_up", "w_down")}
+    shared = tuple(up(inp[n])[None] for n in ("shared_gate", "shared_up", "shared_down"))
+    n1 = N // 2
+    T = N - n1
+    perm = torch.empty(N, dtype=torch.int32, device=dev)
+    demand = torch.empty((2, L, E), dtype=torch.int32, device=dev)
+    info = torch.empty(8, dtype=torch.int64, device=dev)
+    ws_s = ops.workspace_tensor(ops.schedule_workspace(N, L, E, k), dev)
+    ops.schedule(routes_d, E, perm=perm, demand=demand, info=info, workspace=ws_s)
+    d_host = demand.cpu().numpy()
+    slots, slot_d, slot_w = [], [], []
+    for b in range(2):
+        sl = ops.plan_slots(d_host[b, 0], S)
+        res = torch.tensor([e for e in range(E) if sl[e] >= 0], dtype=torch.long, device=dev)
+        slots.append(sl)
+        slot_d.append(torch.from_numpy(sl).to(dev))
+        slot_w.append(tuple(W[n].index_select(0, res).contiguous()
+                            for n in ("w_gate", "w_up", "w_down")))
+    idx = torch.empty((N, k), dtype=torch.int32, device=dev)
+    gw = torch.empty((N, k), dtype=torch.float32, device=dev)
+    R = T * k
+    ws_p = ops.workspace_tensor(ops.permute_workspace(T, k, E), dev)
+    ws_p1 = ops.workspace_tensor(ops.permute_workspace(T, 1, 1), dev)
+    ws_f = ops.workspace_tensor(ops.expert_ffn_workspace(R, H, F, E), dev)
+    ws_f1 = ops.workspace_tensor(ops.expert_ffn_workspace(T, H, n_s * F, 1), dev)
+    zeros1 = torch.zeros((N, 1), dtype=torch.int32, device=dev)
+    bufs = []
+    for b in range(2):
+        bufs.append(dict(
+            off=torch.empty(E + 1, dtype=torch.int32, device=dev),
+            rop=torch.empty(R, dtype=torch.int32, device=dev),
+            por=torch.empty(R, dtype=torch.int32, device=dev),
+            xp=torch.empty((R, H), dtype=torch.bfloat16, device=dev),
+            yp=torch.empty((R, H), dtype=torch.bfloat16, device=dev),
+            off1=torch.empty(2, dtype=torch.int32, device=dev),
+            rop1=torch.empty(T, dtype=torch.int32, device=dev),
+            por1=torch.empty(T, dtype=torch.int32, device=dev),
+            xs=torch.empty((T, H), dtype=torch.bfloat16, device=dev),
+            ys=torch.empty((T, H), dtype=torch.bfloat16, device=dev),
+            inc=torch.empty(T, dtype=torch.int32, device=dev)))
+    y = torch.zeros((N, H), dtype=torch.bfloat16, device=dev)
+    names = ["schedule", "route", "permute", "expert_ffn", "shared_gather", "shared_ffn",
+             "combine"]
+
+    def step(ev=None):
+        marks = []
+
+        def mark():
+            if ev is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                marks.append(e)
+        mark()
+        ops.schedule(routes_d, E, perm=perm, demand=demand, info=info, workspace=ws_s)
+        mark()
+        ops.route(x, wr, k, bias=bias_d, topk_idx=idx, topk_w=gw)
+        mark()
+        for b in range(2):
+            tok = perm[:n1] if b == 0 else perm[n1:]
+            bf = bufs[b]
+            ops.permute(x, idx, E, token_ids=tok, expert_offsets=bf["off"], row_of_pair=bf["rop"],
+                        pair_of_row=bf["por"], x_perm=bf["xp"], workspace=ws_p)
+            mark()
+            ops.expert_ffn(bf["xp"], bf["off"], *slot_w[b], slot_of_expert=slot_d[b],
+                           y_perm=bf["yp"], workspace=ws_f)
+            mark()
+            ops.permute(x, zeros1, 1, token_ids=tok, expert_offsets=bf["off1"],
+                        row_of_pair=bf["rop1"], pair_of_row=bf["por1"], x_perm=bf["xs"],
+                        workspace=ws_p1)
+            mark()
+            ops.expert_ffn(bf["xs"], bf["off1"], *shared, y_perm=bf["ys"], workspace=ws_f1)
+            mark()
+            ops.combine(bf["yp"], idx, gw, bf["rop"], token_ids=tok, slot_of_expert=slot_d[b],
+                        y_shared=bf["ys"], y=y, incomplete=bf["inc"])
+            mark()
+        return marks
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    K = args.steps
+    all_marks = []
+    t0 = time.perf_counter()
+    for _ in range(K):
+        all_marks.append(step(True))
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / K
+    st = {n: 0.0 for n in names}
+    for m in all_marks:
+        st["schedule"] += m[0].elapsed_time(m[1])
+        st["route"] += m[1].elapsed_time(m[2])
+        for b in range(2):
+            base = 2 + 5 * b
+            for j, n in enumerate(names[2:]):
+                st[n] += m[base + j].elapsed_time(m[base + j + 1])
+    st = {n: v / K for n, v in st.items()}
+    idx_h = idx.cpu().numpy()
+    perm_h = perm.cpu().numpy()
+    resident_pairs = 0
+    incomplete = 0
+    for b, tok in enumerate((perm_h[:n1], perm_h[n1:])):
+        hit = slots[b][idx_h[tok]] >= 0
+        resident_pairs += int(hit.sum())
+        incomplete += int((~hit).any(axis=1).sum())
+    inc_dev = int(sum(int(bufs[b]["inc"].sum()) for b in range(2)))
+    assert inc_dev == incomplete and torch.isfinite(y.float()).all().item()
+    ffn_flop = 6.0 * H * F * resident_pairs
+    sh_flop = 6.0 * H * (n_s * F) * N
+    bytes_route = N * H * 2 + E * H * 2 + N * E * 4 + N * k * 8
+    bytes_perm = N * H * 2 + N * k * H * 2 + N * k * 12
+    bytes_gather = 2 * N * H * 2
+    bytes_comb = N * k * H * 2 + 2 * N * H * 2 + N * k * 12
+    inf = info.cpu().numpy()
+
+    def rate(nbytes, ms):
+        return {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
+                "hbm_frac": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 3)}
+    rec = {
+        "metric": "DeepSeek-V2-Lite-shaped MoE layer: tokens/s and per-stage rates",
+        "value": N / (ms_step * 1e-3), "unit": "tokens/s", "ms_per_step": ms_step, "steps": K,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"DeepSeek-V2-Lite-shaped MoE layer: {N} tokens scheduled into "
+                               f"two batches by {L}-layer predicted routes (keep {cfg['keep']}, "
+                               f"zipf {cfg['zipf']}), H={H}, E={E}, F={F}, top-{k}, {S} of {E} "
+                               f"experts resident per batch, {n_s} shared experts"},
+        "stages": {
+            "schedule": {"ms": round(st["schedule"], 4), "iters": int(inf[0]),
+                         "obj_before": int(inf[4]), "obj_after": int(inf[5])},
+            "route": rate(bytes_route, st["route"]),
+            "permute": rate(bytes_perm, st["permute"]),
+            "expert_ffn": {"ms": round(st["expert_ffn"], 4),
+                           "TFLOP/s": round(ffn_flop / st["expert_ffn"] / 1e9, 1),
+                           "mfma_frac": round(ffn_flop / st["expert_ffn"] / 1e9 / PEAK_BF16_TFLOPS, 3)},
+            "shared_gather": rate(bytes_gather, st["shared_gather"]),
+            "shared_ffn": {"ms": round(st["shared_ffn"], 4),
+                           "TFLOP/s": round(sh_flop / st["shared_ffn"] / 1e9, 1),
+                           "mfma_frac": round(sh_flop / st["shared_ffn"] / 1e9 / PEAK_BF16_TFLOPS, 3)},
+            "combine": rate(bytes_comb, st["combine"]),
+        },
+        "resident_pair_share": round(resident_pairs / (N * k), 4),
+        "incomplete_tokens": incomplete,
+    }
+    print(json.dumps(rec))
+
+
 def stack_report(args):
     """Dual-batch pipeline over a stack of MoE layers (one JSON line).
 
@@ -595,6 +774,9 @@ def main():
         return
     if args.sched_sweep:
         sched_sweep_report(args)
+        return
+    if args.deepseek:
+        deepseek_report(args)
         return
     if args.rpp:
         rpp_report(args)
