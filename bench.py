@@ -129,7 +129,7 @@ def ece_report(args):
     from paper_2410_17954_amd import ece, ops, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.config(4)
+    cfg = synth.workload("qwen15_moe_layer")
     T, H, E, F, k, S = cfg["T"], cfg["H"], cfg["E"], cfg["F"], cfg["k"], cfg["S"]
     inp = synth.layer_inputs(cfg, args.seed, T=T, parts=("x", "router", "experts", "bias"))
 
@@ -252,7 +252,7 @@ def decode_report(args):
     from paper_2410_17954_amd import ops, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.config(2)
+    cfg = synth.workload("mixtral8x7b_layer")
     H, E, F, k = cfg["H"], cfg["E"], cfg["F"], cfg["k"]
     Tmax = 256
     inp = synth.layer_inputs(cfg, args.seed, T=Tmax, parts=("x", "router", "experts"))
@@ -328,7 +328,7 @@ def ways_report(args):
     from paper_2410_17954_amd import ops, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.config(4)
+    cfg = synth.workload("qwen15_moe_layer")
     L, E, k = cfg["L"], cfg["E"], cfg["k"]
     per_batch = 64                   # decode-sized batches: not every expert is hit
     out = []
@@ -390,7 +390,7 @@ def sched_sweep_report(args):
     from paper_2410_17954_amd import ops, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.config(3)
+    cfg = synth.workload("mixtral8x7b_route_grouped")
     L, E, k = cfg["L"], cfg["E"], cfg["k"]
     W = (L * E + 63) // 64
     Nmax = 1 << 20
@@ -447,7 +447,7 @@ def deepseek_report(args):
     from paper_2410_17954_amd import ops, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.config(5)
+    cfg = synth.workload("deepseek_v2_lite_layer")
     N, H, E, F, k, L, S = (cfg[n] for n in ("T", "H", "E", "F", "k", "L", "S"))
     n_s = cfg["n_shared"]
     inp = synth.layer_inputs(cfg, args.seed, T=N)
@@ -620,7 +620,7 @@ def stack_report(args):
     from paper_2410_17954_amd import ops, pipeline, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.config(3)
+    cfg = synth.workload("mixtral8x7b_route_grouped")
     H, E, F, k = cfg["H"], cfg["E"], cfg["F"], cfg["k"]
     L = args.stack_layers
     N = cfg["T"]                                   # one unit: two batches of N / 2
@@ -785,7 +785,7 @@ def main():
     from paper_2410_17954_amd import ops, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.config(2)
+    cfg = synth.workload("mixtral8x7b_layer")
     T, H, E, F, k, L = cfg["T"], cfg["H"], cfg["E"], cfg["F"], cfg["k"], cfg["L"]
     N = 2 * T                        # one scheduling unit = two adjacent batches
     n1 = N // 2

@@ -30,22 +30,23 @@ import os
 
 import numpy as np
 
-# Workload shapes. T = tokens in one layer call, H hidden, E routed experts,
-# F expert FFN width, k experts per token, S resident slots, n_shared
-# always-on shared experts (each of width F), L layers in the predicted route.
-CONFIGS = {
-    1: dict(name="tiny_fp32", dtype="f32", T=64, H=128, E=8, F=256, k=2, S=8,
+# Workload shapes, by name. T = tokens in one layer call, H hidden, E routed
+# experts, F expert FFN width, k experts per token, S resident slots, n_shared
+# always-on shared experts (each of width F), L layers in the predicted route;
+# seed is the seed its inputs are drawn with.
+WORKLOADS = {
+    "tiny_fp32": dict(seed=1, dtype="f32", T=64, H=128, E=8, F=256, k=2, S=8,
             n_shared=0, L=4, keep=0.7, zipf=1.1, zipf_bias=None, boost=0.0),
-    2: dict(name="mixtral8x7b_layer", dtype="bf16", T=4096, H=4096, E=8, F=14336,
+    "mixtral8x7b_layer": dict(seed=2, dtype="bf16", T=4096, H=4096, E=8, F=14336,
             k=2, S=8, n_shared=0, L=32, keep=0.7, zipf=1.1, zipf_bias=None,
             boost=0.0),
-    3: dict(name="mixtral8x7b_route_grouped", dtype="bf16", T=8192, H=4096, E=8,
+    "mixtral8x7b_route_grouped": dict(seed=3, dtype="bf16", T=8192, H=4096, E=8,
             F=14336, k=2, S=4, n_shared=0, L=32, keep=0.7, zipf=1.1,
             zipf_bias=None, boost=3.0),
-    4: dict(name="qwen15_moe_layer", dtype="bf16", T=8192, H=2048, E=60, F=1408,
+    "qwen15_moe_layer": dict(seed=4, dtype="bf16", T=8192, H=2048, E=60, F=1408,
             k=4, S=32, n_shared=4, L=24, keep=0.7, zipf=1.2, zipf_bias=1.2,
             boost=0.0),
-    5: dict(name="deepseek_v2_lite_layer", dtype="bf16", T=32768, H=2048, E=64,
+    "deepseek_v2_lite_layer": dict(seed=5, dtype="bf16", T=32768, H=2048, E=64,
             F=1408, k=6, S=48, n_shared=2, L=26, keep=0.7, zipf=1.0,
             zipf_bias=1.0, boost=3.0),
 }
@@ -57,8 +58,8 @@ _STREAM = {"x": 0, "router": 1, "w_gate": 2, "w_up": 3, "w_down": 4,
            "bias_rank": 8, "routes": 9, "logits": 10, "idx": 11, "misc": 12}
 
 
-def config(n):
-    return dict(CONFIGS[n], id=n)
+def workload(name):
+    return dict(WORKLOADS[name], name=name)
 
 
 def rng_for(seed, name, block=None):

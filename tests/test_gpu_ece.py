@@ -25,7 +25,7 @@ def _cache(store, S):
 
 
 def test_load_experts_copies_whole_experts():
-    cfg = dict(synth.config(2), H=256, F=512)
+    cfg = dict(synth.workload("mixtral8x7b_layer"), H=256, F=512)
     store = _store(synth.layer_inputs(cfg, 3, T=8, parts=("experts",)))
     cache = _cache(store, 3)
     ops.load_experts(store, cache, [5, 0, 7], [2, 0, 1])
@@ -36,7 +36,7 @@ def test_load_experts_copies_whole_experts():
 
 
 def test_load_experts_rejects_bad_ids():
-    cfg = dict(synth.config(2), H=64, F=64)
+    cfg = dict(synth.workload("mixtral8x7b_layer"), H=64, F=64)
     store = _store(synth.layer_inputs(cfg, 3, T=8, parts=("experts",)))
     cache = _cache(store, 2)
     for ex, sl in (([0, 1], [1, 1]), ([8], [0]), ([0], [2]), ([-1], [0])):
@@ -50,7 +50,7 @@ def test_load_experts_rejects_bad_ids():
                                              # the resident experts are done: rounds of 1, 2, 1, 2
 ])
 def test_corrected_layer_equals_all_resident_layer(S, resident, rounds):
-    cfg = dict(synth.config(2), T=512, H=512, F=1024)
+    cfg = dict(synth.workload("mixtral8x7b_layer"), T=512, H=512, F=1024)
     E, k = cfg["E"], cfg["k"]
     inp = synth.layer_inputs(cfg, 7)
     x_d = to_dev(inp["x"])

@@ -47,7 +47,7 @@ def _run(counts, H, F, slot, S, seed, dtype="bf16", tol=1e-2, extra_rows=0):
 
 
 def test_tiny_fp32_config():
-    cfg = synth.config(1)
+    cfg = synth.workload("tiny_fp32")
     counts = np.bincount(synth.random_topk_idx(64, 8, 2, 1).ravel(), minlength=8)
     _run(counts, cfg["H"], cfg["F"], None, 8, seed=1, dtype="f32", tol=1e-4)
 
@@ -102,23 +102,24 @@ def test_shared_experts_as_one_dense_group():
     assert rel_max_err(vals(y), ref) <= 1e-2
 
 
-@pytest.mark.parametrize("cfg_id", [2, 4])
-def test_full_shape_sampled_rows(cfg_id):
+@pytest.mark.parametrize("name", ["mixtral8x7b_layer", "qwen15_moe_layer"])
+def test_full_shape_sampled_rows(name):
     """Full expert shapes; the oracle evaluates the first and last row of every
     expert and a seeded sample of rows one by one."""
-    cfg = synth.config(cfg_id)
+    cfg = synth.workload(name)
+    seed = cfg["seed"]
     E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
-    T = 4096 if cfg_id == 2 else 8192
-    idx = synth.random_topk_idx(T, E, k, seed=cfg_id, skew=None if cfg_id == 2 else 1.2)
+    T = cfg["T"]
+    idx = synth.random_topk_idx(T, E, k, seed=seed, skew=cfg["zipf_bias"])
     counts = np.bincount(idx.ravel(), minlength=E)
     offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
     R = int(offsets[-1])
-    inp = synth.layer_inputs(cfg, cfg_id, T=R, parts=("x", "experts"))
+    inp = synth.layer_inputs(cfg, seed, T=R, parts=("x", "experts"))
     x = inp["x"]
     y = ops.expert_ffn(to_dev(x), to_dev(offsets), to_dev(inp["w_gate"]), to_dev(inp["w_up"]),
                        to_dev(inp["w_down"]))
     got = vals(y)
-    g = np.random.default_rng(cfg_id)
+    g = np.random.default_rng(seed)
     sample = set(g.choice(R, size=24, replace=False).tolist())
     for e in range(E):
         if counts[e]:
@@ -159,7 +160,7 @@ def test_full_shape_decode_batch(T):
     """Decode-sized batch at the full 8-expert shape (H 4096, F 14336): 24 or
     100 tokens with top-2 give up to 16, or 17 to 32, rows per expert; every
     row is checked."""
-    cfg = synth.config(2)
+    cfg = synth.workload("mixtral8x7b_layer")
     E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
     idx = synth.random_topk_idx(T, E, k, seed=77)
     counts = np.bincount(idx.ravel(), minlength=E)

@@ -139,7 +139,7 @@ def test_stack_full_shape_two_layers_sampled():
     """Mixtral-shaped pre-normalised blocks (H 4096, 8 experts of F 14336,
     top-2) over a 4096-token batch of an 8192-token unit; the oracle checks a
     seeded sample of tokens, layer by layer."""
-    cfg = synth.config(2)
+    cfg = synth.workload("mixtral8x7b_layer")
     E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
     L, n, T = 2, 8192, 4096
     g = torch.Generator(device="cuda:0")

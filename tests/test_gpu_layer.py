@@ -61,7 +61,7 @@ def _oracle_sample(inp, cfg, sample, slot_np, bias=None, renorm=True):
 
 
 def test_tiny_fp32_layer_full():
-    cfg = synth.config(1)
+    cfg = synth.workload("tiny_fp32")
     inp = synth.layer_inputs(cfg, 1)
     E, k = cfg["E"], cfg["k"]
     x_d = to_dev(inp["x"])
@@ -76,7 +76,7 @@ def test_tiny_fp32_layer_full():
 
 
 def test_mixtral_layer_full_size_sampled():
-    cfg = synth.config(2)
+    cfg = synth.workload("mixtral8x7b_layer")
     T, E, k = cfg["T"], cfg["E"], cfg["k"]
     inp = synth.layer_inputs(cfg, 2)
     x_d = to_dev(inp["x"])
@@ -94,14 +94,15 @@ def test_mixtral_layer_full_size_sampled():
     assert rel_max_err(vals(y)[sample], ref["y"]) <= 1e-2
 
 
-def _scheduled_unit(cfg_id, n_sample=48):
+def _scheduled_unit(name, n_sample=48):
     """Route-grouped workload: schedule N tokens by predicted route, plan each
     batch's resident set from the predicted demand of layer 0, run layer 0
     batch by batch with misses flagged."""
-    cfg = synth.config(cfg_id)
+    cfg = synth.workload(name)
+    seed = cfg["seed"]
     N, E, k, L, S = cfg["T"], cfg["E"], cfg["k"], cfg["L"], cfg["S"]
-    inp = synth.layer_inputs(cfg, cfg_id, T=N)
-    routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], cfg_id)
+    inp = synth.layer_inputs(cfg, seed, T=N)
+    routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], seed)
     bias = synth.route_boost_bias(routes, 0, E, cfg["boost"], inp.get("bias"))
     perm, demand, info = ops.schedule(to_dev(routes), E)
     r_perm, r_demand, r_info = oracle.schedule(routes, E)
@@ -118,7 +119,7 @@ def _scheduled_unit(cfg_id, n_sample=48):
     assert np.array_equal(to_host(idx), oracle.topk_select(z, k))
     y = torch.zeros_like(x_d)
     n1 = int(r_info[7])
-    g = np.random.default_rng(cfg_id)
+    g = np.random.default_rng(seed)
     d_host = to_host(demand)
     for b, tok in enumerate((r_perm[:n1], r_perm[n1:])):
         slot = ops.plan_slots(d_host[b, 0], S)
@@ -134,15 +135,15 @@ def _scheduled_unit(cfg_id, n_sample=48):
 
 
 def test_route_grouped_mixtral_unit_with_misses():
-    _scheduled_unit(3)
+    _scheduled_unit("mixtral8x7b_route_grouped")
 
 
 def test_deepseek_unit_scheduled_shared_experts():
-    _scheduled_unit(5)
+    _scheduled_unit("deepseek_v2_lite_layer")
 
 
 def test_qwen_layer_zipf_bias_shared_experts():
-    cfg = synth.config(4)
+    cfg = synth.workload("qwen15_moe_layer")
     T, E, k, S = cfg["T"], cfg["E"], cfg["k"], cfg["S"]
     inp = synth.layer_inputs(cfg, 4)
     x_d = to_dev(inp["x"])
@@ -165,7 +166,7 @@ def test_qwen_layer_zipf_bias_shared_experts():
 def test_missed_experts_second_pass_completes_the_output():
     """Real-time correction: run the resident experts, then the missed ones
     with accumulate=1; the sum equals the all-resident layer."""
-    cfg = dict(synth.config(2), T=512, H=512, F=1024)
+    cfg = dict(synth.workload("mixtral8x7b_layer"), T=512, H=512, F=1024)
     E, k = cfg["E"], cfg["k"]
     inp = synth.layer_inputs(cfg, 7)
     x_d = to_dev(inp["x"])

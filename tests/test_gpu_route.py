@@ -31,8 +31,8 @@ def test_signed_zero_and_equal_logits():
     assert to_host(idx).tolist() == oracle.topk_select(z.astype(np.float64), 3).tolist()
 
 
-def _x_mode_case(cfg_id, T, seed, bias_kind=None, renorm=True):
-    cfg = synth.config(cfg_id)
+def _x_mode_case(name, T, seed, bias_kind=None, renorm=True):
+    cfg = synth.workload(name)
     inp = synth.layer_inputs(cfg, seed, T=T, parts=("x", "router"))
     E, k = cfg["E"], cfg["k"]
     bias = None
@@ -59,38 +59,38 @@ def _x_mode_case(cfg_id, T, seed, bias_kind=None, renorm=True):
 
 
 def test_x_mode_tiny_fp32():
-    _x_mode_case(1, 64, 1)
+    _x_mode_case("tiny_fp32", 64, 1)
 
 
 @pytest.mark.parametrize("T", [1, 17, 300])
 def test_x_mode_ragged_token_counts(T):
-    _x_mode_case(2, T, 7)
+    _x_mode_case("mixtral8x7b_layer", T, 7)
 
 
 def test_x_mode_mixtral_full_size():
-    near = _x_mode_case(2, 8192, 2)
+    near = _x_mode_case("mixtral8x7b_layer", 8192, 2)
     # a sizeable share of tokens is not decided by the float32 error bound
     # alone; those go through the float64 refinement
     assert near > 0
 
 
 def test_x_mode_qwen_expert_bias():
-    _x_mode_case(4, 2048, 4, bias_kind="expert")
+    _x_mode_case("qwen15_moe_layer", 2048, 4, bias_kind="expert")
 
 
 def test_x_mode_deepseek_token_bias_no_renorm():
-    _x_mode_case(5, 4096, 5, bias_kind="token", renorm=False)
+    _x_mode_case("deepseek_v2_lite_layer", 4096, 5, bias_kind="token", renorm=False)
 
 
 @pytest.mark.parametrize("T", [17, 8209])
 def test_x_mode_64_token_tiles_ragged(T):
     # 33..64 experts run in 64-token tiles: one partial tile, and many tiles
     # with a ragged last one
-    _x_mode_case(5, T, 11, bias_kind="expert")
+    _x_mode_case("deepseek_v2_lite_layer", T, 11, bias_kind="expert")
 
 
 def test_x_mode_48_experts():
-    cfg = dict(synth.config(4), E=40, k=5)
+    cfg = dict(synth.workload("qwen15_moe_layer"), E=40, k=5)
     inp = synth.layer_inputs(cfg, 12, T=300, parts=("x", "router"))
     idx, w, z = ops.route(to_dev(inp["x"]), to_dev(inp["w_router"]), 5, want_logits=True)
     x, wr = synth.values(inp["x"]), synth.values(inp["w_router"])
@@ -101,7 +101,7 @@ def test_x_mode_48_experts():
 
 
 def test_x_mode_wide_expert_count():
-    cfg = dict(synth.config(4), E=256, k=8)
+    cfg = dict(synth.workload("qwen15_moe_layer"), E=256, k=8)
     inp = synth.layer_inputs(cfg, 9, T=100, parts=("x", "router"))
     idx, w, z = ops.route(to_dev(inp["x"]), to_dev(inp["w_router"]), 8, want_logits=True)
     x, wr = synth.values(inp["x"]), synth.values(inp["w_router"])

@@ -39,7 +39,7 @@ def test_markov_routes(N, L, E, k, s):
 
 
 def test_route_grouped_mixtral_unit():
-    cfg = synth.config(3)
+    cfg = synth.workload("mixtral8x7b_route_grouped")
     routes = synth.predicted_routes(cfg["T"], cfg["L"], cfg["E"], cfg["k"], cfg["keep"],
                                     cfg["zipf"], seed=3)
     info = _check(routes, cfg["E"])
@@ -47,7 +47,7 @@ def test_route_grouped_mixtral_unit():
 
 
 def test_deepseek_unit_26_layers():
-    cfg = synth.config(5)
+    cfg = synth.workload("deepseek_v2_lite_layer")
     routes = synth.predicted_routes(cfg["T"], cfg["L"], cfg["E"], cfg["k"], cfg["keep"],
                                     cfg["zipf"], seed=5)
     _check(routes, cfg["E"])
@@ -154,7 +154,7 @@ def test_multi_way_no_guard_and_one_round():
 
 
 def test_multi_way_mixtral_unit_four_batches():
-    cfg = synth.config(2)
+    cfg = synth.workload("mixtral8x7b_layer")
     routes = synth.predicted_routes(2 * cfg["T"], cfg["L"], cfg["E"], cfg["k"], cfg["keep"],
                                     cfg["zipf"], seed=53)
     rp, ro, ri = _check_multi(routes, cfg["E"], 4)

@@ -28,7 +28,7 @@ def test_swiglu_matrix_form_matches_loops():
 
 
 def test_expert_ffn_tiny_config_against_loops():
-    cfg = synth.config(1)
+    cfg = synth.workload("tiny_fp32")
     inp = synth.layer_inputs(cfg, seed=1, T=3, parts=("x", "experts"))
     x = inp["x"].astype(np.float64)
     e = 5

@@ -99,7 +99,7 @@ def test_single_expert_gets_weight_one():
 
 
 def test_router_logits_against_loops():
-    cfg = synth.config(1)
+    cfg = synth.workload("tiny_fp32")
     inp = synth.layer_inputs(cfg, seed=1, T=6, parts=("x", "router"))
     x, wr = inp["x"].astype(np.float64), inp["w_router"].astype(np.float64)
     bias = np.linspace(-1, 1, cfg["E"])

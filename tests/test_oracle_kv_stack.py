@@ -59,7 +59,7 @@ def test_reindex_finds_every_token_in_its_new_batch():
 
 
 def _stack_inputs(L, T=9, seed=5, E=None):
-    cfg = synth.config(1)
+    cfg = synth.workload("tiny_fp32")
     layers = []
     for l in range(L):
         inp = synth.layer_inputs(cfg, seed=seed + l, T=T, parts=("router", "experts"))

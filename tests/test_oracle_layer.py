@@ -9,8 +9,8 @@ import oracle
 from paper_2410_17954_amd import synth
 
 
-def _inputs(n=1, T=12, seed=1, parts=("x", "router", "experts", "shared", "bias")):
-    cfg = synth.config(n)
+def _inputs(name="tiny_fp32", T=12, seed=1, parts=("x", "router", "experts", "shared", "bias")):
+    cfg = synth.workload(name)
     inp = synth.layer_inputs(cfg, seed=seed, T=T, parts=parts)
     return cfg, {k: synth.values(v) for k, v in inp.items()}
 
@@ -38,7 +38,7 @@ def test_k_equals_E_is_the_soft_mixture():
 
 
 def test_shared_experts_concatenate_along_F():
-    cfg, d = _inputs(4, T=5, parts=("x", "shared"))
+    cfg, d = _inputs("qwen15_moe_layer", T=5, parts=("x", "shared"))
     H, F, ns = cfg["H"], cfg["F"], cfg["n_shared"]
     wg, wu, wd = d["shared_gate"], d["shared_up"], d["shared_down"]
     x = d["x"]
