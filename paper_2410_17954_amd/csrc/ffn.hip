@@ -558,12 +558,14 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   using I3 = std::integral_constant<int, 3>;
 
   bool in_tail = false;                        // thread 0 only
+  // thread 0: the next whole-round claim, issued while the current tile runs
+  int32_t j_next = tid == 0 ? atomicAdd(&claim[xcd], 1) : 0;
   for (;;) {
     if (tid == 0) {
       int64_t tt = -1;
       int pc = 0;
       if (!in_tail) {
-        const int64_t j = atomicAdd(&claim[xcd], 1);
+        const int64_t j = j_next;
         const int64_t c = ((j / per_xcd) * 8 + xcd) * per_xcd + (j % per_xcd);
         if (c < full) tt = c;
         else in_tail = true;
@@ -582,11 +584,17 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
     const int64_t t = s_claim;
     const int piece = s_piece;
     if (t < 0) break;
+    if (tid == 0 && !in_tail) j_next = atomicAdd(&claim[xcd], 1);
     const bool split_tile = t >= full && split > 1;
     const int64_t kbeg = split_tile ? piece * ksteps / split : 0;
     const int64_t nks = split_tile ? (piece + 1) * ksteps / split - kbeg : ksteps;
+    // the last expert whose first tile is at or before t (binary search)
     int e = 0;
-    while (e + 1 < E && (int64_t)prefix[e + 1] * n_tiles <= t) ++e;
+    for (int hi = E - 1; e < hi;) {
+      const int mid = (e + hi + 1) >> 1;
+      if ((int64_t)prefix[mid] * n_tiles <= t) e = mid;
+      else hi = mid - 1;
+    }
     const int64_t local = t - (int64_t)prefix[e] * n_tiles;
     const int64_t me = prefix[e + 1] - prefix[e];
     const int64_t nt = local / me;
