@@ -580,7 +580,10 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
       s_claim = tt;
       s_piece = pc;
     }
-    __syncthreads();
+    // LDS only: the claim, and every wave's last reads of the staging stages
+    // before the prologue refills them; the previous epilogue's global
+    // stores drain on their own (nothing in this launch reads them)
+    lds_barrier();
     const int64_t t = s_claim;
     const int piece = s_piece;
     if (t < 0) break;
