@@ -179,3 +179,17 @@ def test_full_shape_decode_batch(T):
             ref[lo:hi] = oracle.swiglu(synth.values(x[lo:hi]), synth.values(inp["w_gate"][e]),
                                        synth.values(inp["w_up"][e]), synth.values(inp["w_down"][e]))
     assert rel_max_err(got, ref) <= 1e-2
+
+
+def test_bf16_many_experts_large_tiles():
+    # 256 experts, a third of them empty and some non-resident, the rest from 1
+    # to 700 rows: too many rows for the few-row kernels, so every tile's
+    # expert is found among long flat stretches of the row-tile prefix
+    g = np.random.default_rng(91)
+    E = 256
+    counts = np.where(g.random(E) < 0.35, 0, g.integers(1, 700, size=E))
+    slot = np.full(E, -1, np.int32)
+    res = np.flatnonzero(g.random(E) < 0.8)
+    slot[res] = np.arange(len(res), dtype=np.int32)
+    assert counts.sum() > 32 * E
+    _run(counts, 64, 96, slot, len(res), seed=91)
