@@ -770,7 +770,9 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
         else if (inflight == 1) wait_vmcnt<2 * PPW>();
         else wait_vmcnt<0>();
       }
-      __syncthreads();
+      // every wave has its own pieces of step 0; the barrier makes that true
+      // of all of them (LDS only: steps 1 and 2 keep loading)
+      lds_barrier();
       rd(I0{}, 0, fa0, fb0);
       int64_t kt = 0;
       for (; kt + STAGES + STAGES - 1 <= nks; kt += STAGES) {
