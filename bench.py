@@ -942,6 +942,11 @@ def main():
     # the same fractions against what this chip measured (probe kernels, below)
     for name in ("route", "permute", "combine"):
         stages[name]["hbm_frac_measured"] = stages[name]["GB/s"] / ceilings["hbm_read_GBps"]
+    # routing is one cold read of x while the cache holds the FFN's and
+    # combine's dirty lines: the dirty-cache pass is its own ceiling (permute
+    # and combine also write, and read data written just before)
+    stages["route"]["frac_of_dirty_cache_read"] = (stages["route"]["GB/s"] /
+                                                   ceilings["read_64MiB_dirty_GBps"])
     stages["expert_ffn"]["mfma_frac_measured"] = achieved / ceilings["mfma_bf16_TFLOPs"]
 
     out = {
@@ -1018,10 +1023,39 @@ def measured_ceilings(torch, ops, dev):
     buf = torch.ones(2 ** 30, dtype=torch.uint8, device=dev)
     rms = timed(lambda: lib.moe_probe_read(ops._ptr(buf), buf.numel(), ops._ptr(out_u),
                                            out_u.numel(), st), 5)
+
+    # One 64 MiB pass (a routed batch's activations) in three cache states:
+    # warm (read just before), clean (a 512 MiB read evicted it) and dirty (a
+    # 512 MiB write evicted it: the last-level cache holds dirty lines that are
+    # written back during the pass, as after the expert FFN and combine).
+    a = torch.ones(64 * 2 ** 20, dtype=torch.uint8, device=dev)
+    big = buf[:512 * 2 ** 20]
+
+    def read(t):
+        lib.moe_probe_read(ops._ptr(t), t.numel(), ops._ptr(out_u), out_u.numel(), st)
+
+    def state(prep):
+        ts = []
+        for rep in range(6):
+            prep(rep)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            read(a)
+            e1.record()
+            torch.cuda.synchronize()
+            if rep:
+                ts.append(e0.elapsed_time(e1))
+        return a.numel() / (float(np.median(ts)) * 1e-3) / 1e9
+    warm = state(lambda rep: read(a))
+    clean = state(lambda rep: read(big))
+    dirty = state(lambda rep: big.fill_(rep))
     return {"mfma_bf16_TFLOPs": flops / (ms * 1e-3) / 1e12,
             "hbm_read_GBps": buf.numel() / (rms * 1e-3) / 1e9,
+            "read_64MiB_warm_GBps": warm, "read_64MiB_clean_GBps": clean,
+            "read_64MiB_dirty_GBps": dirty,
             "probes": "moe_probe_mfma_bf16 (4 waves per SIMD, 8 MFMA chains, "
-                      f"{iters} rounds), moe_probe_read (1 GiB, one pass)"}
+                      f"{iters} rounds), moe_probe_read (1 GiB, one pass; 64 MiB after a "
+                      "read of it, after a 512 MiB read, after a 512 MiB write)"}
 
 
 def measured_traffic():
