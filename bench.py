@@ -323,7 +323,9 @@ def ways_report(args):
     routes: for B batches of 64 tokens, the time of one call (HIP events,
     median of 7) and the active (layer, expert) pairs summed over the batches
     (Eq. 2 generalised) for the input order cut into B contiguous batches and
-    for the scheduled batches. One JSON line."""
+    for the scheduled batches; once on the unstructured Markov routes and once
+    on topic-structured ones (two topics, 16-token batches, synth.topic_routes).
+    One JSON line."""
     import torch
     from paper_2410_17954_amd import ops, synth
 
@@ -332,9 +334,15 @@ def ways_report(args):
     L, E, k = cfg["L"], cfg["E"], cfg["k"]
     per_batch = 64                   # decode-sized batches: not every expert is hit
     out = []
-    for B in (2, 4, 8, 16, 64):
-        N = B * per_batch
-        routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], args.seed)
+    topics, topic_batch = 2, 16      # topic case: two topics, 16-token batches
+    out_topics = []
+    for B, structured in [(b, False) for b in (2, 4, 8, 16, 64)] + \
+                         [(b, True) for b in (2, 4, 8, 16, 64)]:
+        N = B * (topic_batch if structured else per_batch)
+        if structured:
+            routes = synth.topic_routes(N, L, E, k, cfg["keep"], cfg["zipf"], topics, args.seed)
+        else:
+            routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], args.seed)
         rt = torch.from_numpy(np.ascontiguousarray(routes, dtype=np.uint8)).to(dev)
         ws = ops.workspace_tensor(ops.schedule_multi_workspace(N, L, E, k, B), dev)
         perm = torch.empty(N, dtype=torch.int32, device=dev)
@@ -357,14 +365,15 @@ def ways_report(args):
             if rep >= args.warmup:
                 ts.append(e0.elapsed_time(e1))
         before = 0
+        nb = N // B
         for b in range(B):
-            r = routes[b * per_batch:(b + 1) * per_batch].astype(np.int64)
+            r = routes[b * nb:(b + 1) * nb].astype(np.int64)
             act = np.zeros((L, E), dtype=bool)
             for l in range(L):
                 act[l, np.unique(r[:, l, :])] = True
             before += int(act.sum())
         after = int((demand.cpu().numpy() > 0).sum())
-        out.append({"batches": B, "tokens": N, "ms": round(float(np.median(ts)), 4),
+        (out_topics if structured else out).append({"batches": B, "tokens": N, "ms": round(float(np.median(ts)), 4),
                     "active_pairs_input_order": before, "active_pairs_scheduled": after,
                     "experts_per_layer_per_batch_input": round(before / (B * L), 2),
                     "experts_per_layer_per_batch_scheduled": round(after / (B * L), 2)})
@@ -372,7 +381,12 @@ def ways_report(args):
            "config": {"workload": f"Qwen1.5-MoE-shaped predicted routes: L={L}, E={E}, top-{k}, "
                                   f"batches of {per_batch} tokens, keep {cfg['keep']}, "
                                   f"zipf {cfg['zipf']}"},
-           "steps": out, "data": "synthetic"}
+           "steps": out,
+           "steps_topic_routes": out_topics,
+           "topic_routes": f"batches of {topic_batch} tokens, {topics} topics, each token on "
+                           "one topic's Markov chain over its own expert popularity order, "
+                           "topics mixed along the token axis",
+           "data": "synthetic"}
     print(json.dumps(rec))
 
 

@@ -201,6 +201,22 @@ def predicted_routes(N, L, E, k, keep, s, seed):
     return routes.astype(np.uint8)
 
 
+def topic_routes(N, L, E, k, keep, s, topics, seed):
+    """Predicted routes with topic structure, uint8 [N, L, k]: each token
+    belongs to one of `topics` topics (uniformly, in random order along the
+    token axis); a topic's tokens follow the Markov chain of predicted_routes
+    over that topic's own expert popularity order (seed seed * 1009 + 1 + t),
+    so tokens of one topic tend to share experts."""
+    g = rng_for(seed, "misc")
+    topic = g.integers(0, topics, size=N)
+    routes = np.zeros((N, L, k), dtype=np.uint8)
+    for t in range(topics):
+        rows = np.flatnonzero(topic == t)
+        if rows.size:
+            routes[rows] = predicted_routes(rows.size, L, E, k, keep, s, seed * 1009 + 1 + t)
+    return routes
+
+
 def predicted_and_actual_routes(N, L, E, k, keep, s, acc, seed):
     """(actual, predicted) uint8 [N, L, k]: actual routes from the Markov chain
     of predicted_routes; the prediction keeps each choice with probability

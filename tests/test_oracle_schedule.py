@@ -323,3 +323,15 @@ def test_multi_more_batches_than_tokens():
     for r in (1, 3, 5, 6):                       # one token: identity, L*k pairs
         assert info[r].tolist() == [0, 1, -1, -1, 4, 4, 0, 0]
     assert demand.sum() == 3 * 2 * 2
+
+
+def test_topic_structured_routes_are_regrouped():
+    # two 16-token batches whose tokens follow two topics (each with its own
+    # expert popularity): the scheduler regroups them and activates fewer
+    # (layer, expert) pairs than the input split
+    cfg = synth.workload("qwen15_moe_layer")
+    r = synth.topic_routes(32, cfg["L"], cfg["E"], cfg["k"], cfg["keep"], cfg["zipf"], 2, 2)
+    perm, demand, info = oracle.schedule(r, cfg["E"])
+    assert info[6] == 0 and info[5] < info[4]
+    assert info[5] == oracle.eq2_objective(oracle.route_bits(r, cfg["E"]).reshape(32, -1),
+                                           np.isin(np.arange(32), perm[:16]))
