@@ -124,3 +124,49 @@ def test_sequences_are_independent_and_the_position_bias_is_used():
     p0["dec_rel"][:] = 0.0
     _, nob = rpp.rpp_forward(ids, w0, DIMS)
     assert not np.allclose(nob, all3)
+
+
+def _bias_only_attention(S, bidirectional, hot_bucket, beta):
+    """One head whose scores come from the relative-position table alone (zero
+    query and key weights), with a table that is beta on `hot_bucket` and zero
+    elsewhere; the values are the one-hot rows of the identity, so row i of
+    the output is query i's attention distribution over the keys."""
+    h = 1
+    rel = np.zeros((32, h))
+    rel[hot_bucket, 0] = beta
+    bias = rpp.position_bias(S, rel, bidirectional, 32, 128)
+    x = np.eye(S)[None]                                # [1, S, S]: token j -> e_j
+    zero = np.zeros((S, S))
+    return rpp._attention(x, x, zero, zero, np.eye(S), np.eye(S), h, bias)[0]
+
+
+def test_position_bias_direction_causal_by_hand():
+    # Decoder (causal): query i sees keys j <= i at distance n = i - j >= 0.
+    # The bucket of distance 1 (bucket 1) carries ln 3, every other bucket 0:
+    #   query 0: only key 0                          -> [1, 0, 0]
+    #   query 1: key 0 (n=1, weight 3), key 1 (n=0)  -> [3/4, 1/4, 0]
+    #   query 2: keys 0 (n=2), 1 (n=1, weight 3), 2  -> [1/5, 3/5, 1/5]
+    # With the distance taken the other way round (key - query) every visible
+    # key would clip to bucket 0 and the table entry would never be read.
+    p = _bias_only_attention(3, False, 1, math.log(3.0))
+    np.testing.assert_allclose(p, [[1, 0, 0], [0.75, 0.25, 0], [0.2, 0.6, 0.2]], atol=1e-15)
+    # bucket 0 (distance 0) differs from bucket 1: weighting it instead favours
+    # the diagonal
+    p0 = _bias_only_attention(3, False, 0, math.log(3.0))
+    np.testing.assert_allclose(p0, [[1, 0, 0], [0.25, 0.75, 0], [0.2, 0.2, 0.6]], atol=1e-15)
+
+
+def test_position_bias_direction_bidirectional_by_hand():
+    # Encoder: keys before the query (n = i - j > 0) take the lower half of the
+    # buckets, keys after it (n < 0) the upper half (16 + |n|). ln 3 on bucket
+    # 1 (one step back):
+    #   query 0: no key one step back                 -> uniform [1/3, 1/3, 1/3]
+    #   query 1: key 0 weighted 3                      -> [3/5, 1/5, 1/5]
+    #   query 2: key 1 weighted 3                      -> [1/5, 3/5, 1/5]
+    p = _bias_only_attention(3, True, 1, math.log(3.0))
+    np.testing.assert_allclose(p, [[1 / 3, 1 / 3, 1 / 3], [0.6, 0.2, 0.2], [0.2, 0.6, 0.2]],
+                               atol=1e-15)
+    # ln 3 on bucket 17 (one step ahead) mirrors it
+    p = _bias_only_attention(3, True, 17, math.log(3.0))
+    np.testing.assert_allclose(p, [[0.2, 0.6, 0.2], [0.2, 0.2, 0.6], [1 / 3, 1 / 3, 1 / 3]],
+                               atol=1e-15)
