@@ -61,7 +61,7 @@ enum moe_status {
 enum moe_dtype { MOE_F32 = 0, MOE_BF16 = 1 };
 
 /* Version of this interface; bumped on any incompatible change. */
-#define MOEFLOW_ABI_VERSION 1
+#define MOEFLOW_ABI_VERSION 2
 int moe_abi_version(void);
 
 /* Static, human-readable name of a status code. */
@@ -119,13 +119,20 @@ int moe_route(const void* x, const void* w_gate, int32_t dtype,
  * demand  [2,L,E] int32  tokens of each new batch using (l, e); may be NULL
  * info    [8] int64      {iters, converged, medoid1, medoid2, obj_before,
  *                         obj_after, used_original, n1}
+ * err     int32          may be NULL; set to 1 (never cleared: the caller
+ *                        clears it) when the result is not to be trusted
+ * Untrusted result: the rounds of larger inputs run in one launch whose
+ *   blocks wait for each other at grid barriers; every wait is bounded, and a
+ *   wait that gives up (after 2^20 polls, when the device kept some blocks
+ *   from becoming resident that long) lets the launch finish with info[0] =
+ *   -1 and *err = 1. perm, demand and the batch sizes are then unspecified.
  * Limits: N >= 1, 0 <= n1 <= N, L >= 1, 1 <= k <= E <= 256, max_iters >= 1,
  *   N < 2^26, L*E < 2^24. n1 == 0 or n1 == N returns the identity with iters = 0.
  * ---------------------------------------------------------------------- */
 size_t moe_schedule_workspace(int64_t N, int32_t L, int32_t E, int32_t k);
 int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t E, int32_t k,
                  int64_t n1, int32_t max_iters, int32_t keep_original_if_worse,
-                 int32_t* perm, int32_t* demand, int64_t* info,
+                 int32_t* perm, int32_t* demand, int64_t* info, int32_t* err,
                  void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
@@ -148,6 +155,9 @@ int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t E, int32_t
  *                                pre-order (medoids are node-local indices);
  *                                a split of an empty node records
  *                                {0, 1, -1, -1, 0, 0, 0, 0}; may be NULL
+ * err            int32           as for moe_schedule: set to 1 when any split's
+ *                                result is not to be trusted (its info[0] is
+ *                                -1); may be NULL
  * All arrays are DEVICE memory owned by the caller; the workspace (size from
  * moe_schedule_multi_workspace, 256-byte aligned) is scratch for the call.
  * Runs B-1 two-way splits on `stream`, with no host synchronisation.
@@ -159,7 +169,7 @@ size_t moe_schedule_multi_workspace(int64_t N, int32_t L, int32_t E, int32_t k, 
 int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, int32_t E, int32_t k,
                        int32_t B, int32_t max_iters, int32_t keep_original_if_worse,
                        int32_t* perm, int32_t* batch_offsets, int32_t* demand, int64_t* info,
-                       void* workspace, size_t ws_bytes, void* stream);
+                       int32_t* err, void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * moe_kv_gather -- KV-cache Merge and the row movement of Reindex (Sec. 3.3.3).
@@ -286,7 +296,9 @@ int moe_probe_read(const void* src, int64_t bytes, uint32_t* out, int32_t out_le
 
 /* ------------------------------------------------------------------------
  * moe_permute -- group the (token, choice) pairs of one batch by expert so
- * that every expert sees its tokens as one contiguous block of rows.
+ * that every expert sees its tokens as one contiguous block of rows: the
+ * batched evaluation of the selected experts E_i(x) of Sec. 2.1's MoE layer
+ * (each expert applied once to all the tokens that chose it).
  *
  * Batch position i (0 <= i < T) is token t_i = token_ids[i] (or i when
  * token_ids is NULL); pair p = i*k + j is its j-th choice, on expert
@@ -376,6 +388,15 @@ int moe_combine(const void* y_perm, int32_t dtype, int64_t H, int64_t rows,
  * Expert cache engine (Sec. 3.4). Host-side planning over small integer
  * tables, and the loading of whole experts into device cache slots.
  *
+ * moe_plan_slots -- the resident set of one layer from predicted demand
+ *   (the planning step of PLEC, Sec. 3.4.1: the cache holds the experts the
+ *   prediction says the layer will use most): the S experts with the largest
+ *   demand, equal demand lower expert id first, occupy slots 0..S-1 in
+ *   ascending expert id; every other expert gets slot -1 (not resident).
+ *   demand [E] int32 HOST; slot_of_expert [E] int32 HOST output. S larger
+ *   than E is taken as E, S <= 0 leaves nothing resident. Errors: MOE_ERR_ARG
+ *   on NULL or E < 1.
+ *
  * moe_plec_order -- the load order of PLEC's cross-layer plan (Sec. 3.4.1):
  *   every (layer, expert) with predicted demand > 0, layers in execution
  *   order, larger demand first, equal demand lower expert id first.
@@ -412,6 +433,7 @@ int moe_combine(const void* y_perm, int32_t dtype, int64_t H, int64_t rows,
  *   slot named twice (nothing is enqueued); MOE_ERR_HIP if a copy cannot be
  *   enqueued.
  * ---------------------------------------------------------------------- */
+int moe_plan_slots(const int32_t* demand, int32_t E, int32_t S, int32_t* slot_of_expert);
 int moe_plec_order(const int32_t* demand, int32_t L, int32_t E, int32_t* items,
                    int32_t* n_items);
 int moe_plec_run(const int32_t* pred_demand, const int32_t* actual_demand, int32_t L,

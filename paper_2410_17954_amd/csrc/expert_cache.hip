@@ -38,6 +38,22 @@ std::vector<Item> load_order(const int32_t* demand, int L, int E) {
 }  // namespace
 }  // namespace moe
 
+extern "C" int moe_plan_slots(const int32_t* demand, int32_t E, int32_t S,
+                              int32_t* slot_of_expert) {
+  MOE_CHECK_ARG(demand && slot_of_expert && E >= 1);
+  std::vector<int32_t> ids(E);
+  for (int32_t e = 0; e < E; ++e) ids[e] = e;
+  // larger demand first; equal demand, lower id first
+  std::stable_sort(ids.begin(), ids.end(),
+                   [&](int32_t a, int32_t b) { return demand[a] > demand[b]; });
+  const int32_t n = S < 0 ? 0 : (S > E ? E : S);
+  std::vector<char> chosen(E, 0);
+  for (int32_t i = 0; i < n; ++i) chosen[ids[i]] = 1;
+  int32_t next = 0;
+  for (int32_t e = 0; e < E; ++e) slot_of_expert[e] = chosen[e] ? next++ : -1;
+  return MOE_OK;
+}
+
 extern "C" int moe_plec_order(const int32_t* demand, int32_t L, int32_t E, int32_t* items,
                               int32_t* n_items) {
   using namespace moe;

@@ -23,7 +23,7 @@
 //            perm by stable compaction, demand, info.
 // All ties go to the lower signature rank. Up to 1024 tokens whose paths fit
 // in LDS run every step in one block (sch_small); otherwise the rounds run in
-// one cooperative launch over tokens laid out in signature order (a per-phase
+// one resident-grid launch over tokens laid out in signature order (a per-phase
 // launch sequence covers shapes beyond its limits). Nothing is read back to
 // the host.
 #include "common.h"
@@ -449,8 +449,8 @@ sch_repack(const uint64_t* __restrict__ bits, const int32_t* __restrict__ ones,
 }
 
 // ------------------------------------------- per-phase launches (fallback)
-// Used when the shapes exceed the cooperative kernel's LDS limits or a
-// cooperative launch is refused; token-index space throughout.
+// Used when the shapes exceed the round-loop kernel's LDS limits or its
+// launch is refused; token-index space throughout.
 // Column counts. mode 0: all tokens -> cnt[0]; mode 1: original split
 // (i < n1 -> cnt[0], else cnt[1]); mode 2: current batches (in1[i] -> cnt[0]).
 // tot[c] accumulates |r_i| of the tokens counted into cnt[c].
@@ -640,8 +640,9 @@ sch_select(int N, int n1, int nbins, int off, const int32_t* __restrict__ delta,
   }
 }
 
-// ------------------------------------------------ cooperative round loop
-// All rounds in one cooperative launch (every block resident). Tokens are
+// ------------------------------------------------ resident-grid round loop
+// All rounds in one launch whose blocks are all resident at once (at most one
+// block per compute unit is needed). Tokens are
 // addressed by signature position r: block b owns a contiguous range of at
 // most PPT * kCoopT positions, thread t positions t0 + t + j kCoopT (j < PPT),
 // and keeps their state (delta, batch) in registers and their path words in
@@ -1205,7 +1206,8 @@ sch_fin_scatter(int N, int n1, int LE, int trivial, const int32_t* __restrict__ 
                 const int32_t* __restrict__ cnt, const int32_t* __restrict__ cnt_orig,
                 const int32_t* __restrict__ blkcnt, const int64_t* __restrict__ state,
                 const int32_t* __restrict__ err, int32_t* __restrict__ perm,
-                int32_t* __restrict__ demand, int64_t* __restrict__ info) {
+                int32_t* __restrict__ demand, int64_t* __restrict__ info,
+                int32_t* __restrict__ err_out) {
   const bool use_orig = state[ST_USE_ORIG] != 0;
   const int i = blockIdx.x * kSel + threadIdx.x;
   if (use_orig) {
@@ -1235,8 +1237,9 @@ sch_fin_scatter(int N, int n1, int LE, int trivial, const int32_t* __restrict__ 
       demand[LE + q] = o0 + o1 - c1;
     }
   if (threadIdx.x == 0) {
-    // a bounded wait that timed out in the cooperative loop marks the result
+    // a bounded wait that timed out in the round loop marks the result
     info[0] = (*err) ? -1 : (trivial ? 0 : state[ST_ITERS]);
+    if (*err && err_out) *err_out = 1;
     info[1] = trivial ? 1 : state[ST_CONV];
     info[2] = trivial ? -1 : state[ST_AM1];
     info[3] = trivial ? -1 : state[ST_AM2];
@@ -1786,8 +1789,8 @@ extern "C" size_t moe_schedule_workspace(int64_t N, int32_t L, int32_t E, int32_
 
 extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t E, int32_t k,
                             int64_t n1, int32_t max_iters, int32_t keep_original_if_worse,
-                            int32_t* perm, int32_t* demand, int64_t* info, void* workspace,
-                            size_t ws_bytes, void* stream) {
+                            int32_t* perm, int32_t* demand, int64_t* info, int32_t* err_out,
+                            void* workspace, size_t ws_bytes, void* stream) {
   using namespace moe;
   MOE_CHECK_ARG(routes && perm && info);
   MOE_CHECK_ARG(N >= 1 && L >= 1 && E >= 1 && E <= 256 && k >= 1 && k <= E);
@@ -1913,10 +1916,20 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
                          : ppt_t == 4 ? reinterpret_cast<const void*>(&sch_coop<4>)
                          : ppt_t == 8 ? reinterpret_cast<const void*>(&sch_coop<8>)
                                       : reinterpret_cast<const void*>(&sch_coop<16>);
+        // An ordinary launch: nb <= compute units and at least one block fits
+        // on a compute unit, so every block becomes resident once the units
+        // are free of other work (blocks of kernels on other streams retire
+        // without waiting for this one); the barrier waits are bounded in
+        // any case. (The cooperative launch API adds nothing to that on this
+        // path; processes that used it faulted in the runtime's teardown at
+        // exit when traced by the profiler.)
+        int per_cu = 0;
         if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) ==
                 hipSuccess &&
-            hipLaunchCooperativeKernel(fn, dim3(nb), dim3(kCoopT), args, (unsigned)lds, st) ==
-                hipSuccess)
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kCoopT, lds) ==
+                hipSuccess &&
+            per_cu >= 1 &&
+            hipLaunchKernel(fn, dim3(nb), dim3(kCoopT), args, lds, st) == hipSuccess)
           done = true;
         else
           (void)hipGetLastError();               // nothing ran: take the per-phase path
@@ -1969,7 +1982,8 @@ extern "C" int moe_schedule(const uint8_t* routes, int64_t N, int32_t L, int32_t
                                              cnt, cnt_orig, blkcnt, state);
   MOE_CHECK_LAUNCH();
   sch_fin_scatter<<<fgrid, dim3(kSel), 0, st>>>(n, (int)n1, LE, trivial ? 1 : 0, in1, cnt,
-                                               cnt_orig, blkcnt, state, err, perm, demand, info);
+                                               cnt_orig, blkcnt, state, err, perm, demand, info,
+                                               err_out);
   MOE_CHECK_LAUNCH();
 #undef MOE_TRY
   return MOE_OK;
@@ -2170,7 +2184,8 @@ extern "C" int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, i
                                   int32_t k, int32_t B, int32_t max_iters,
                                   int32_t keep_original_if_worse, int32_t* perm,
                                   int32_t* batch_offsets, int32_t* demand, int64_t* info,
-                                  void* workspace, size_t ws_bytes, void* stream) {
+                                  int32_t* err_out, void* workspace, size_t ws_bytes,
+                                  void* stream) {
   using namespace moe;
   MOE_CHECK_ARG(routes && perm && batch_offsets);
   MOE_CHECK_ARG(N >= 1 && L >= 1 && E >= 1 && E <= 256 && k >= 1 && k <= E);
@@ -2205,7 +2220,7 @@ extern "C" int moe_schedule_multi(const uint8_t* routes, int64_t N, int32_t L, i
         routes, ids, v.n, row, rt);
     MOE_CHECK_LAUNCH();
     const int rc = moe_schedule(rt, v.n, L, E, k, n1, max_iters, keep_original_if_worse, sub_perm,
-                                nullptr, info_row, sub_ws, sub_bytes, stream);
+                                nullptr, info_row, err_out, sub_ws, sub_bytes, stream);
     if (rc != MOE_OK) return rc;
     const dim3 g((unsigned)ceil_div(v.n, 256));
     sch_multi_compose<<<g, dim3(256), 0, st>>>(ids, sub_perm, v.n, tmp);

@@ -66,8 +66,9 @@ def run_layer(x, topk_idx, topk_w, E, store, cache, slot_of_expert, token_ids=No
     ws = workspaces or {}
     offs, rop, por, xp = ops.permute(x, topk_idx, E, token_ids=token_ids,
                                      workspace=ws.get("permute"))
-    # the misses need the rows per expert on the host (one small copy)
-    counts = torch.diff(offs).cpu().numpy()
+    # the misses need the rows per expert on the host: one small copy of the
+    # offsets, differenced there
+    counts = np.diff(offs.cpu().numpy().astype(np.int64))
     slot_host = np.asarray(slot_of_expert, dtype=np.int32)
     rounds = correction_plan(counts, slot_host, S)
     # every slot table goes up in one transfer, before any cross-stream wait

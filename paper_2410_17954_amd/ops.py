@@ -46,7 +46,7 @@ def load_library(path=None):
         "moe_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "moe_route": (I32, [P, P, I32, I64, I64, I32, I32, P, I32, I32, P, P, P, P]),
         "moe_schedule_workspace": (SZ, [I64, I32, I32, I32]),
-        "moe_schedule": (I32, [P, I64, I32, I32, I32, I64, I32, I32, P, P, P, P, SZ, P]),
+        "moe_schedule": (I32, [P, I64, I32, I32, I32, I64, I32, I32, P, P, P, P, P, SZ, P]),
         "moe_kv_gather": (I32, [P, P, I32, I64, I64, P, I64, P, P, P]),
         "moe_kv_reindex": (I32, [P, I64, P, I32, P, P, P, P]),
         "moe_stack_workspace": (SZ, [I64, I64, I64, I32, I32, I32]),
@@ -58,14 +58,15 @@ def load_library(path=None):
         "moe_rpp_workspace": (SZ, [I32, I32, P]),
         "moe_rpp_forward": (I32, [P, I32, I32, P, P, P, P, P, P, SZ, P]),
         "moe_schedule_multi_workspace": (SZ, [I64, I32, I32, I32, I32]),
-        "moe_schedule_multi": (I32, [P, I64, I32, I32, I32, I32, I32, I32, P, P, P, P, P, SZ,
-                                     P]),
+        "moe_schedule_multi": (I32, [P, I64, I32, I32, I32, I32, I32, I32, P, P, P, P, P, P,
+                                     SZ, P]),
         "moe_permute_workspace": (SZ, [I64, I32, I32]),
         "moe_permute": (I32, [P, I32, I64, I64, P, I64, P, I32, I32, P, P, P, P, P, SZ, P]),
         "moe_expert_ffn_workspace": (SZ, [I64, I64, I64, I32, I32]),
         "moe_expert_ffn": (I32, [P, I32, I64, I64, I64, P, I32, P, I32, P, P, P, P, P, SZ, P]),
         "moe_combine": (I32, [P, I32, I64, I64, P, I64, I64, I32, P, P, P, P, I32, P, I32, P,
                               P, P]),
+        "moe_plan_slots": (I32, [P, I32, I32, P]),
         "moe_plec_order": (I32, [P, I32, I32, P, P]),
         "moe_plec_run": (I32, [P, P, I32, I32, I32, P, P, P, P, P]),
         "moe_lru_run": (I32, [P, I32, I32, I32, I32, P, P]),
@@ -86,7 +87,7 @@ def exported_symbols():
             "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_kv_gather",
             "moe_kv_reindex", "moe_stack_workspace", "moe_stack_forward",
             "moe_rpp_weights_count", "moe_rpp_workspace", "moe_rpp_forward",
-            "moe_probe_mfma_bf16", "moe_probe_read", "moe_plec_order",
+            "moe_probe_mfma_bf16", "moe_probe_read", "moe_plan_slots", "moe_plec_order",
             "moe_plec_run", "moe_lru_run", "moe_load_experts"]
 
 
@@ -196,9 +197,10 @@ def schedule_workspace(N, L, E, k):
 
 def schedule(routes, E, n1=None, max_iters=10, keep_original_if_worse=True,
              perm=None, demand=None, info=None, workspace=None, want_demand=True,
-             stream=None):
+             err=None, stream=None):
     """moe_schedule over routes uint8 [N, L, k]. Returns (perm int32 [N],
-    demand int32 [2, L, E] or None, info int64 [8])."""
+    demand int32 [2, L, E] or None, info int64 [8]). err: optional device
+    int32 [1] that the call sets to 1 when its result is not to be trusted."""
     torch = _torch()
     lib = load_library()
     _dev(routes)
@@ -214,9 +216,10 @@ def schedule(routes, E, n1=None, max_iters=10, keep_original_if_worse=True,
     if info is None:
         info = torch.empty(8, dtype=torch.int64, device=dev)
     ws, nbytes = _workspace(lib.moe_schedule_workspace(N, L, E, k), dev, workspace)
+    _dev(err)
     st = lib.moe_schedule(_ptr(routes), N, L, E, k, n1, max_iters,
                           1 if keep_original_if_worse else 0, _ptr(perm), _ptr(demand),
-                          _ptr(info), _ptr(ws), nbytes, _stream(stream))
+                          _ptr(info), _ptr(err), _ptr(ws), nbytes, _stream(stream))
     _check("moe_schedule", st)
     return perm, demand, info
 
@@ -227,10 +230,10 @@ def schedule_multi_workspace(N, L, E, k, B):
 
 def schedule_multi(routes, E, B, max_iters=10, keep_original_if_worse=True, perm=None,
                    batch_offsets=None, demand=None, info=None, workspace=None,
-                   want_demand=True, want_info=True, stream=None):
+                   want_demand=True, want_info=True, err=None, stream=None):
     """moe_schedule_multi over routes uint8 [N, L, k] into B batches. Returns
     (perm int32 [N], batch_offsets int32 [B+1], demand int32 [B, L, E] or None,
-    info int64 [B-1, 8] or None)."""
+    info int64 [B-1, 8] or None). err: as for schedule."""
     torch = _torch()
     lib = load_library()
     _dev(routes)
@@ -247,10 +250,11 @@ def schedule_multi(routes, E, B, max_iters=10, keep_original_if_worse=True, perm
     if info is None and want_info and B > 1:
         info = torch.empty((B - 1, 8), dtype=torch.int64, device=dev)
     ws, nbytes = _workspace(lib.moe_schedule_multi_workspace(N, L, E, k, B), dev, workspace)
+    _dev(err)
     st = lib.moe_schedule_multi(_ptr(routes), N, L, E, k, B, max_iters,
                                 1 if keep_original_if_worse else 0, _ptr(perm),
-                                _ptr(batch_offsets), _ptr(demand), _ptr(info), _ptr(ws), nbytes,
-                                _stream(stream))
+                                _ptr(batch_offsets), _ptr(demand), _ptr(info), _ptr(err),
+                                _ptr(ws), nbytes, _stream(stream))
     _check("moe_schedule_multi", st)
     return perm, batch_offsets, demand, info
 
@@ -503,18 +507,15 @@ def combine(y_perm, topk_idx, topk_w, row_of_pair, token_ids=None, slot_of_exper
 
 # ------------------------------------------------------------------ slot table
 def plan_slots(demand, S):
-    """Resident set of one layer from predicted demand (host, the planning step
-    of the expert cache, Sec. 3.4.1): the S experts with the largest demand
-    (equal demand: lower id first) occupy slots 0..S-1 in ascending expert id;
-    slot -1 marks a non-resident expert. demand: int [E]. Returns int32 [E]."""
-    demand = np.asarray(demand).astype(np.int64)
-    E = demand.shape[0]
-    S = max(0, min(int(S), E))
-    # sort key: larger demand first, then lower id
-    keyed = sorted(range(E), key=lambda e: (-int(demand[e]), e))[:S]
-    slot = np.full(E, -1, dtype=np.int32)
-    for s_idx, e in enumerate(sorted(keyed)):
-        slot[e] = s_idx
+    """moe_plan_slots: the resident set of one layer from predicted demand
+    int [E] (host). Returns slot_of_expert int32 [E] (-1 = not resident)."""
+    lib = load_library()
+    d = np.ascontiguousarray(np.asarray(demand), dtype=np.int32)
+    if d.ndim != 1:
+        raise ValueError("demand must be [E]")
+    slot = np.empty(d.shape[0], dtype=np.int32)
+    _check("moe_plan_slots", lib.moe_plan_slots(d.ctypes.data_as(ctypes.c_void_p), d.shape[0],
+                                                int(S), slot.ctypes.data_as(ctypes.c_void_p)))
     return slot
 
 

@@ -8,6 +8,8 @@ With `overlap` the scheduling of unit u+1 (token scheduler, KV merge/reindex)
 runs on a second stream while unit u's layers run on the main stream; unit
 u+1's layers wait for it through an event. Without it everything runs in
 order on the main stream. Both orders give the same results bit for bit.
+A plan's err word is set when the scheduler's result is not to be trusted or
+a KV index is out of range; the caller checks it.
 
 Every step is a call of libmoeflow; this module only orders them on streams.
 Routing prediction (Sec. 3.2) is outside the path: each unit carries its
@@ -70,15 +72,21 @@ class DualBatchPipeline:
         torch = self.torch
         N, L_pred, k = unit.routes.shape
         p = UnitPlan()
+        if self.overlap:
+            # the side stream reads these; the caching allocator must not hand
+            # their memory out again before it has
+            unit.routes.record_stream(self.side)
+            for kv in unit.kv:
+                kv.record_stream(self.side)
         with torch.cuda.stream(self.side):
             key = (N, L_pred, k)
             if key not in self._sched_ws:
                 self._sched_ws[key] = ops.workspace_tensor(
                     ops.schedule_multi_workspace(N, L_pred, self.E, k, 2), self.dev)
+            p.err = torch.zeros(1, dtype=torch.int32, device=self.dev)
             p.perm, p.offsets, p.demand, p.info = ops.schedule_multi(
                 unit.routes, self.E, 2, max_iters=self.max_iters,
-                keep_original_if_worse=self.keep, workspace=self._sched_ws[key])
-            p.err = torch.zeros(1, dtype=torch.int32, device=self.dev)
+                keep_original_if_worse=self.keep, workspace=self._sched_ws[key], err=p.err)
             if unit.kv:
                 p.kv_new, _ = ops.kv_gather(unit.kv, index=p.perm, err=p.err)
             p.batch_of, p.pos_of, _ = ops.kv_reindex(p.perm, p.offsets, err=p.err)
@@ -109,6 +117,13 @@ class DualBatchPipeline:
         plans = []
         if not units:
             return plans
+        if self.overlap:
+            # whatever the caller enqueued on the main stream before this call
+            # (the units' routes, KV caches, hidden states) is complete before
+            # the side stream reads it
+            produced = self.torch.cuda.Event()
+            produced.record(self.main)
+            self.side.wait_event(produced)
         nxt = self._plan(units[0])
         for u, unit in enumerate(units):
             cur = nxt

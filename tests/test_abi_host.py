@@ -30,14 +30,14 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 25, names
+    assert len(names) == 26, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
 
 
 def test_version_and_status_strings(lib):
-    assert lib.moe_abi_version() == 1
+    assert lib.moe_abi_version() == 2
     for s in range(5):
         assert lib.moe_status_str(s)
     assert lib.moe_status_str(99) == b"unknown status"
@@ -59,7 +59,7 @@ def test_schedule_multi_rejects_bad_arguments(lib):
     S = None
     ws = lib.moe_schedule_multi_workspace(16, 2, 8, 2, 4)
     args = lambda N, E, k, B, perm=FAKE, off=FAKE, it=3, keep=1, nbytes=ws: lib.moe_schedule_multi(
-        FAKE, N, 2, E, k, B, it, keep, perm, off, S, S, FAKE, nbytes, S)
+        FAKE, N, 2, E, k, B, it, keep, perm, off, S, S, S, FAKE, nbytes, S)
     assert args(0, 8, 2, 4) == ops.MOE_ERR_ARG            # no tokens
     assert args(16, 8, 2, 0) == ops.MOE_ERR_ARG           # no batches
     assert args(16, 8, 2, 4097) == ops.MOE_ERR_ARG        # too many batches
@@ -88,11 +88,12 @@ def test_route_rejects_bad_arguments(lib):
 
 def test_schedule_rejects_bad_arguments(lib):
     S = None
-    ok = (FAKE, 64, 4, 8, 2, 32, 10, 1, FAKE, FAKE, FAKE)
-    bad_n1 = (FAKE, 64, 4, 8, 2, 65, 10, 1, FAKE, FAKE, FAKE)
+    ok = (FAKE, 64, 4, 8, 2, 32, 10, 1, FAKE, FAKE, FAKE, S)
+    bad_n1 = (FAKE, 64, 4, 8, 2, 65, 10, 1, FAKE, FAKE, FAKE, S)
     assert lib.moe_schedule(*bad_n1, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
-    assert lib.moe_schedule(FAKE, 64, 4, 8, 2, 32, 0, 1, FAKE, FAKE, FAKE, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
-    assert lib.moe_schedule(FAKE, 64, 4, 8, 9, 32, 10, 1, FAKE, FAKE, FAKE, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_schedule(FAKE, 64, 4, 8, 2, 32, 0, 1, FAKE, FAKE, FAKE, S, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_schedule(FAKE, 64, 4, 8, 9, 32, 10, 1, FAKE, FAKE, FAKE, S, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
+    assert lib.moe_schedule(S, 64, 4, 8, 2, 32, 10, 1, FAKE, FAKE, FAKE, S, FAKE, 1 << 20, S) == ops.MOE_ERR_ARG
     assert lib.moe_schedule(*ok, S, 0, S) == ops.MOE_ERR_WORKSPACE
     assert lib.moe_schedule(*ok, FAKE, 16, S) == ops.MOE_ERR_WORKSPACE
     assert lib.moe_schedule(*ok, ctypes.c_void_p(0x1001), 1 << 20, S) == ops.MOE_ERR_WORKSPACE
@@ -127,12 +128,25 @@ def test_combine_rejects_bad_arguments(lib):
     assert lib.moe_combine(S, 1, 64, 10, S, 5, 5, 2, FAKE, FAKE, FAKE, S, 0, S, 0, FAKE, S, S) == ops.MOE_ERR_ARG
 
 
-def test_plan_slots_host_rule():
+def test_plan_slots_host_rule(lib):
     import numpy as np
+    import oracle
     slot = ops.plan_slots(np.array([5, 0, 9, 5, 1]), 3)
     assert slot.tolist() == [0, -1, 1, 2, -1]
     assert ops.plan_slots(np.array([1, 2]), 0).tolist() == [-1, -1]
+    assert ops.plan_slots(np.array([1, 2]), -3).tolist() == [-1, -1]
     assert ops.plan_slots(np.array([1, 2]), 5).tolist() == [0, 1]
+    assert ops.plan_slots(np.zeros(6, np.int32), 2).tolist() == [0, 1, -1, -1, -1, -1]
+    # the library's rule against the oracle's on random demand with many ties
+    g = np.random.default_rng(3)
+    for _ in range(200):
+        E = int(g.integers(1, 70))
+        d = g.integers(0, 5, size=E)
+        S = int(g.integers(-1, E + 3))
+        assert ops.plan_slots(d, S).tolist() == oracle.plan_slots(d, S).tolist()
+    S = None
+    assert lib.moe_plan_slots(S, 4, 2, FAKE) == ops.MOE_ERR_ARG
+    assert lib.moe_plan_slots(FAKE, 0, 2, FAKE) == ops.MOE_ERR_ARG
 
 
 def test_kv_and_stack_reject_bad_arguments(lib):

@@ -77,3 +77,34 @@ def test_single_unit_and_no_kv():
     torch.cuda.synchronize()
     assert plans[0].kv_new is None
     assert sorted(to_host(plans[0].perm).tolist()) == list(range(N))
+
+
+def test_inputs_produced_on_the_main_stream_are_waited_for():
+    # The units' routes, KV caches and hidden states are written on the main
+    # stream behind a long kernel just before run(): the side stream's
+    # scheduling must see the written values, so the plans and outputs equal
+    # those of the in-order run on inputs that were complete beforehand.
+    layers, units, (N, E, k) = _setup(n_units=2, seed=5)
+    ref = _dev_units(units)
+    ref_plans = pipeline.DualBatchPipeline(layers, k, E, N, overlap=False).run(ref)
+    torch.cuda.synchronize()
+    src = _dev_units(units)
+    torch.cuda.synchronize()
+    us = [pipeline.Unit(h=torch.empty_like(u.h), routes=torch.empty_like(u.routes),
+                        kv=[torch.empty_like(c) for c in u.kv]) for u in src]
+    for u in us:                       # garbage that a racing reader would see
+        u.routes.fill_(255)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(50_000_000)      # holds the main stream for tens of ms
+    for u, s in zip(us, src):
+        u.h.copy_(s.h)
+        u.routes.copy_(s.routes)
+        for c, d in zip(u.kv, s.kv):
+            c.copy_(d)
+    plans = pipeline.DualBatchPipeline(layers, k, E, N, overlap=True).run(us)
+    torch.cuda.synchronize()
+    for u, r, p, rp in zip(us, ref, plans, ref_plans):
+        assert np.array_equal(to_host(p.perm), to_host(rp.perm))
+        assert np.array_equal(to_host(p.kv_new), to_host(rp.kv_new))
+        assert np.array_equal(to_host(u.h), to_host(r.h))
+        assert to_host(p.err)[0] == 0

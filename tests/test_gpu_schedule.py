@@ -5,6 +5,7 @@ import os
 
 import numpy as np
 import pytest
+import torch
 
 import oracle
 from paper_2410_17954_amd import ops, synth
@@ -16,9 +17,11 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 def _check(routes, E, n1=None, max_iters=10, keep=True):
     routes = np.ascontiguousarray(routes, dtype=np.uint8)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda:0")
     perm, demand, info = ops.schedule(to_dev(routes), E, n1=n1, max_iters=max_iters,
-                                      keep_original_if_worse=keep)
+                                      keep_original_if_worse=keep, err=err)
     rp, rd, ri = oracle.schedule(routes, E, n1, max_iters, keep)
+    assert to_host(err)[0] == 0, "every grid barrier of the round loop completed"
     assert to_host(info).tolist() == ri.tolist()
     assert np.array_equal(to_host(perm), rp)
     assert np.array_equal(to_host(demand), rd)
@@ -119,9 +122,11 @@ def test_long_paths_read_from_memory():
 # ----------------------------------------------------------------- B batches
 def _check_multi(routes, E, B, max_iters=10, keep=True):
     routes = np.ascontiguousarray(routes, dtype=np.uint8)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda:0")
     perm, off, demand, info = ops.schedule_multi(to_dev(routes), E, B, max_iters=max_iters,
-                                                 keep_original_if_worse=keep)
+                                                 keep_original_if_worse=keep, err=err)
     rp, ro, rd, ri = oracle.schedule_multi(routes, E, B, max_iters, keep)
+    assert to_host(err)[0] == 0
     assert to_host(off).tolist() == ro.tolist()
     if B > 1:
         assert to_host(info).tolist() == ri.tolist()
