@@ -321,6 +321,33 @@ int moe_permute(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
                 void* x_perm, void* workspace, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * moe_permute_noalloc -- moe_permute for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the same computation, outputs and argument rules,
+ * without a workspace argument. Its scratch is a static device array of
+ * MOE_PERMUTE_NOALLOC_SCRATCH_BYTES inside the library; every device the
+ * library runs on holds its own copy until the process ends. The first call
+ * on a device looks up that copy's address (with the device current) and
+ * keeps it; no call allocates or frees anything.
+ * Every call on one device shares that device's array and leaves its contents
+ * behind (nothing in it needs clearing: each call writes every word it reads):
+ * calls that may overlap on one device -- on different streams, or from
+ * different threads without ordering -- race and must not be issued; calls on
+ * one stream are ordered and safe.
+ * Limit: moe_permute_workspace(T, k, E) <= MOE_PERMUTE_NOALLOC_SCRATCH_BYTES
+ *   (4 MiB: about 33.5 million tokens with E = 8, k = 2; 2.2 million with
+ *   E = 60, k = 4; 262016 with E = 256, k = 8); a larger call returns
+ *   MOE_ERR_WORKSPACE and enqueues nothing. MOE_ERR_HIP if the array's
+ *   address cannot be looked up.
+ * ---------------------------------------------------------------------- */
+#define MOE_PERMUTE_NOALLOC_SCRATCH_BYTES (4 * 1024 * 1024)
+int moe_permute_noalloc(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
+                        const int32_t* token_ids, int64_t T,
+                        const int32_t* topk_idx, int32_t k, int32_t E,
+                        int32_t* expert_offsets, int32_t* row_of_pair, int32_t* pair_of_row,
+                        void* x_perm, void* stream);
+
+/* ------------------------------------------------------------------------
  * moe_expert_ffn -- the experts E_i of Sec. 2.1 in SwiGLU form, over the rows
  * each expert owns, for experts resident in the expert cache (Sec. 3.4):
  *

@@ -20,6 +20,7 @@
 #include "common.h"
 
 #include <algorithm>
+#include <mutex>
 
 namespace moe {
 namespace {
@@ -334,35 +335,24 @@ extern "C" size_t moe_permute_workspace(int64_t T, int32_t k, int32_t E) {
   return align_up((size_t)(2 * nchunks * E + E) * sizeof(int32_t), 256);
 }
 
-extern "C" int moe_permute(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
-                           const int32_t* token_ids, int64_t T, const int32_t* topk_idx,
-                           int32_t k, int32_t E, int32_t* expert_offsets,
-                           int32_t* row_of_pair, int32_t* pair_of_row, void* x_perm,
-                           void* workspace, size_t ws_bytes, void* stream) {
-  using namespace moe;
-  MOE_CHECK_ARG(T >= 1 && k >= 1 && E >= 1 && E <= 256 && k <= E);
-  MOE_CHECK_ARG(n_tokens >= 1 && (token_ids != nullptr || n_tokens >= T));
-  MOE_CHECK_ARG(topk_idx && expert_offsets && row_of_pair && pair_of_row);
-  MOE_CHECK_ARG((x == nullptr) == (x_perm == nullptr));
+namespace moe {
+namespace {
+
+// Validation and launches shared by moe_permute and moe_permute_noalloc;
+// `workspace` holds at least moe_permute_workspace(T, k, E) bytes.
+int permute_run(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
+                const int32_t* token_ids, int64_t T, const int32_t* topk_idx, int32_t k,
+                int32_t E, int32_t* expert_offsets, int32_t* row_of_pair, int32_t* pair_of_row,
+                void* x_perm, void* workspace, hipStream_t st) {
   const int64_t P = T * (int64_t)k;
-  MOE_CHECK_ARG(P < ((int64_t)1 << 31));
   int64_t row_vecs = 0;
-  if (x) {
-    MOE_CHECK_ARG(valid_dtype(dtype) && H >= 1);
-    const int64_t elt = dtype == MOE_BF16 ? 2 : 4;
-    if ((H * elt) % 16 != 0) return MOE_ERR_UNSUPPORTED;
-    row_vecs = H * elt / 16;
-  }
-  const size_t need = moe_permute_workspace(T, k, E);
-  if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255))
-    return MOE_ERR_WORKSPACE;
+  if (x) row_vecs = H * (dtype == MOE_BF16 ? 2 : 4) / 16;
   const int64_t ct = perm_chunk_tokens(T, k);
   const int64_t nchunks = ceil_div(T, ct);
   if (nchunks > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
   int32_t* counts = static_cast<int32_t*>(workspace);
   int32_t* chunk_base = counts + nchunks * E;
   int32_t* totals = chunk_base + nchunks * E;
-  hipStream_t st = as_stream(stream);
   PairSrc src{token_ids, topk_idx, n_tokens, k, E};
   perm_count_kernel<<<dim3((unsigned)nchunks), dim3(kPermThreads), 0, st>>>(src, P, ct * k, counts);
   MOE_CHECK_LAUNCH();
@@ -383,4 +373,97 @@ extern "C" int moe_permute(const void* x, int32_t dtype, int64_t H, int64_t n_to
   }
   MOE_CHECK_LAUNCH();
   return MOE_OK;
+}
+
+// Host-side argument checks of both entry points (nothing is enqueued when
+// they fail).
+int permute_check(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
+                  const int32_t* token_ids, int64_t T, const int32_t* topk_idx, int32_t k,
+                  int32_t E, const int32_t* expert_offsets, const int32_t* row_of_pair,
+                  const int32_t* pair_of_row, const void* x_perm) {
+  MOE_CHECK_ARG(T >= 1 && k >= 1 && E >= 1 && E <= 256 && k <= E);
+  MOE_CHECK_ARG(n_tokens >= 1 && (token_ids != nullptr || n_tokens >= T));
+  MOE_CHECK_ARG(topk_idx && expert_offsets && row_of_pair && pair_of_row);
+  MOE_CHECK_ARG((x == nullptr) == (x_perm == nullptr));
+  MOE_CHECK_ARG(T * (int64_t)k < ((int64_t)1 << 31));
+  if (x) {
+    MOE_CHECK_ARG(valid_dtype(dtype) && H >= 1);
+    const int64_t elt = dtype == MOE_BF16 ? 2 : 4;
+    if ((H * elt) % 16 != 0) return MOE_ERR_UNSUPPORTED;
+  }
+  return MOE_OK;
+}
+
+}  // namespace
+}  // namespace moe
+
+extern "C" int moe_permute(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
+                           const int32_t* token_ids, int64_t T, const int32_t* topk_idx,
+                           int32_t k, int32_t E, int32_t* expert_offsets,
+                           int32_t* row_of_pair, int32_t* pair_of_row, void* x_perm,
+                           void* workspace, size_t ws_bytes, void* stream) {
+  using namespace moe;
+  const int rc = permute_check(x, dtype, H, n_tokens, token_ids, T, topk_idx, k, E,
+                               expert_offsets, row_of_pair, pair_of_row, x_perm);
+  if (rc != MOE_OK) return rc;
+  const size_t need = moe_permute_workspace(T, k, E);
+  if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return MOE_ERR_WORKSPACE;
+  return permute_run(x, dtype, H, n_tokens, token_ids, T, topk_idx, k, E, expert_offsets,
+                     row_of_pair, pair_of_row, x_perm, workspace, as_stream(stream));
+}
+
+// ------------------------------------------------------------ no allocation
+// moe_permute_noalloc takes its scratch from this array instead of a caller's
+// workspace. Each device holds its own copy for the life of the process; host
+// code never passes the array's name to a kernel (on the host it is only a
+// stand-in for the symbol), only the device address looked up for the current
+// device with hipGetSymbolAddress.
+static __device__ __align__(256) int32_t scratch[MOE_PERMUTE_NOALLOC_SCRATCH_BYTES / 4];
+
+namespace moe {
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+hipError_t scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+}  // namespace
+}  // namespace moe
+
+extern "C" int moe_permute_noalloc(const void* x, int32_t dtype, int64_t H, int64_t n_tokens,
+                                   const int32_t* token_ids, int64_t T,
+                                   const int32_t* topk_idx, int32_t k, int32_t E,
+                                   int32_t* expert_offsets, int32_t* row_of_pair,
+                                   int32_t* pair_of_row, void* x_perm, void* stream) {
+  using namespace moe;
+  const int rc = permute_check(x, dtype, H, n_tokens, token_ids, T, topk_idx, k, E,
+                               expert_offsets, row_of_pair, pair_of_row, x_perm);
+  if (rc != MOE_OK) return rc;
+  if (moe_permute_workspace(T, k, E) > (size_t)MOE_PERMUTE_NOALLOC_SCRATCH_BYTES)
+    return MOE_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (scratch_address(&ws) != hipSuccess) {
+    (void)hipGetLastError();
+    return MOE_ERR_HIP;
+  }
+  return permute_run(x, dtype, H, n_tokens, token_ids, T, topk_idx, k, E, expert_offsets,
+                     row_of_pair, pair_of_row, x_perm, ws, as_stream(stream));
 }

@@ -62,6 +62,7 @@ def load_library(path=None):
                                      SZ, P]),
         "moe_permute_workspace": (SZ, [I64, I32, I32]),
         "moe_permute": (I32, [P, I32, I64, I64, P, I64, P, I32, I32, P, P, P, P, P, SZ, P]),
+        "moe_permute_noalloc": (I32, [P, I32, I64, I64, P, I64, P, I32, I32, P, P, P, P, P]),
         "moe_expert_ffn_workspace": (SZ, [I64, I64, I64, I32, I32]),
         "moe_expert_ffn": (I32, [P, I32, I64, I64, I64, P, I32, P, I32, P, P, P, P, P, SZ, P]),
         "moe_combine": (I32, [P, I32, I64, I64, P, I64, I64, I32, P, P, P, P, I32, P, I32, P,
@@ -83,7 +84,7 @@ def load_library(path=None):
 def exported_symbols():
     return ["moe_abi_version", "moe_status_str", "moe_route", "moe_schedule_workspace",
             "moe_schedule", "moe_schedule_multi_workspace", "moe_schedule_multi",
-            "moe_permute_workspace", "moe_permute",
+            "moe_permute_workspace", "moe_permute", "moe_permute_noalloc",
             "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_kv_gather",
             "moe_kv_reindex", "moe_stack_workspace", "moe_stack_forward",
             "moe_rpp_weights_count", "moe_rpp_workspace", "moe_rpp_forward",
@@ -443,6 +444,34 @@ def permute(x, topk_idx, E, token_ids=None, T=None, expert_offsets=None, row_of_
                          _ptr(row_of_pair), _ptr(pair_of_row), _ptr(x_perm), _ptr(ws), nbytes,
                          _stream(stream))
     _check("moe_permute", st)
+    return expert_offsets, row_of_pair, pair_of_row, x_perm
+
+
+def permute_noalloc(x, topk_idx, E, expert_offsets, row_of_pair, pair_of_row, x_perm=None,
+                    token_ids=None, T=None, stream=None):
+    """moe_permute_noalloc: moe_permute into outputs the caller allocated
+    beforehand, with the library's static scratch instead of a workspace
+    (nothing is allocated). Calls that may overlap on one device race."""
+    lib = load_library()
+    _dev(x, topk_idx, token_ids, expert_offsets, row_of_pair, pair_of_row, x_perm)
+    n_tokens, k = topk_idx.shape
+    if T is None:
+        T = token_ids.shape[0] if token_ids is not None else n_tokens
+    if (x is None) != (x_perm is None):
+        raise ValueError("x and x_perm go together")
+    if (expert_offsets.numel() < E + 1 or row_of_pair.numel() < T * k
+            or pair_of_row.numel() < T * k):
+        raise ValueError("output maps too small")
+    dt, H = MOE_F32, 0
+    if x is not None:
+        dt, H = _dtype_code(x), x.shape[1]
+        if x_perm.dtype != x.dtype or x_perm.shape[1] != H or x_perm.shape[0] < T * k:
+            raise ValueError("x_perm must be [T*k, H] of x's dtype")
+    st = lib.moe_permute_noalloc(_ptr(x), dt, H, x.shape[0] if x is not None else n_tokens,
+                                 _ptr(token_ids), T, _ptr(topk_idx), k, E,
+                                 _ptr(expert_offsets), _ptr(row_of_pair), _ptr(pair_of_row),
+                                 _ptr(x_perm), _stream(stream))
+    _check("moe_permute_noalloc", st)
     return expert_offsets, row_of_pair, pair_of_row, x_perm
 
 

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 26, names
+    assert len(names) == 27, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
@@ -197,3 +197,16 @@ def test_rpp_weight_count_and_bad_arguments(lib):
     assert call(gg=odd, nbytes=lib.moe_rpp_workspace(2, 8, ctypes.byref(odd))) == \
         ops.MOE_ERR_UNSUPPORTED
     assert call(nbytes=ws - 1) == ops.MOE_ERR_WORKSPACE
+
+
+def test_permute_noalloc_rejects_on_the_host(lib):
+    S = None
+    # beyond the static scratch (300000 tokens, 256 experts, top-8)
+    assert lib.moe_permute_workspace(300000, 8, 256) > 4 * 1024 * 1024
+    assert lib.moe_permute_noalloc(S, 0, 0, 300000, S, 300000, FAKE, 8, 256, FAKE, FAKE, FAKE, S,
+                                   S) == ops.MOE_ERR_WORKSPACE
+    # the argument rules of moe_permute
+    assert lib.moe_permute_noalloc(S, 0, 0, 10, S, 10, S, 2, 8, FAKE, FAKE, FAKE, S, S) == ops.MOE_ERR_ARG
+    assert lib.moe_permute_noalloc(S, 0, 0, 10, S, 10, FAKE, 9, 8, FAKE, FAKE, FAKE, S, S) == ops.MOE_ERR_ARG
+    assert lib.moe_permute_noalloc(FAKE, 1, 64, 10, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, S, S) == ops.MOE_ERR_ARG
+    assert lib.moe_permute_noalloc(FAKE, 1, 60, 10, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, FAKE, S) == ops.MOE_ERR_UNSUPPORTED
