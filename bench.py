@@ -58,6 +58,11 @@ def parse():
                         "and reindexed) with and without the scheduling stream overlapped")
     p.add_argument("--stack-layers", type=int, default=32)
     p.add_argument("--stack-units", type=int, default=3)
+    p.add_argument("--stack-predictor", action="store_true",
+                   help="with --stack: units carry token ids (16 sequences of 512) and each "
+                        "unit's plan runs the routing path predictor (hidden 32, FFN 2048, "
+                        "random weights) and the per-layer top-2 of its logits before the "
+                        "token scheduler")
     p.add_argument("--rpp", action="store_true",
                    help="instead of the layer throughput, time the routing path predictor's "
                         "forward pass (16 sequences of 512 tokens, hidden 32, FFN 2048, random "
@@ -66,6 +71,14 @@ def parse():
                    help="instead of the layer throughput, time the two-way token scheduler on "
                         "Mixtral-shaped 32-layer predicted routes from 1024 to 2^20 tokens: "
                         "us per call, Eq. 2 before and after, effective GB/s")
+    p.add_argument("--route-grouped", action="store_true",
+                   help="instead of the all-resident Mixtral-shaped layer, time the route-grouped "
+                        "one: 8192 tokens scheduled into two batches by 32-layer predicted "
+                        "routes, 4 of 8 experts resident per batch, misses flagged")
+    p.add_argument("--qwen", action="store_true",
+                   help="instead of the Mixtral-shaped layer, time the Qwen1.5-MoE-shaped one: "
+                        "8192 tokens, 60 experts with a Zipf-skewed router, 32 resident, four "
+                        "shared experts; the FFN also split at the ridge (315 rows)")
     p.add_argument("--deepseek", action="store_true",
                    help="instead of the Mixtral-shaped layer, time the DeepSeek-V2-Lite-shaped "
                         "one: 32768 tokens scheduled into two batches by 26-layer predicted "
@@ -445,27 +458,84 @@ def sched_sweep_report(args):
     print(json.dumps(rec))
 
 
-def deepseek_report(args):
-    """DeepSeek-V2-Lite-shaped layer (H 2048, 64 routed experts of width 1408,
-    top-6, two shared experts as one FFN of width 2816): one step schedules
-    32768 tokens into two batches of 16384 by 26-layer predicted routes,
+def _median_ms(torch, fn, reps=7):
+    """Median of HIP-event times of fn() on the current stream (after one
+    untimed call), each behind a short device sleep so that host launch time
+    is not counted."""
+    fn()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000000)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return float(np.median(ts))
+
+
+def _rate(nbytes, ms):
+    return {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
+            "hbm_frac": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 3)}
+
+
+def _mfma(flop, ms):
+    return {"ms": round(ms, 4), "TFLOP/s": round(flop / ms / 1e9, 1),
+            "mfma_frac": round(flop / ms / 1e9 / PEAK_BF16_TFLOPS, 3)}
+
+
+def _weight_bound_split(torch, ops, xp, off, counts, slot_np, slot_w, ws_f, yp, H, F, E, dev,
+                        ridge_rows=315):
+    """The FFN of one batch run twice more outside the timed step, once with
+    only the resident experts that have fewer than ridge_rows rows (below the
+    ridge every weight byte serves fewer flops than HBM can feed the MFMA, so
+    these experts are bound by reading their weights) and once with only the
+    others: weight GB/s and HBM fraction of the first, TFLOP/s of the second."""
+    small = np.array([slot_np[e] >= 0 and 0 < counts[e] < ridge_rows for e in range(E)])
+    large = np.array([slot_np[e] >= 0 and counts[e] >= ridge_rows for e in range(E)])
+    out = {"ridge_rows": ridge_rows}
+    for name, sel in (("under_ridge", small), ("over_ridge", large)):
+        if not sel.any():
+            out[name] = None
+            continue
+        sl = np.where(sel, slot_np, -1).astype(np.int32)
+        sl_d = torch.from_numpy(sl).to(dev)
+        ms = _median_ms(torch, lambda: ops.expert_ffn(xp, off, *slot_w, slot_of_expert=sl_d,
+                                                      y_perm=yp, workspace=ws_f))
+        rows = int(counts[sel].sum())
+        wbytes = 3.0 * H * F * 2 * int(sel.sum())
+        rec = {"experts": int(sel.sum()), "rows": rows, "ms": round(ms, 4),
+               "weight_GB/s": round(wbytes / ms / 1e6, 1),
+               "weight_hbm_frac": round(wbytes / ms / 1e6 / PEAK_HBM_GBS, 3),
+               **{k: v for k, v in _mfma(6.0 * H * F * rows, ms).items() if k != "ms"}}
+        out[name] = rec
+    return out
+
+
+def scheduled_layer_report(args, name):
+    """A route-grouped MoE layer (Mixtral-shaped with 4 of 8 experts resident,
+    or DeepSeek-V2-Lite-shaped with 48 of 64 and shared experts): one step
+    schedules N tokens into two batches by multi-layer predicted routes,
     routes all of them (router bias toward each token's predicted layer-0
     experts, so that prediction and routing mostly agree), then per batch
-    permutes, runs the 48 resident experts (the batch's 48 most demanded by
+    permutes, runs the resident experts (the batch's S most demanded by
     prediction; the slot tables and slot weights are set up once, before the
     timed region, as the expert cache would hold them), gathers the batch for
-    the shared experts, runs them, and combines. Tokens/s, per-stage HIP-event
-    times and rates (routed and shared FFN against the bf16 MFMA peak). One
-    JSON line."""
+    the shared experts and runs them (if any), and combines; tokens whose
+    experts are not all resident are flagged (misses). Tokens/s, per-stage
+    HIP-event times and rates (routed and shared FFN against the bf16 MFMA
+    peak), and the FFN of one batch split at the ridge. One JSON line."""
     import torch
     from paper_2410_17954_amd import ops, synth
 
     dev = torch.device("cuda:0")
-    cfg = synth.workload("deepseek_v2_lite_layer")
+    cfg = synth.workload(name)
     N, H, E, F, k, L, S = (cfg[n] for n in ("T", "H", "E", "F", "k", "L", "S"))
     n_s = cfg["n_shared"]
-    inp = synth.layer_inputs(cfg, args.seed, T=N)
-    routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], args.seed)
+    inp = synth.layer_inputs(cfg, cfg["seed"], T=N)
+    routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], cfg["seed"])
     bias = synth.route_boost_bias(routes, 0, E, cfg["boost"], inp.get("bias"))
 
     def up(a):
@@ -476,14 +546,16 @@ def deepseek_report(args):
 
     x, wr, bias_d, routes_d = up(inp["x"]), up(inp["w_router"]), up(bias), up(routes)
     W = {n: up(inp[n]) for n in ("w_gate", "w_up", "w_down")}
-    shared = tuple(up(inp[n])[None] for n in ("shared_gate", "shared_up", "shared_down"))
+    shared = (tuple(up(inp[n])[None] for n in ("shared_gate", "shared_up", "shared_down"))
+              if n_s else None)
     n1 = N // 2
     T = N - n1
     perm = torch.empty(N, dtype=torch.int32, device=dev)
     demand = torch.empty((2, L, E), dtype=torch.int32, device=dev)
     info = torch.empty(8, dtype=torch.int64, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
     ws_s = ops.workspace_tensor(ops.schedule_workspace(N, L, E, k), dev)
-    ops.schedule(routes_d, E, perm=perm, demand=demand, info=info, workspace=ws_s)
+    ops.schedule(routes_d, E, perm=perm, demand=demand, info=info, workspace=ws_s, err=err)
     d_host = demand.cpu().numpy()
     slots, slot_d, slot_w = [], [], []
     for b in range(2):
@@ -493,31 +565,37 @@ def deepseek_report(args):
         slot_d.append(torch.from_numpy(sl).to(dev))
         slot_w.append(tuple(W[n].index_select(0, res).contiguous()
                             for n in ("w_gate", "w_up", "w_down")))
+    del W
     idx = torch.empty((N, k), dtype=torch.int32, device=dev)
     gw = torch.empty((N, k), dtype=torch.float32, device=dev)
     R = T * k
     ws_p = ops.workspace_tensor(ops.permute_workspace(T, k, E), dev)
-    ws_p1 = ops.workspace_tensor(ops.permute_workspace(T, 1, 1), dev)
     ws_f = ops.workspace_tensor(ops.expert_ffn_workspace(R, H, F, E), dev)
-    ws_f1 = ops.workspace_tensor(ops.expert_ffn_workspace(T, H, n_s * F, 1), dev)
-    zeros1 = torch.zeros((N, 1), dtype=torch.int32, device=dev)
+    if n_s:
+        ws_p1 = ops.workspace_tensor(ops.permute_workspace(T, 1, 1), dev)
+        ws_f1 = ops.workspace_tensor(ops.expert_ffn_workspace(T, H, n_s * F, 1), dev)
+        zeros1 = torch.zeros((N, 1), dtype=torch.int32, device=dev)
     bufs = []
     for b in range(2):
-        bufs.append(dict(
-            off=torch.empty(E + 1, dtype=torch.int32, device=dev),
-            rop=torch.empty(R, dtype=torch.int32, device=dev),
-            por=torch.empty(R, dtype=torch.int32, device=dev),
-            xp=torch.empty((R, H), dtype=torch.bfloat16, device=dev),
-            yp=torch.empty((R, H), dtype=torch.bfloat16, device=dev),
-            off1=torch.empty(2, dtype=torch.int32, device=dev),
-            rop1=torch.empty(T, dtype=torch.int32, device=dev),
-            por1=torch.empty(T, dtype=torch.int32, device=dev),
-            xs=torch.empty((T, H), dtype=torch.bfloat16, device=dev),
-            ys=torch.empty((T, H), dtype=torch.bfloat16, device=dev),
-            inc=torch.empty(T, dtype=torch.int32, device=dev)))
+        bf = dict(off=torch.empty(E + 1, dtype=torch.int32, device=dev),
+                  rop=torch.empty(R, dtype=torch.int32, device=dev),
+                  por=torch.empty(R, dtype=torch.int32, device=dev),
+                  xp=torch.empty((R, H), dtype=torch.bfloat16, device=dev),
+                  yp=torch.empty((R, H), dtype=torch.bfloat16, device=dev),
+                  inc=torch.empty(T, dtype=torch.int32, device=dev))
+        if n_s:
+            bf.update(off1=torch.empty(2, dtype=torch.int32, device=dev),
+                      rop1=torch.empty(T, dtype=torch.int32, device=dev),
+                      por1=torch.empty(T, dtype=torch.int32, device=dev),
+                      xs=torch.empty((T, H), dtype=torch.bfloat16, device=dev),
+                      ys=torch.empty((T, H), dtype=torch.bfloat16, device=dev))
+        bufs.append(bf)
     y = torch.zeros((N, H), dtype=torch.bfloat16, device=dev)
-    names = ["schedule", "route", "permute", "expert_ffn", "shared_gather", "shared_ffn",
-             "combine"]
+    names = ["schedule", "route", "permute", "expert_ffn"]
+    if n_s:
+        names += ["shared_gather", "shared_ffn"]
+    names += ["combine"]
+    per_batch = len(names) - 2
 
     def step(ev=None):
         marks = []
@@ -528,7 +606,7 @@ def deepseek_report(args):
                 e.record()
                 marks.append(e)
         mark()
-        ops.schedule(routes_d, E, perm=perm, demand=demand, info=info, workspace=ws_s)
+        ops.schedule(routes_d, E, perm=perm, demand=demand, info=info, workspace=ws_s, err=err)
         mark()
         ops.route(x, wr, k, bias=bias_d, topk_idx=idx, topk_w=gw)
         mark()
@@ -541,14 +619,15 @@ def deepseek_report(args):
             ops.expert_ffn(bf["xp"], bf["off"], *slot_w[b], slot_of_expert=slot_d[b],
                            y_perm=bf["yp"], workspace=ws_f)
             mark()
-            ops.permute(x, zeros1, 1, token_ids=tok, expert_offsets=bf["off1"],
-                        row_of_pair=bf["rop1"], pair_of_row=bf["por1"], x_perm=bf["xs"],
-                        workspace=ws_p1)
-            mark()
-            ops.expert_ffn(bf["xs"], bf["off1"], *shared, y_perm=bf["ys"], workspace=ws_f1)
-            mark()
+            if n_s:
+                ops.permute(x, zeros1, 1, token_ids=tok, expert_offsets=bf["off1"],
+                            row_of_pair=bf["rop1"], pair_of_row=bf["por1"], x_perm=bf["xs"],
+                            workspace=ws_p1)
+                mark()
+                ops.expert_ffn(bf["xs"], bf["off1"], *shared, y_perm=bf["ys"], workspace=ws_f1)
+                mark()
             ops.combine(bf["yp"], idx, gw, bf["rop"], token_ids=tok, slot_of_expert=slot_d[b],
-                        y_shared=bf["ys"], y=y, incomplete=bf["inc"])
+                        y_shared=bf["ys"] if n_s else None, y=y, incomplete=bf["inc"])
             mark()
         return marks
 
@@ -567,10 +646,11 @@ def deepseek_report(args):
         st["schedule"] += m[0].elapsed_time(m[1])
         st["route"] += m[1].elapsed_time(m[2])
         for b in range(2):
-            base = 2 + 5 * b
+            base = 2 + per_batch * b
             for j, n in enumerate(names[2:]):
                 st[n] += m[base + j].elapsed_time(m[base + j + 1])
     st = {n: v / K for n, v in st.items()}
+    assert int(err.item()) == 0, "the scheduler flagged its result"
     idx_h = idx.cpu().numpy()
     perm_h = perm.cpu().numpy()
     resident_pairs = 0
@@ -582,39 +662,162 @@ def deepseek_report(args):
     inc_dev = int(sum(int(bufs[b]["inc"].sum()) for b in range(2)))
     assert inc_dev == incomplete and torch.isfinite(y.float()).all().item()
     ffn_flop = 6.0 * H * F * resident_pairs
-    sh_flop = 6.0 * H * (n_s * F) * N
     bytes_route = N * H * 2 + E * H * 2 + N * E * 4 + N * k * 8
     bytes_perm = N * H * 2 + N * k * H * 2 + N * k * 12
-    bytes_gather = 2 * N * H * 2
-    bytes_comb = N * k * H * 2 + 2 * N * H * 2 + N * k * 12
+    bytes_comb = N * k * H * 2 + (2 if n_s else 1) * N * H * 2 + N * k * 12
     inf = info.cpu().numpy()
-
-    def rate(nbytes, ms):
-        return {"ms": round(ms, 4), "GB/s": round(nbytes / ms / 1e6, 1),
-                "hbm_frac": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 3)}
+    counts0 = np.diff(bufs[0]["off"].cpu().numpy().astype(np.int64))
+    stages = {
+        "schedule": {"ms": round(st["schedule"], 4), "iters": int(inf[0]),
+                     "obj_before": int(inf[4]), "obj_after": int(inf[5])},
+        "route": _rate(bytes_route, st["route"]),
+        "permute": _rate(bytes_perm, st["permute"]),
+        "expert_ffn": _mfma(ffn_flop, st["expert_ffn"]),
+    }
+    if n_s:
+        stages["shared_gather"] = _rate(2 * N * H * 2, st["shared_gather"])
+        stages["shared_ffn"] = _mfma(6.0 * H * (n_s * F) * N, st["shared_ffn"])
+    stages["combine"] = _rate(bytes_comb, st["combine"])
+    split = _weight_bound_split(torch, ops, bufs[0]["xp"], bufs[0]["off"], counts0, slots[0],
+                                slot_w[0], ws_f, bufs[0]["yp"], H, F, E, dev)
+    desc = {"mixtral8x7b_route_grouped": "Mixtral-8x7B-shaped", "deepseek_v2_lite_layer":
+            "DeepSeek-V2-Lite-shaped"}[name]
     rec = {
-        "metric": "DeepSeek-V2-Lite-shaped MoE layer: tokens/s and per-stage rates",
+        "metric": f"{desc} route-grouped MoE layer: tokens/s and per-stage rates",
         "value": N / (ms_step * 1e-3), "unit": "tokens/s", "ms_per_step": ms_step, "steps": K,
         "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"DeepSeek-V2-Lite-shaped MoE layer: {N} tokens scheduled into "
-                               f"two batches by {L}-layer predicted routes (keep {cfg['keep']}, "
-                               f"zipf {cfg['zipf']}), H={H}, E={E}, F={F}, top-{k}, {S} of {E} "
-                               f"experts resident per batch, {n_s} shared experts"},
-        "stages": {
-            "schedule": {"ms": round(st["schedule"], 4), "iters": int(inf[0]),
-                         "obj_before": int(inf[4]), "obj_after": int(inf[5])},
-            "route": rate(bytes_route, st["route"]),
-            "permute": rate(bytes_perm, st["permute"]),
-            "expert_ffn": {"ms": round(st["expert_ffn"], 4),
-                           "TFLOP/s": round(ffn_flop / st["expert_ffn"] / 1e9, 1),
-                           "mfma_frac": round(ffn_flop / st["expert_ffn"] / 1e9 / PEAK_BF16_TFLOPS, 3)},
-            "shared_gather": rate(bytes_gather, st["shared_gather"]),
-            "shared_ffn": {"ms": round(st["shared_ffn"], 4),
-                           "TFLOP/s": round(sh_flop / st["shared_ffn"] / 1e9, 1),
-                           "mfma_frac": round(sh_flop / st["shared_ffn"] / 1e9 / PEAK_BF16_TFLOPS, 3)},
-            "combine": rate(bytes_comb, st["combine"]),
-        },
+        "config": {"workload": f"{desc} MoE layer: {N} tokens scheduled into two batches by "
+                               f"{L}-layer predicted routes (keep {cfg['keep']}, zipf "
+                               f"{cfg['zipf']}), H={H}, E={E}, F={F}, top-{k}, {S} of {E} "
+                               f"experts resident per batch (misses flagged)"
+                               + (f", {n_s} shared experts" if n_s else ""),
+                   "router_boost": cfg["boost"]},
+        "stages": stages,
+        "batch0_ffn_by_ridge": split,
+        "batch0_rows_per_expert": counts0.tolist(),
         "resident_pair_share": round(resident_pairs / (N * k), 4),
+        "incomplete_tokens": incomplete,
+    }
+    print(json.dumps(rec))
+
+
+def qwen_report(args):
+    """Qwen1.5-MoE-shaped layer (H 2048, 60 routed experts of width 1408,
+    top-4, Zipf(1.2)-skewed router, four shared experts as one FFN of width
+    5632): one 8192-token batch per step is routed, permuted, run through the
+    32 resident experts (the batch's 32 most routed: the expert cache with a
+    perfect predictor; slot weights set up once, before the timed region),
+    gathered for the shared experts, run through them, and combined. The
+    routed experts' row counts fall off along the Zipf tail, so below about
+    315 rows an expert is bound by reading its weights: the FFN is also timed
+    with only those experts, and with only the others. One JSON line."""
+    import torch
+    from paper_2410_17954_amd import ops, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.workload("qwen15_moe_layer")
+    T, H, E, F, k, S, n_s = (cfg[n] for n in ("T", "H", "E", "F", "k", "S", "n_shared"))
+    inp = synth.layer_inputs(cfg, cfg["seed"], T=T)
+
+    def up(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    x, wr, bias_d = up(inp["x"]), up(inp["w_router"]), up(inp["bias"])
+    W = {n: up(inp[n]) for n in ("w_gate", "w_up", "w_down")}
+    shared = tuple(up(inp[n])[None] for n in ("shared_gate", "shared_up", "shared_down"))
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    gw = torch.empty((T, k), dtype=torch.float32, device=dev)
+    ops.route(x, wr, k, bias=bias_d, topk_idx=idx, topk_w=gw)
+    routed = np.bincount(idx.cpu().numpy().ravel(), minlength=E)
+    slot = ops.plan_slots(routed, S)
+    res = torch.tensor([e for e in range(E) if slot[e] >= 0], dtype=torch.long, device=dev)
+    slot_w = tuple(W[n].index_select(0, res).contiguous() for n in ("w_gate", "w_up", "w_down"))
+    del W
+    slot_d = torch.from_numpy(slot).to(dev)
+    R = T * k
+    off = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    rop = torch.empty(R, dtype=torch.int32, device=dev)
+    por = torch.empty(R, dtype=torch.int32, device=dev)
+    xp = torch.empty((R, H), dtype=torch.bfloat16, device=dev)
+    yp = torch.empty((R, H), dtype=torch.bfloat16, device=dev)
+    off1 = torch.empty(2, dtype=torch.int32, device=dev)
+    rop1 = torch.empty(T, dtype=torch.int32, device=dev)
+    por1 = torch.empty(T, dtype=torch.int32, device=dev)
+    ys = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+    inc = torch.empty(T, dtype=torch.int32, device=dev)
+    y = torch.zeros((T, H), dtype=torch.bfloat16, device=dev)
+    ws_p = ops.workspace_tensor(ops.permute_workspace(T, k, E), dev)
+    ws_f = ops.workspace_tensor(ops.expert_ffn_workspace(R, H, F, E), dev)
+    ws_f1 = ops.workspace_tensor(ops.expert_ffn_workspace(T, H, n_s * F, 1), dev)
+    names = ["route", "permute", "expert_ffn", "shared_ffn", "combine"]
+
+    def step(ev=None):
+        marks = []
+
+        def mark():
+            if ev is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                marks.append(e)
+        mark()
+        ops.route(x, wr, k, bias=bias_d, topk_idx=idx, topk_w=gw)
+        mark()
+        ops.permute(x, idx, E, expert_offsets=off, row_of_pair=rop, pair_of_row=por, x_perm=xp,
+                    workspace=ws_p)
+        mark()
+        ops.expert_ffn(xp, off, *slot_w, slot_of_expert=slot_d, y_perm=yp, workspace=ws_f)
+        mark()
+        # the shared experts see the batch in token order: x itself, no gather
+        ops.expert_ffn(x, off1, *shared, y_perm=ys, workspace=ws_f1)
+        mark()
+        ops.combine(yp, idx, gw, rop, slot_of_expert=slot_d, y_shared=ys, y=y, incomplete=inc)
+        mark()
+        return marks
+
+    off1.copy_(torch.tensor([0, T], dtype=torch.int32))
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    K = args.steps
+    all_marks = []
+    t0 = time.perf_counter()
+    for _ in range(K):
+        all_marks.append(step(True))
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / K
+    st = {n: sum(m[j].elapsed_time(m[j + 1]) for m in all_marks) / K
+          for j, n in enumerate(names)}
+    counts = np.diff(off.cpu().numpy().astype(np.int64))
+    assert np.array_equal(counts, routed)
+    resident_pairs = int(counts[slot >= 0].sum())
+    incomplete = int((slot[idx.cpu().numpy()] < 0).any(axis=1).sum())
+    assert int(inc.sum()) == incomplete and torch.isfinite(y.float()).all().item()
+    bytes_route = T * H * 2 + E * H * 2 + T * E * 4 + T * k * 8 + E * 4
+    bytes_perm = T * H * 2 + R * H * 2 + T * k * 12
+    bytes_comb = R * H * 2 + 2 * T * H * 2 + T * k * 12
+    split = _weight_bound_split(torch, ops, xp, off, counts, slot, slot_w, ws_f, yp, H, F, E,
+                                dev)
+    rec = {
+        "metric": "Qwen1.5-MoE-shaped MoE layer: tokens/s and per-stage rates",
+        "value": T / (ms_step * 1e-3), "unit": "tokens/s", "ms_per_step": ms_step, "steps": K,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"Qwen1.5-MoE-shaped MoE layer: one batch of {T} tokens, H={H}, "
+                               f"E={E}, F={F}, top-{k}, router skewed by a Zipf({cfg['zipf_bias']})"
+                               f"-ranked bias, {S} of {E} experts resident (the batch's most "
+                               f"routed), {n_s} shared experts (one FFN of width {n_s * F})"},
+        "stages": {
+            "route": _rate(bytes_route, st["route"]),
+            "permute": _rate(bytes_perm, st["permute"]),
+            "expert_ffn": _mfma(6.0 * H * F * resident_pairs, st["expert_ffn"]),
+            "shared_ffn": _mfma(6.0 * H * (n_s * F) * T, st["shared_ffn"]),
+            "combine": _rate(bytes_comb, st["combine"]),
+        },
+        "ffn_by_ridge": split,
+        "rows_per_resident_expert": sorted((int(c) for c in counts[slot >= 0]), reverse=True),
+        "resident_pair_share": round(resident_pairs / R, 4),
         "incomplete_tokens": incomplete,
     }
     print(json.dumps(rec))
@@ -650,23 +853,35 @@ def stack_report(args):
     layers = [(rnd((E, H), 0.02), rnd((E, F, H), 0.02), rnd((E, F, H), 0.02),
                rnd((E, H, F), 0.02)) for _ in range(L)]
     n_units = 1 + args.stack_units
+    predictor = None
+    if args.stack_predictor:
+        dims = dict(vocab=32000, d_model=32, n_heads=4, d_ff=2048, n_enc=3, n_dec=3, L=L, E=E,
+                    num_buckets=32, max_distance=128, eps=1e-6)
+        pw = torch.randn(ops.rpp_weights_count(dims), generator=g, device=dev) * 0.1
+        predictor = dict(weights=pw, dims=dims)
 
     def make_units(seed0):
         us = []
         for u in range(n_units):
+            kv = [torch.randint(0, 256, (L, N // 2, kv_row), dtype=torch.uint8, device=dev,
+                                generator=g) for _ in range(2)]
+            if predictor is not None:
+                ids = torch.randint(0, 32000, (16, N // 16), dtype=torch.int32, device=dev,
+                                    generator=g)
+                us.append(pipeline.Unit(h=rnd((N, H), 1.0), kv=kv, ids=ids))
+                continue
             routes = synth.predicted_routes(N, L, E, k, cfg["keep"], cfg["zipf"], seed0 + u)
             us.append(pipeline.Unit(
                 h=rnd((N, H), 1.0),
                 routes=torch.from_numpy(np.ascontiguousarray(routes, dtype=np.uint8)).to(dev),
-                kv=[torch.randint(0, 256, (L, N // 2, kv_row), dtype=torch.uint8, device=dev,
-                                  generator=g) for _ in range(2)]))
+                kv=kv))
         return us
 
     out = {}
     state = {}
     for overlap in (True, False):
         units = make_units(args.seed * 1000)
-        pl = pipeline.DualBatchPipeline(layers, k, E, N, overlap=overlap)
+        pl = pipeline.DualBatchPipeline(layers, k, E, N, overlap=overlap, predictor=predictor)
         pl.run(units[:1])                          # warm-up unit
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -678,7 +893,7 @@ def stack_report(args):
         del units, pl
     # the scheduling work of one unit alone (token scheduler + KV merge/reindex)
     units = make_units(args.seed * 1000 + 7)
-    pl = pipeline.DualBatchPipeline(layers, k, E, N, overlap=False)
+    pl = pipeline.DualBatchPipeline(layers, k, E, N, overlap=False, predictor=predictor)
     pl._plan(units[0])
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -698,7 +913,10 @@ def stack_report(args):
            "tokens_per_s_in_order": round(toks / out[False], 1),
            "ms_per_unit_overlapped": round(out[True] / args.stack_units * 1e3, 3),
            "ms_per_unit_in_order": round(out[False] / args.stack_units * 1e3, 3),
-           "schedule_and_kv_ms_per_unit": round(plan_ms, 3),
+           "plan_ms_per_unit": round(plan_ms, 3),
+           "plan": ("routing path predictor (16 x 512 tokens, hidden 32, FFN 2048) + top-2 per "
+                    "layer + token scheduler + KV merge/reindex" if predictor is not None else
+                    "token scheduler + KV merge/reindex (routes given)"),
            "kv_bytes_moved_per_unit": 2 * L * N * kv_row,
            "final_state_finite": state[True][0],
            "final_state_abs_mean": round(state[True][1], 3),
@@ -790,7 +1008,13 @@ def main():
         sched_sweep_report(args)
         return
     if args.deepseek:
-        deepseek_report(args)
+        scheduled_layer_report(args, "deepseek_v2_lite_layer")
+        return
+    if args.route_grouped:
+        scheduled_layer_report(args, "mixtral8x7b_route_grouped")
+        return
+    if args.qwen:
+        qwen_report(args)
         return
     if args.rpp:
         rpp_report(args)

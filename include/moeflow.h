@@ -4,6 +4,7 @@
  * token batches:
  *
  *   moe_route       softmax top-k gating                        (Sec. 2.1)
+ *   moe_route_binarize  routing paths from predictor scores     (Sec. 3.2)
  *   moe_schedule    balanced rebatching of two adjacent batches
  *                   by predicted routing path                   (Sec. 3.3, Eq. 2)
  *   moe_schedule_multi  the same into B batches by recursive bisection
@@ -94,6 +95,26 @@ int moe_route(const void* x, const void* w_gate, int32_t dtype,
               int64_t T, int64_t H, int32_t E, int32_t k,
               const float* bias, int32_t bias_mode, int32_t renormalize,
               float* logits, int32_t* topk_idx, float* topk_w, void* stream);
+
+/* ------------------------------------------------------------------------
+ * moe_route_binarize -- a token's routing path from the predictor's output
+ * (Sec. 3.2: the predictor scores every expert of every layer for each token;
+ * the route r_i keeps, per layer, the experts predicted to be selected -- here
+ * the k with the highest scores, the gate's own rule). Sigmoid is monotone,
+ * so ranking logits ranks probabilities.
+ *
+ *   routes[r, j] = the expert with the j-th largest logits[r, :], descending;
+ *                  equal logits go to the lower expert index; -0.0 == +0.0
+ *
+ * logits [rows, E] float32 DEVICE: one row per (token, layer), e.g. the
+ *        [B, S, L, E] output of moe_rpp_forward viewed as [B*S*L, E]
+ * routes [rows, k] uint8 DEVICE output: laid out [N, L, k] for moe_schedule
+ *        when rows = N*L
+ * Limits: rows >= 1, 1 <= k <= E <= 256. NaN logits: unspecified ids.
+ * Errors: MOE_ERR_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_HIP.
+ * ---------------------------------------------------------------------- */
+int moe_route_binarize(const float* logits, int64_t rows, int32_t E, int32_t k,
+                       uint8_t* routes, void* stream);
 
 /* ------------------------------------------------------------------------
  * moe_schedule -- the Token Scheduler (Sec. 3.3): split N tokens (two adjacent

@@ -744,8 +744,46 @@ route_logits_kernel(const float* __restrict__ logits, int64_t T, int E, int k, i
   gate_weights(logits + t * E, E, k, renorm, topk_idx + t * k, topk_w + t * k);
 }
 
+// Routing paths from predictor logits: row r (a token at one layer) gets the
+// k experts with the largest logits, descending, equal logits lower id first.
+// One thread per row; the row is scanned k times (E <= 256, k small).
+__global__ void binarize_kernel(const float* __restrict__ logits, int64_t rows, int E, int k,
+                                uint8_t* __restrict__ routes) {
+  const int64_t r = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (r >= rows) return;
+  const float* z = logits + r * E;
+  float prev_v = INFINITY;
+  int prev_e = -1;
+  for (int j = 0; j < k; ++j) {
+    float bv = -INFINITY;
+    int be = -1;
+    for (int e = 0; e < E; ++e) {
+      const float v = z[e];
+      const bool after_prev = (v < prev_v) || (v == prev_v && e > prev_e);
+      if (after_prev && (be < 0 || v > bv)) {
+        bv = v;
+        be = e;
+      }
+    }
+    routes[r * k + j] = (uint8_t)(be < 0 ? 0 : be);
+    prev_v = bv;
+    prev_e = be;
+  }
+}
+
 }  // namespace
 }  // namespace moe
+
+extern "C" int moe_route_binarize(const float* logits, int64_t rows, int32_t E, int32_t k,
+                                  uint8_t* routes, void* stream) {
+  using namespace moe;
+  MOE_CHECK_ARG(logits && routes && rows >= 1 && E >= 1 && E <= 256 && k >= 1 && k <= E);
+  if (ceil_div(rows, 256) > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
+  binarize_kernel<<<dim3((unsigned)ceil_div(rows, 256)), dim3(256), 0, as_stream(stream)>>>(
+      logits, rows, E, k, routes);
+  MOE_CHECK_LAUNCH();
+  return MOE_OK;
+}
 
 extern "C" int moe_route(const void* x, const void* w_gate, int32_t dtype, int64_t T,
                          int64_t H, int32_t E, int32_t k, const float* bias,

@@ -45,6 +45,7 @@ def load_library(path=None):
         "moe_abi_version": (I32, []),
         "moe_status_str": (ctypes.c_char_p, [ctypes.c_int]),
         "moe_route": (I32, [P, P, I32, I64, I64, I32, I32, P, I32, I32, P, P, P, P]),
+        "moe_route_binarize": (I32, [P, I64, I32, I32, P, P]),
         "moe_schedule_workspace": (SZ, [I64, I32, I32, I32]),
         "moe_schedule": (I32, [P, I64, I32, I32, I32, I64, I32, I32, P, P, P, P, P, SZ, P]),
         "moe_kv_gather": (I32, [P, P, I32, I64, I64, P, I64, P, P, P]),
@@ -82,7 +83,8 @@ def load_library(path=None):
 
 
 def exported_symbols():
-    return ["moe_abi_version", "moe_status_str", "moe_route", "moe_schedule_workspace",
+    return ["moe_abi_version", "moe_status_str", "moe_route", "moe_route_binarize",
+            "moe_schedule_workspace",
             "moe_schedule", "moe_schedule_multi_workspace", "moe_schedule_multi",
             "moe_permute_workspace", "moe_permute", "moe_permute_noalloc",
             "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_kv_gather",
@@ -192,6 +194,26 @@ def route(x=None, w_gate=None, k=1, bias=None, renormalize=True, logits=None,
 
 
 # -------------------------------------------------------------------- schedule
+def route_binarize(logits, k, routes=None, stream=None):
+    """moe_route_binarize over logits float32 [..., E] (rows = the leading
+    dimensions). Returns uint8 routes [..., k]."""
+    torch = _torch()
+    lib = load_library()
+    _dev(logits, routes)
+    if logits.dtype != torch.float32 or logits.dim() < 2:
+        raise TypeError("logits must be float32 [..., E]")
+    E = logits.shape[-1]
+    rows = logits.numel() // E
+    shape = tuple(logits.shape[:-1]) + (k,)
+    if routes is None:
+        routes = torch.empty(shape, dtype=torch.uint8, device=logits.device)
+    elif routes.dtype != torch.uint8 or tuple(routes.shape) != shape:
+        raise ValueError("routes must be uint8 of shape logits.shape[:-1] + (k,)")
+    _check("moe_route_binarize", lib.moe_route_binarize(_ptr(logits), rows, E, k, _ptr(routes),
+                                                        _stream(stream)))
+    return routes
+
+
 def schedule_workspace(N, L, E, k):
     return load_library().moe_schedule_workspace(N, L, E, k)
 

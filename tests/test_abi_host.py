@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 27, names
+    assert len(names) == 28, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
@@ -210,3 +210,12 @@ def test_permute_noalloc_rejects_on_the_host(lib):
     assert lib.moe_permute_noalloc(S, 0, 0, 10, S, 10, FAKE, 9, 8, FAKE, FAKE, FAKE, S, S) == ops.MOE_ERR_ARG
     assert lib.moe_permute_noalloc(FAKE, 1, 64, 10, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, S, S) == ops.MOE_ERR_ARG
     assert lib.moe_permute_noalloc(FAKE, 1, 60, 10, S, 10, FAKE, 2, 8, FAKE, FAKE, FAKE, FAKE, S) == ops.MOE_ERR_UNSUPPORTED
+
+
+def test_route_binarize_rejects_on_the_host(lib):
+    S = None
+    assert lib.moe_route_binarize(S, 10, 8, 2, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route_binarize(FAKE, 10, 8, 2, S, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route_binarize(FAKE, 0, 8, 2, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route_binarize(FAKE, 10, 8, 9, FAKE, S) == ops.MOE_ERR_ARG
+    assert lib.moe_route_binarize(FAKE, 10, 257, 2, FAKE, S) == ops.MOE_ERR_ARG

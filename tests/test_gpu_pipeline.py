@@ -108,3 +108,42 @@ def test_inputs_produced_on_the_main_stream_are_waited_for():
         assert np.array_equal(to_host(p.kv_new), to_host(rp.kv_new))
         assert np.array_equal(to_host(u.h), to_host(r.h))
         assert to_host(p.err)[0] == 0
+
+
+def test_predictor_in_the_plan_overlapped_equals_in_order():
+    # Units carry token ids; each plan runs the routing path predictor, the
+    # per-layer top-k of its logits, the scheduler and the KV work on the side
+    # stream. Overlapped and in-order runs agree bit for bit, the routes are
+    # the top-k of the predictor's logits (moe_route_binarize, checked against
+    # the oracle on the same logits), and the split is the scheduler's on
+    # those routes.
+    layers, units, (N, E, k) = _setup(n_units=3, seed=11)
+    L = 2
+    dims = dict(vocab=1000, d_model=32, n_heads=4, d_ff=256, n_enc=1, n_dec=1, L=L, E=E,
+                num_buckets=32, max_distance=128, eps=1e-6)
+    g = np.random.default_rng(12)
+    w = to_dev((g.standard_normal(ops.rpp_weights_count(dims)) * 0.3).astype(np.float32))
+    ids = [g.integers(0, 1000, size=(4, N // 4)).astype(np.int32) for _ in units]
+    pred = dict(weights=w, dims=dims)
+    res = {}
+    for overlap in (True, False):
+        us = [pipeline.Unit(h=to_dev(h), kv=[to_dev(c) for c in kv], ids=to_dev(i))
+              for (h, _, kv), i in zip(units, ids)]
+        plans = pipeline.DualBatchPipeline(layers, k, E, N, overlap=overlap,
+                                           predictor=pred).run(us)
+        torch.cuda.synchronize()
+        res[overlap] = ([to_host(u.h) for u in us], plans)
+    for a, b in zip(res[True][0], res[False][0]):
+        assert np.array_equal(a, b)
+    for i, pa, pb in zip(ids, res[True][1], res[False][1]):
+        for name in ("routes", "perm", "kv_new", "demand"):
+            assert np.array_equal(to_host(getattr(pa, name)), to_host(getattr(pb, name)))
+        assert to_host(pa.err)[0] == 0
+        _, logits, err = ops.rpp_forward(to_dev(i), w, dims, want_logits=True)
+        torch.cuda.synchronize()
+        z = to_host(logits).astype(np.float64).reshape(-1, E)
+        routes = to_host(pa.routes)
+        assert np.array_equal(routes.reshape(-1, k).astype(np.int64), oracle.topk_select(z, k))
+        rp, rd, _ = oracle.schedule(routes, E, N // 2)
+        assert np.array_equal(to_host(pa.perm), rp)
+        assert np.array_equal(to_host(pa.demand), rd)

@@ -6,6 +6,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from oracle import rpp as orpp
 from paper_2410_17954_amd import ops
 from gpu_helpers import to_dev, to_host
@@ -47,6 +48,7 @@ def _check(dims, B, S, seed, sample=None):
     gl = to_host(logits).astype(np.float64)[rows]
     assert np.abs(gl - rl).max() <= 1e-4 * np.abs(rl).max() + 1e-5
     assert np.abs(to_host(probs).astype(np.float64)[rows] - rp).max() <= 1e-5
+    return logits, rl, 1e-4 * np.abs(rl).max() + 1e-5
 
 
 def test_small_dims_ragged_sequences():
@@ -65,10 +67,51 @@ def test_wider_attention_heads(h):
     _check(dict(PAPER, vocab=500, n_heads=h, n_enc=1, n_dec=1, L=4, E=6), 2, 70, seed=3 + h)
 
 
-def test_scheduling_unit_of_8192_tokens():
-    # the bench's batch: 16 sequences of 512 tokens, Mixtral's 32 layers x 8 experts;
-    # the oracle checks the first and the last sequence
-    _check(PAPER, 16, 512, seed=5, sample=[0, 15])
+def _check_routes(logits, ref_logits, tol, k):
+    """Routing paths from the predictor's logits (moe_route_binarize): equal,
+    on every (token, layer) row, to the oracle's top-k of the same float32
+    logits; and equal to the oracle's top-k of its own float64 logits on every
+    row whose k-th and (k+1)-th logits are more than twice the logit
+    tolerance apart (the other rows are near ties the float32 forward may
+    decide either way; they are counted)."""
+    E = logits.shape[-1]
+    routes = ops.route_binarize(logits, k)
+    torch.cuda.synchronize()
+    got = to_host(routes).reshape(-1, k).astype(np.int64)
+    z32 = to_host(logits).astype(np.float64).reshape(-1, E)
+    assert np.array_equal(got, oracle.topk_select(z32, k))
+    z = ref_logits.reshape(-1, E)
+    zs = -np.sort(-z, axis=1)
+    sure = (zs[:, k - 1] - zs[:, k] > 2 * tol) if k < E else np.ones(len(z), bool)
+    assert np.array_equal(got[sure], oracle.topk_select(z, k)[sure])
+    return int((~sure).sum())
+
+
+def test_scheduling_unit_of_8192_tokens_and_its_routes():
+    # the bench's unit: 16 sequences of 512 tokens, Mixtral's 32 layers x 8
+    # experts; every sequence is compared, then the routes binarised from the
+    # logits (top-2 of each layer)
+    logits, rl, tol = _check(PAPER, 16, 512, seed=5)
+    near = _check_routes(logits, rl, tol, 2)
+    assert near < rl.size // 8 // 100                 # near ties are rare
+
+
+@pytest.mark.parametrize("E,k", [(60, 4), (64, 6), (5, 5), (1, 1)])
+def test_routes_of_other_shapes(E, k):
+    dims = dict(PAPER, vocab=400, n_enc=1, n_dec=1, L=5, E=E)
+    logits, rl, tol = _check(dims, 2, 33, seed=40 + E)
+    _check_routes(logits, rl, tol, k)
+
+
+def test_route_binarize_ties_and_signed_zeros():
+    # exact ties go to the lower expert id; -0.0 equals +0.0
+    z = np.array([[1.0, 3.0, 3.0, 2.0],
+                  [0.0, -0.0, 0.0, -1.0],
+                  [-np.inf, -np.inf, 5.0, -np.inf],
+                  [2.0, 2.0, 2.0, 2.0]], dtype=np.float32)
+    got = to_host(ops.route_binarize(to_dev(z), 3)).astype(np.int64)
+    assert got.tolist() == [[1, 2, 3], [0, 1, 2], [2, 0, 1], [0, 1, 2]]
+    assert np.array_equal(got, oracle.topk_select(z.astype(np.float64), 3))
 
 
 def test_out_of_range_ids_are_flagged():
