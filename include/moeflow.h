@@ -464,6 +464,27 @@ int moe_combine(const void* y_perm, int32_t dtype, int64_t H, int64_t rows,
  *   (may be NULL with n_prefetch) = the items loaded before the first layer;
  *   hits, needed [L] int64 outputs; loads = every expert load of the batch.
  *
+ * moe_plec_begin / moe_plec_layer / moe_plec_advance -- the same policy as
+ *   moe_plec_run, step by step, with cache slots assigned, so that a run on
+ *   the device can execute it: the caller copies each listed load (layer,
+ *   expert, slot) into the cache and runs each layer with the slot table it
+ *   gets. state: HOST memory of moe_plec_state_bytes(L, E, budget) bytes,
+ *   owned by the caller, written by begin and updated by the other calls.
+ *   Free slots are taken lowest index first.
+ *   begin: the load order from pred_demand [L,E] (HOST int32) and the
+ *     prefetch; loads [budget][3] int32 HOST output, n_loads their number.
+ *   layer(l): layers in order, each once, after its actual demand [E] (HOST
+ *     int32: rows routed to each expert) is known: hits and needed (HOST
+ *     int64 outputs), the correction loads ([E][3], slot -1 = served without
+ *     caching: no slot could be taken; never when budget >= E), and
+ *     slot_of_expert [E] (HOST int32 output, may be NULL): the slot of every
+ *     resident expert of layer l once the corrections are in, -1 otherwise.
+ *   advance(l): layer l has run: its slots are freed and refilled with the
+ *     next items of later layers; loads [budget][3] as for begin. The slots
+ *     freed were read by layer l's experts: those loads must wait for them.
+ *   Errors: MOE_ERR_ARG (NULL pointers, sizes, a too small state, layers out
+ *   of order).
+ *
  * moe_lru_run -- the baseline: a fixed cache of `capacity` experts per layer
  *   with least-recently-used replacement, kept across B batches; a layer's
  *   used experts are looked up in ascending id. actual_demand [B,L,E] int32
@@ -487,6 +508,13 @@ int moe_plec_order(const int32_t* demand, int32_t L, int32_t E, int32_t* items,
 int moe_plec_run(const int32_t* pred_demand, const int32_t* actual_demand, int32_t L,
                  int32_t E, int32_t budget, int32_t* prefetch, int32_t* n_prefetch,
                  int64_t* hits, int64_t* needed, int64_t* loads);
+size_t moe_plec_state_bytes(int32_t L, int32_t E, int32_t budget);
+int moe_plec_begin(const int32_t* pred_demand, int32_t L, int32_t E, int32_t budget,
+                   void* state, size_t state_bytes, int32_t* loads, int32_t* n_loads);
+int moe_plec_layer(void* state, int32_t l, const int32_t* actual_demand,
+                   int32_t* slot_of_expert, int32_t* loads, int32_t* n_loads, int64_t* hits,
+                   int64_t* needed);
+int moe_plec_advance(void* state, int32_t l, int32_t* loads, int32_t* n_loads);
 int moe_lru_run(const int32_t* actual_demand, int32_t B, int32_t L, int32_t E,
                 int32_t capacity, int64_t* hits, int64_t* needed);
 int moe_load_experts(const void* w_gate_src, const void* w_up_src, const void* w_down_src,

@@ -72,6 +72,10 @@ def load_library(path=None):
         "moe_plec_order": (I32, [P, I32, I32, P, P]),
         "moe_plec_run": (I32, [P, P, I32, I32, I32, P, P, P, P, P]),
         "moe_lru_run": (I32, [P, I32, I32, I32, I32, P, P]),
+        "moe_plec_state_bytes": (SZ, [I32, I32, I32]),
+        "moe_plec_begin": (I32, [P, I32, I32, I32, P, SZ, P, P]),
+        "moe_plec_layer": (I32, [P, I32, P, P, P, P, P, P]),
+        "moe_plec_advance": (I32, [P, I32, P, P]),
         "moe_load_experts": (I32, [P, P, P, I32, P, P, P, I32, I64, I64, I32, P, P, I32, P]),
     }
     for name, (res, args) in sig.items():
@@ -91,7 +95,8 @@ def exported_symbols():
             "moe_kv_reindex", "moe_stack_workspace", "moe_stack_forward",
             "moe_rpp_weights_count", "moe_rpp_workspace", "moe_rpp_forward",
             "moe_probe_mfma_bf16", "moe_probe_read", "moe_plan_slots", "moe_plec_order",
-            "moe_plec_run", "moe_lru_run", "moe_load_experts"]
+            "moe_plec_run", "moe_lru_run", "moe_load_experts", "moe_plec_state_bytes",
+            "moe_plec_begin", "moe_plec_layer", "moe_plec_advance"]
 
 
 def _check(name, status):
@@ -608,6 +613,46 @@ def plec_run(pred_demand, actual_demand, budget):
                           needed.ctypes.data_as(ctypes.c_void_p), ctypes.byref(loads))
     _check("moe_plec_run", st)
     return {"prefetch": pre[:npre.value], "hits": hits, "needed": needed, "loads": loads.value}
+
+
+class PlecPlanner:
+    """moe_plec_begin / moe_plec_layer / moe_plec_advance over host state:
+    the PLEC policy step by step with cache slots assigned. Loads come back as
+    int32 [n, 3] rows (layer, expert, slot)."""
+
+    def __init__(self, pred_demand, budget):
+        self.lib = load_library()
+        d, dp = _host_i32(pred_demand)
+        self.L, self.E = d.shape
+        self.budget = int(budget)
+        n = self.lib.moe_plec_state_bytes(self.L, self.E, self.budget)
+        self.state = ctypes.create_string_buffer(n)
+        self._buf = np.empty((max(self.budget, self.E, 1), 3), dtype=np.int32)
+        cnt = ctypes.c_int32(0)
+        _check("moe_plec_begin", self.lib.moe_plec_begin(
+            dp, self.L, self.E, self.budget, self.state, n,
+            self._buf.ctypes.data_as(ctypes.c_void_p), ctypes.byref(cnt)))
+        self.prefetch = self._buf[:cnt.value].copy()
+
+    def layer(self, l, actual_demand):
+        """Returns (slot_of_expert int32 [E], correction loads [n, 3], hits,
+        needed)."""
+        a, ap = _host_i32(actual_demand)
+        slot = np.empty(self.E, dtype=np.int32)
+        cnt = ctypes.c_int32(0)
+        hits, needed = ctypes.c_int64(0), ctypes.c_int64(0)
+        _check("moe_plec_layer", self.lib.moe_plec_layer(
+            self.state, int(l), ap, slot.ctypes.data_as(ctypes.c_void_p),
+            self._buf.ctypes.data_as(ctypes.c_void_p), ctypes.byref(cnt), ctypes.byref(hits),
+            ctypes.byref(needed)))
+        return slot, self._buf[:cnt.value].copy(), hits.value, needed.value
+
+    def advance(self, l):
+        """Layer l has run: returns the refill loads [n, 3]."""
+        cnt = ctypes.c_int32(0)
+        _check("moe_plec_advance", self.lib.moe_plec_advance(
+            self.state, int(l), self._buf.ctypes.data_as(ctypes.c_void_p), ctypes.byref(cnt)))
+        return self._buf[:cnt.value].copy()
 
 
 def lru_run(actual_demands, capacity):

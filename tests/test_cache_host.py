@@ -92,3 +92,86 @@ def test_hit_ratio_on_predicted_routes():
     assert (lh, ln) == oracle.lru_run(np.stack(acts).tolist(), CS)
     assert ln == pn
     assert ph / pn > lh / ln
+
+
+def _execute_plan(pred, act, budget):
+    """Runs the step-by-step planner against a model of the cache's slots
+    (slot -> (layer, expert) held), applying every listed load, and checks
+    that each layer finds every expert it uses in the slot its table names.
+    Returns the planner's per-layer hits, needed, the start sets and the
+    number of loads."""
+    L, E = pred.shape
+    pl = ops.PlecPlanner(pred, budget)
+    held = [None] * budget
+    loads = 0
+
+    def apply(rows, allowed=None):
+        nonlocal loads
+        seen = set()
+        for l, e, q in rows.tolist():
+            loads += 1
+            if q < 0:                      # served without caching
+                continue
+            assert 0 <= q < budget and q not in seen
+            if allowed is not None:
+                assert q in allowed, (l, e, q)
+            seen.add(q)
+            held[q] = (l, e)
+
+    apply(pl.prefetch, allowed=set(range(budget)))
+    assert len(pl.prefetch) <= budget
+    hits, needed, starts = [], [], []
+    for l in range(L):
+        starts.append(sorted(e for (ll, e) in (h for h in held if h) if ll == l))
+        before = list(held)
+        slot, corr, h, n = pl.layer(l, act[l])
+        # a correction goes into a free slot, or over an expert of this layer
+        # that the batch does not use, or over an item of a later layer
+        ok = {q for q in range(budget)
+              if before[q] is None or (before[q][0] == l and act[l][before[q][1]] <= 0)
+              or before[q][0] > l}
+        apply(corr, allowed=ok)
+        for e in range(E):
+            if slot[e] >= 0:
+                assert held[slot[e]] == (l, e)
+            elif act[l][e] > 0:
+                assert budget < E, "an expert without a slot needs budget < E"
+        hits.append(h)
+        needed.append(n)
+        freed = {q for q in range(budget) if held[q] is not None and held[q][0] == l}
+        for q in freed:
+            held[q] = None
+        free = {q for q in range(budget) if held[q] is None}
+        apply(pl.advance(l), allowed=free)
+        assert all(h is None or h[0] > l for h in held)
+    return hits, needed, starts, loads
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_step_planner_executes_the_oracle_policy(seed):
+    g = np.random.default_rng(100 + seed)
+    for _ in range(40):
+        L, E = int(g.integers(1, 7)), int(g.integers(1, 20))
+        pred = (g.random((L, E)) < 0.4) * g.integers(1, 6, size=(L, E))
+        act = np.where(g.random((L, E)) < 0.8, pred, (g.random((L, E)) < 0.3) * 2)
+        budget = int(g.integers(0, L * E + 2))
+        ref = oracle.plec_run(pred.tolist(), act.tolist(), budget)
+        hits, needed, starts, loads = _execute_plan(pred, act, budget)
+        assert hits == ref["hits"] and needed == ref["needed"]
+        assert starts == ref["start_sets"]
+        assert loads == ref["loads"]
+
+
+def test_step_planner_worked_example():
+    # Sec. 3.4.1: e12, e13, e14 and e22 prefetched into the 4 slots; when the
+    # first layer has run, e23 is loaded into a slot it freed
+    g = json.load(open(os.path.join(GOLDEN, "plec_worked_example.json")))
+    pred = np.array(g["pred_demand"])
+    pl = ops.PlecPlanner(pred, g["budget"])
+    assert [tuple(r[:2]) for r in pl.prefetch.tolist()] == [tuple(x) for x in g["prefetch"]]
+    slot, corr, h, n = pl.layer(0, pred[0])
+    assert len(corr) == 0 and h == n == 3
+    refill = pl.advance(0)
+    freed = {int(slot[e]) for e in range(pred.shape[1]) if slot[e] >= 0}
+    assert [tuple(r[:2]) for r in refill.tolist()] == [(1, 2)]
+    assert int(refill[0, 2]) in freed
