@@ -4,9 +4,9 @@
 // bf16 inputs: the projection z = x . W_g^T runs on MFMA (v_mfma_f32_16x16x32_bf16),
 // in float32 chains of 8 K-steps that are added into float64 accumulators.
 // Up to 32 and above 64 experts: 16 tokens per block, the K dimension split
-// into contiguous ranges over the waves. 33-64 experts: 64 tokens per block,
-// one wave per 16-token tile, the router matrix staged through LDS chunk by
-// chunk. The same block then selects the top-k of each token exactly (see
+// into contiguous ranges over the waves. 33-64 experts: 16 to 64 tokens per
+// block in tiles of 16, the waves of a tile splitting the experts, the router
+// matrix staged through LDS chunk by chunk. The same block then selects the top-k of each token exactly (see
 // route_decide) and computes its gates.
 // float32 inputs (small, correctness-oriented): one block per token, one
 // thread per expert, float64 logits.
@@ -583,14 +583,24 @@ route_ksplit_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__
 // chunk and the next x fragments are loaded while the current ones are used.
 constexpr int kWChunk = 256;                      // K-columns per staged chunk
 constexpr int kWPitch = kWChunk + 8;              // padded row (bank spread)
-constexpr int kTileTok = 64;
+// 33-64 experts: blocks per compute unit wanted before a larger token tile is
+// used (measured at 8192 Qwen-shaped tokens: 64-token tiles, 128 blocks, 59 us;
+// 32, 256 blocks, 46 us; 16, 512 blocks, 41 us)
+constexpr int kRouteTileBlocks = 2;
 
+// TB tokens per block (64, 32 or 16): TB / 16 tiles of 16 tokens, the waves
+// of a tile splitting the 64 expert columns between them.
+template <int TB>
 __global__ void __launch_bounds__(256, 2)
 route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ wg, int64_t T,
                    int64_t H, int E, int k, const float* __restrict__ bias, int bias_mode,
                    int renorm, float* __restrict__ logits, int32_t* __restrict__ topk_idx,
                    float* __restrict__ topk_w) {
-  constexpr int NEB = 4, EP = 64, TB = kTileTok, NW = 4;
+  constexpr int NEB = 4, EP = 64, NW = 4;
+  constexpr int TT = TB / 16;                     // 16-token tiles
+  constexpr int WPT = NW / TT;                    // waves per tile
+  constexpr int NEBW = NEB / WPT;                 // 16-expert blocks per wave
+  static_assert(TT * WPT == NW && NEBW * WPT == NEB, "tile split");
   constexpr int SS = kWChunk / 32;                // K-steps per chunk (= kChainSteps)
   static_assert(SS == kChainSteps, "one float32 chain per chunk");
   constexpr int WV = EP * kWChunk / 8 / (NW * kWave);   // 16-byte W pieces per thread
@@ -608,8 +618,9 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
   const int64_t tok0 = (int64_t)blockIdx.x * TB;
   const int row = lane & 15;
   const int kq = (lane >> 4) * 8;
-  const bool row_ok = tok0 + wave * 16 + row < T;
-  const uint16_t* xrow = x + (tok0 + wave * 16 + row) * H + kq;
+  const int tw = wave % TT, eg = wave / TT;       // token tile, expert group
+  const bool row_ok = tok0 + tw * 16 + row < T;
+  const uint16_t* xrow = x + (tok0 + tw * 16 + row) * H + kq;
   const int64_t nch = (H + kWChunk - 1) / kWChunk;
 
   auto load_x = [&](int64_t c, uint4 (&xa)[SS]) {
@@ -639,10 +650,10 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
     }
   };
 
-  f32x4_t acc[NEB], acs[NEB];
-  double a64[NEB][4];
+  f32x4_t acc[NEBW], acs[NEBW];
+  double a64[NEBW][4];
 #pragma unroll
-  for (int b = 0; b < NEB; ++b) {
+  for (int b = 0; b < NEBW; ++b) {
     acs[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 4; ++i) a64[b][i] = 0.0;
@@ -659,14 +670,15 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
       load_w(c + 1, wr);
     }
 #pragma unroll
-    for (int nb = 0; nb < NEB; ++nb) acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NEBW; ++nb) acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < SS; ++u) {
       const bf16x8_t av = __builtin_bit_cast(bf16x8_t, xc[u]);
       const bf16x8_t aa = __builtin_bit_cast(bf16x8_t, abs_bf16x8(xc[u]));
 #pragma unroll
-      for (int nb = 0; nb < NEB; ++nb) {
-        const uint4 bv = *reinterpret_cast<const uint4*>(&wsh[(nb * 16 + row) * kWPitch + u * 32 + kq]);
+      for (int nb = 0; nb < NEBW; ++nb) {
+        const int eb = eg * NEBW + nb;
+        const uint4 bv = *reinterpret_cast<const uint4*>(&wsh[(eb * 16 + row) * kWPitch + u * 32 + kq]);
         acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8_t, bv),
                                                           acc[nb], 0, 0, 0);
         acs[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
@@ -674,7 +686,7 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
       }
     }
 #pragma unroll
-    for (int nb = 0; nb < NEB; ++nb)
+    for (int nb = 0; nb < NEBW; ++nb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) a64[nb][i] += (double)acc[nb][i];
     __syncthreads();                              // every wave is done with this chunk
@@ -689,10 +701,10 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
   // C layout of the 16x16 MFMA: lane holds column (lane % 16), rows
   // 4 * (lane / 16) + i of this wave's tile.
 #pragma unroll
-  for (int nb = 0; nb < NEB; ++nb)
+  for (int nb = 0; nb < NEBW; ++nb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int t = wave * 16 + (lane >> 4) * 4 + i, e = nb * 16 + row;
+      const int t = tw * 16 + (lane >> 4) * 4 + i, e = (eg * NEBW + nb) * 16 + row;
       const int64_t tg = tok0 + t;
       double z = a64[nb][i];
       if (e < E && tg < T) z += (double)bias_of(bias, bias_mode, tg, E, e);
@@ -822,10 +834,21 @@ extern "C" int moe_route(const void* x, const void* w_gate, int32_t dtype, int64
   const auto* xb = static_cast<const uint16_t*>(x);
   const auto* wb = static_cast<const uint16_t*>(w_gate);
   if (neb == 3 || neb == 4) {
-    const int64_t tiles = ceil_div(T, kTileTok);
+    // the largest token tile that still gives every compute unit kRouteTileBlocks blocks
+    const int64_t cus = device_cu_count();
+    const int tb = ceil_div(T, 64) >= kRouteTileBlocks * cus ? 64
+                 : ceil_div(T, 32) >= kRouteTileBlocks * cus ? 32 : 16;
+    const int64_t tiles = ceil_div(T, tb);
     if (tiles > 0x7fffffff) return MOE_ERR_UNSUPPORTED;
-    route_tiles_kernel<<<dim3((unsigned)tiles), dim3(256), 0, st>>>(
-        xb, wb, T, H, E, k, bias, bias_mode, renormalize, logits, topk_idx, topk_w);
+    if (tb == 64)
+      route_tiles_kernel<64><<<dim3((unsigned)tiles), dim3(256), 0, st>>>(
+          xb, wb, T, H, E, k, bias, bias_mode, renormalize, logits, topk_idx, topk_w);
+    else if (tb == 32)
+      route_tiles_kernel<32><<<dim3((unsigned)tiles), dim3(256), 0, st>>>(
+          xb, wb, T, H, E, k, bias, bias_mode, renormalize, logits, topk_idx, topk_w);
+    else
+      route_tiles_kernel<16><<<dim3((unsigned)tiles), dim3(256), 0, st>>>(
+          xb, wb, T, H, E, k, bias, bias_mode, renormalize, logits, topk_idx, topk_w);
     MOE_CHECK_LAUNCH();
     return MOE_OK;
   }

@@ -82,10 +82,12 @@ def test_x_mode_deepseek_token_bias_no_renorm():
     _x_mode_case("deepseek_v2_lite_layer", 4096, 5, bias_kind="token", renorm=False)
 
 
-@pytest.mark.parametrize("T", [17, 8209])
-def test_x_mode_64_token_tiles_ragged(T):
-    # 33..64 experts run in 64-token tiles: one partial tile, and many tiles
-    # with a ragged last one
+@pytest.mark.parametrize("T", [17, 8209, 20001, 40003])
+def test_x_mode_token_tiles_ragged(T):
+    # 33..64 experts run in tiles of 16, 32 or 64 tokens (the largest that
+    # still gives two blocks per compute unit: 16 up to ~16K tokens, 32 up to
+    # ~32K, then 64 on 256 CUs): one partial tile, and many tiles with a
+    # ragged last one, for each tile size
     _x_mode_case("deepseek_v2_lite_layer", T, 11, bias_kind="expert")
 
 
