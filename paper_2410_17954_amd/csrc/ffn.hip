@@ -50,18 +50,23 @@ constexpr int kCounterWords = kClaimWords + 2 * kTailWords;
 // get no row tiles here: they are listed for the few-row kernels instead,
 // those with at most 16 rows in one list and those with 17 to 32 in another
 // (list[0] = the number of experts, list[1..] = their ids in ascending order).
+// With split_small an expert's last row tile, when it holds at most bm / 2
+// rows, is counted apart (prefix2: 0 or 1 per expert), so that the GEMMs can
+// run every expert's full-cost row tiles first and the small ones last.
 __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
                                  const int32_t* __restrict__ slot, int E, int S,
-                                 int64_t max_rows, int bm, int small_tiles,
+                                 int64_t max_rows, int bm, int small_tiles, int split_small,
                                  int32_t* __restrict__ prefix) {
   if (blockIdx.x != 0) return;
   for (int q = threadIdx.x; q < kCounterWords; q += blockDim.x) prefix[E + 1 + q] = 0;
   if (threadIdx.x != 0) return;
   int32_t* const list1 = prefix + E + 1 + kCounterWords;
   int32_t* const list2 = list1 + E + 1;
-  int32_t run = 0, n1 = 0, n2 = 0;
+  int32_t* const prefix2 = list2 + E + 1;
+  int32_t run = 0, run2 = 0, n1 = 0, n2 = 0;
   for (int e = 0; e < E; ++e) {
     prefix[e] = run;
+    prefix2[e] = run2;
     const int s = slot ? slot[e] : e;
     int64_t lo = offsets[e], hi = offsets[e + 1];
     lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
@@ -70,9 +75,18 @@ __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
     const int64_t m = hi - lo;
     if (m <= 16 * small_tiles && m <= 16) list1[1 + n1++] = e;
     else if (m <= 16 * small_tiles) list2[1 + n2++] = e;
-    else run += (int32_t)((m + bm - 1) / bm);
+    else {
+      const int64_t nt = (m + bm - 1) / bm;
+      if (split_small && m - (nt - 1) * bm <= bm / 2) {
+        run += (int32_t)(nt - 1);
+        ++run2;
+      } else {
+        run += (int32_t)nt;
+      }
+    }
   }
   prefix[E] = run;
+  prefix2[E] = run2;
   list1[0] = n1;
   list2[0] = n2;
 }
@@ -472,6 +486,7 @@ constexpr int kMaxPieces = 512;
 constexpr size_t kPieceBytes = 256 * 64 * 16;
 static_assert(BM == BN, "A and B stages share the piece layout");
 static_assert(STAGES * 2 * kStage * 2 <= 160 * 1024, "LDS");
+static_assert(STAGES == 4 || STAGES == 5, "the K loop is written for four or five stages");
 __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r / RPW) % CPR); }
 }  // namespace fast
 
@@ -506,6 +521,7 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
                  int64_t F, int64_t H,
                  const int32_t* __restrict__ offsets, const int32_t* __restrict__ slot,
                  int E, int64_t max_rows, const int32_t* __restrict__ prefix,
+                 const int32_t* __restrict__ prefix2,
                  int32_t* __restrict__ claim, int32_t* __restrict__ tail,
                  float* __restrict__ partial, int max_pieces, uint16_t* __restrict__ C) {
   constexpr int BM = fast::BM, BN = fast::BN, BK = fast::BK, STAGES = fast::STAGES;
@@ -517,12 +533,20 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   const int64_t ldc = N_out;
   const int64_t n_tiles = (N_out + kOutN - 1) / kOutN;
 
+  constexpr int kStage4 = STAGES > 4 ? kStage : 8;   // a fifth stage, or only the claim words
   __shared__ __attribute__((aligned(1024))) uint16_t As0[kStage], As1[kStage], As2[kStage], As3[kStage];
   __shared__ __attribute__((aligned(1024))) uint16_t Bs0[kStage], Bs1[kStage], Bs2[kStage], Bs3[kStage];
-  uint16_t* const As[4] = {As0, As1, As2, As3};
-  uint16_t* const Bs[4] = {Bs0, Bs1, Bs2, Bs3};
-  __shared__ int64_t s_claim;
-  __shared__ int s_piece, s_last;
+  __shared__ __attribute__((aligned(1024))) uint16_t As4[kStage4];
+  __shared__ __attribute__((aligned(1024))) uint16_t Bs4[STAGES > 4 ? kStage : 1];
+  uint16_t* const As[5] = {As0, As1, As2, As3, As4};
+  uint16_t* const Bs[5] = {Bs0, Bs1, Bs2, Bs3, Bs4};
+  // The claim broadcast lives in the fifth A stage: it is written and read
+  // between tiles, when no DMA targets that stage (a tile's first STAGES - 1
+  // steps load stages 0 .. STAGES - 2), and s_last after every wave has left
+  // the K loop.
+  int64_t& s_claim = *reinterpret_cast<int64_t*>(As4);
+  int& s_piece = *reinterpret_cast<int*>(As4 + 4);
+  int& s_last = *reinterpret_cast<int*>(As4 + 6);
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -532,7 +556,10 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   const int lrow = lane / CPR;                // row within a DMA piece
   const int lpch = lane % CPR;                // physical chunk this lane fills
 
-  const int64_t total = (int64_t)prefix[E] * n_tiles;
+  // tiles: every expert's full-cost row tiles (prefix), then the small last
+  // row tiles (prefix2), each in (expert, column tile, row tile) order
+  const int64_t total_big = (int64_t)prefix[E] * n_tiles;
+  const int64_t total = total_big + (int64_t)prefix2[E] * n_tiles;
   if (total == 0) return;                      // every expert went to the few-row kernels
   const int64_t G = gridDim.x;                 // persistent grid, a multiple of 8
   const int64_t per_xcd = G / 8;
@@ -556,6 +583,7 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
 
   bool in_tail = false;                        // thread 0 only
   // thread 0: the next whole-round claim, issued while the current tile runs
@@ -593,15 +621,28 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
     const int64_t nks = split_tile ? (piece + 1) * ksteps / split - kbeg : ksteps;
     // the last expert whose first tile is at or before t (binary search)
     int e = 0;
-    for (int hi = E - 1; e < hi;) {
-      const int mid = (e + hi + 1) >> 1;
-      if ((int64_t)prefix[mid] * n_tiles <= t) e = mid;
-      else hi = mid - 1;
+    int64_t nt, mt;
+    if (t < total_big) {
+      for (int hi = E - 1; e < hi;) {
+        const int mid = (e + hi + 1) >> 1;
+        if ((int64_t)prefix[mid] * n_tiles <= t) e = mid;
+        else hi = mid - 1;
+      }
+      const int64_t local = t - (int64_t)prefix[e] * n_tiles;
+      const int64_t me = prefix[e + 1] - prefix[e];
+      nt = local / me;
+      mt = local - nt * me;
+    } else {
+      const int64_t u = t - total_big;
+      const int64_t si = u / n_tiles;          // which small row tile
+      for (int hi = E - 1; e < hi;) {
+        const int mid = (e + hi + 1) >> 1;
+        if ((int64_t)prefix2[mid] <= si) e = mid;
+        else hi = mid - 1;
+      }
+      nt = u - si * n_tiles;
+      mt = prefix[e + 1] - prefix[e];          // after the expert's full-cost tiles
     }
-    const int64_t local = t - (int64_t)prefix[e] * n_tiles;
-    const int64_t me = prefix[e + 1] - prefix[e];
-    const int64_t nt = local / me;
-    const int64_t mt = local - nt * me;
     const int s = slot ? slot[e] : e;
     int64_t lo = offsets[e];
     lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
@@ -704,6 +745,18 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
           for (int ni = 0; ni < NI; ++ni)
             acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[ni], acc[mi][ni], 0, 0, 0);
       };
+      // Wait until at most n steps issued after the awaited one are in flight.
+      auto wait_steps = [&](int64_t n) {
+        if constexpr (STAGES >= 5) {
+          if (n >= 3) {
+            wait_vmcnt<3 * 2 * PPW>();
+            return;
+          }
+        }
+        if (n >= 2) wait_vmcnt<2 * 2 * PPW>();
+        else if (n == 1) wait_vmcnt<2 * PPW>();
+        else wait_vmcnt<0>();
+      };
       // One K-step on stage J: DMA of step kt+3 into stage J+3 (mod 4); the
       // second half-step's fragments are read while the first half's MFMAs
       // run; wait for step kt+1; barrier; the next step's first fragments are
@@ -714,10 +767,7 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
           issue(std::integral_constant<int, (J + STAGES - 1) % STAGES>{}, kt + STAGES - 1);
         rd(j_c, 1, fa1, fb1);
         mm(fa0, fb0);
-        const int64_t later = min(kt + STAGES - 1, nks - 1) - (kt + 1);
-        if (later >= 2) wait_vmcnt<2 * 2 * PPW>();
-        else if (later == 1) wait_vmcnt<2 * PPW>();
-        else wait_vmcnt<0>();
+        wait_steps(min(kt + STAGES - 1, nks - 1) - (kt + 1));
         lds_barrier();
         if (kt + 1 < nks) rd(std::integral_constant<int, (J + 1) % STAGES>{}, 0, fa0, fb0);
         mm(fa1, fb1);
@@ -742,8 +792,9 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
           __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         }
-        // outstanding after step kt+1: A,B of kt+2 and A of kt+3
-        wait_vmcnt<3 * PPW>();
+        // outstanding after step kt+1: A and B of steps kt+2 .. kt+STAGES-2,
+        // A of kt+STAGES-1
+        wait_vmcnt<(2 * (STAGES - 3) + 1) * PPW>();
         lds_barrier();
         issue_b(std::integral_constant<int, JN>{}, kt + STAGES - 1);
         rd(std::integral_constant<int, (J + 1) % STAGES>{}, 0, fa0, fb0);
@@ -764,12 +815,9 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
       if (0 < nks) issue(I0{}, 0);
       if (1 < nks) issue(I1{}, 1);
       if (2 < nks) issue(I2{}, 2);
-      {
-        const int64_t inflight = min((int64_t)STAGES - 1, nks) - 1;
-        if (inflight >= 2) wait_vmcnt<2 * 2 * PPW>();
-        else if (inflight == 1) wait_vmcnt<2 * PPW>();
-        else wait_vmcnt<0>();
-      }
+      if constexpr (STAGES >= 5)
+        if (3 < nks) issue(I3{}, 3);
+      wait_steps(min((int64_t)STAGES - 1, nks) - 1);
       // every wave has its own pieces of step 0; the barrier makes that true
       // of all of them (LDS only: steps 1 and 2 keep loading)
       lds_barrier();
@@ -780,16 +828,20 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
         step_ss(I1{}, kt + 1);
         step_ss(I2{}, kt + 2);
         step_ss(I3{}, kt + 3);
+        if constexpr (STAGES >= 5) step_ss(I4{}, kt + 4);
       }
       for (; kt + STAGES <= nks; kt += STAGES) {
         step(I0{}, kt);
         step(I1{}, kt + 1);
         step(I2{}, kt + 2);
         step(I3{}, kt + 3);
+        if constexpr (STAGES >= 5) step(I4{}, kt + 4);
       }
       if (kt < nks) step(I0{}, kt);
       if (kt + 1 < nks) step(I1{}, kt + 1);
       if (kt + 2 < nks) step(I2{}, kt + 2);
+      if constexpr (STAGES >= 5)
+        if (kt + 3 < nks) step(I3{}, kt + 3);
 
       // A K-piece stores its fp32 partial tile; the piece that arrives last
       // (a device-scope counter per tail tile, ordered by release and acquire
@@ -995,7 +1047,7 @@ extern "C" size_t moe_expert_ffn_workspace(int64_t max_rows, int64_t H, int64_t 
   if (max_rows < 1 || H < 1 || F < 1 || E < 1 || !valid_dtype(dtype)) return 0;
   const size_t elt = dtype == MOE_BF16 ? 2 : 4;
   size_t bytes = align_up((size_t)max_rows * (size_t)F * elt, 256);
-  bytes += align_up((size_t)(E + 1 + kCounterWords + 2 * (E + 1)) * sizeof(int32_t), 256);
+  bytes += align_up((size_t)(E + 1 + kCounterWords + 3 * (E + 1)) * sizeof(int32_t), 256);
   if (dtype == MOE_BF16 && fast_path(H, F))
     bytes += (size_t)max_split_pieces(max_rows, H, F, E) * fast::kPieceBytes;
   return bytes;
@@ -1048,10 +1100,11 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
   const int small_tiles =
       fast && std::max(H, F) < ((int64_t)1 << 25) && max_rows <= 32 * (int64_t)E ? 2 : 0;
   ffn_tiles_kernel<<<dim3(1), dim3(64), 0, st>>>(expert_offsets, slot_of_expert, E, S, max_rows,
-                                                 bm, small_tiles, prefix);
+                                                 bm, small_tiles, fast ? 1 : 0, prefix);
   MOE_CHECK_LAUNCH();
   const int32_t* const list1 = prefix + E + 1 + kCounterWords;
   const int32_t* const list2 = list1 + E + 1;
+  const int32_t* const prefix2 = list2 + E + 1;
   const bool few = small_tiles > 0;
   const bool big = max_rows > 16 * small_tiles;  // else every expert has few rows
   const bool mid = few && max_rows > 16;          // else none has 17 to 32
@@ -1067,7 +1120,7 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
     int32_t* const claim = prefix + E + 1;
     int32_t* const tail = claim + kClaimWords;
     float* const partial = reinterpret_cast<float*>(
-        reinterpret_cast<char*>(prefix) + align_up((size_t)(E + 1 + kCounterWords + 2 * (E + 1)) * 4, 256));
+        reinterpret_cast<char*>(prefix) + align_up((size_t)(E + 1 + kCounterWords + 3 * (E + 1)) * 4, 256));
     const int pieces = (int)max_split_pieces(max_rows, H, F, E);
     // two blocks per compute unit, striding over the few-row experts' units
     // (more blocks in flight spread the reads over more DRAM rows at once and
@@ -1078,7 +1131,7 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
     if (big) {
       ffn_gemm_bf16_fast<0><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
           xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
-          claim, tail, partial, pieces, ab);
+          prefix2, claim, tail, partial, pieces, ab);
       MOE_CHECK_LAUNCH();
     }
     if (few && !mid) {
@@ -1093,7 +1146,7 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
     if (big) {
       ffn_gemm_bf16_fast<1><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
           ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
-          claim + 8, tail + kTailWords, partial, pieces, yb);
+          prefix2, claim + 8, tail + kTailWords, partial, pieces, yb);
       MOE_CHECK_LAUNCH();
     }
     if (few && !mid) {

@@ -60,6 +60,8 @@ def test_tiny_fp32_config():
     ([700, 3, 0, 1029, 64], 512, 1408),    # Qwen-like F
     ([300, 5, 260], 136, 200),             # H, F not multiples of 32: general path
     ([40, 300], 264, 96),                  # general path, K tail inside a 64-deep step
+    ([263, 544, 300, 1025, 0, 287], 256, 512),   # small last row tiles (7, 32, 44, 1, 31 rows)
+    ([257, 7, 288], 512, 1408),            # small last row tiles next to a lone 7-row expert
 ])
 def test_bf16_ragged_groups(counts, H, F):
     _run(counts, H, F, None, len(counts), seed=sum(counts) + H)
@@ -68,6 +70,7 @@ def test_bf16_ragged_groups(counts, H, F):
 @pytest.mark.parametrize("counts,H,F", [
     ([300, 40, 200], 1024, 4096),      # both GEMMs split their only, partial round along K
     ([9, 1100, 257, 31], 512, 2048),   # split down projection over ragged tiles of every size
+    ([280, 530], 1024, 4096),          # the split round holds small last row tiles (24, 18 rows)
 ])
 def test_bf16_split_k_tail(counts, H, F):
     # Fewer tiles than compute units: the last round is split into K-pieces
