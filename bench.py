@@ -288,7 +288,7 @@ def decode_report(args):
     wg, wu, wd = (up(inp[n]) for n in ("w_gate", "w_up", "w_down"))
     flush = torch.empty(512 * 2 ** 20 // 4, dtype=torch.float32, device=dev)
     out = []
-    for T in (4, 16, 64, 256):
+    for T in (4, 16, 64, 128, 256):
         x = up(inp["x"][:T])
         ws_p = ops.workspace_tensor(ops.permute_workspace(T, k, E), dev)
         ws_f = ops.workspace_tensor(ops.expert_ffn_workspace(T * k, H, F, E), dev)

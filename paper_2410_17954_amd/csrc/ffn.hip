@@ -46,13 +46,15 @@ constexpr int kTailWords = 1 + kMaxTailTiles;
 constexpr int kCounterWords = kClaimWords + 2 * kTailWords;
 
 // Per-expert row-tile prefix of resident experts; also clears the counters.
-// Resident experts with at most 16 * small_tiles rows (small_tiles 0, 1 or 2)
-// get no row tiles here: they are listed for the few-row kernels instead,
-// those with at most 16 rows in one list and those with 17 to 32 in another
-// (list[0] = the number of experts, list[1..] = their ids in ascending order).
+// Resident experts with at most 16 * small_tiles rows (small_tiles 0 or
+// kSmallMaxTiles) get no row tiles here: they are listed for the few-row
+// kernel instead (small[0] = their number, small[1..] = their ids, those with
+// the most 16-row tiles first, ascending ids within a tile count).
 // With split_small an expert's last row tile, when it holds at most bm / 2
 // rows, is counted apart (prefix2: 0 or 1 per expert), so that the GEMMs can
 // run every expert's full-cost row tiles first and the small ones last.
+constexpr int kSmallMaxTiles = 6;              // few-row experts: at most 96 rows
+
 __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
                                  const int32_t* __restrict__ slot, int E, int S,
                                  int64_t max_rows, int bm, int small_tiles, int split_small,
@@ -60,22 +62,25 @@ __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
   if (blockIdx.x != 0) return;
   for (int q = threadIdx.x; q < kCounterWords; q += blockDim.x) prefix[E + 1 + q] = 0;
   if (threadIdx.x != 0) return;
-  int32_t* const list1 = prefix + E + 1 + kCounterWords;
-  int32_t* const list2 = list1 + E + 1;
-  int32_t* const prefix2 = list2 + E + 1;
-  int32_t run = 0, run2 = 0, n1 = 0, n2 = 0;
-  for (int e = 0; e < E; ++e) {
-    prefix[e] = run;
-    prefix2[e] = run2;
+  int32_t* const small = prefix + E + 1 + kCounterWords;
+  int32_t* const prefix2 = small + E + 1;
+  int32_t run = 0, run2 = 0;
+  int32_t n_of[kSmallMaxTiles + 1] = {};
+  auto rows_of = [&](int e) -> int64_t {
     const int s = slot ? slot[e] : e;
     int64_t lo = offsets[e], hi = offsets[e + 1];
     lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
     hi = hi < lo ? lo : (hi > max_rows ? max_rows : hi);
-    if (s < 0 || s >= S || hi == lo) continue;
-    const int64_t m = hi - lo;
-    if (m <= 16 * small_tiles && m <= 16) list1[1 + n1++] = e;
-    else if (m <= 16 * small_tiles) list2[1 + n2++] = e;
-    else {
+    return (s < 0 || s >= S) ? 0 : hi - lo;
+  };
+  for (int e = 0; e < E; ++e) {
+    prefix[e] = run;
+    prefix2[e] = run2;
+    const int64_t m = rows_of(e);
+    if (m == 0) continue;
+    if (m <= 16 * small_tiles) {
+      ++n_of[(m + 15) / 16];
+    } else {
       const int64_t nt = (m + bm - 1) / bm;
       if (split_small && m - (nt - 1) * bm <= bm / 2) {
         run += (int32_t)(nt - 1);
@@ -87,8 +92,20 @@ __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
   }
   prefix[E] = run;
   prefix2[E] = run2;
-  list1[0] = n1;
-  list2[0] = n2;
+  // few-row experts by descending tile count: the grid strides over their
+  // units in list order, so the costliest units start first
+  int32_t at[kSmallMaxTiles + 1];
+  int32_t n = 0;
+  for (int c = kSmallMaxTiles; c >= 1; --c) {
+    at[c] = n;
+    n += n_of[c];
+  }
+  small[0] = n;
+  if (n == 0) return;
+  for (int e = 0; e < E; ++e) {
+    const int64_t m = rows_of(e);
+    if (m > 0 && m <= 16 * small_tiles) small[1 + at[(m + 15) / 16]++] = e;
+  }
 }
 
 // silu(g) * u with the hardware exp2 and reciprocal (about 2 ulp of float32,
@@ -284,35 +301,48 @@ ffn_gemm_bf16(const uint16_t* __restrict__ A, int64_t K,
 }
 
 // ------------------------------------------------------- few rows per expert
-// An expert with at most 16 * MT rows (decode-sized batches; MT = 1 or 2) is
+// An expert with at most 16 * kSmallMaxTiles rows (decode-sized batches) is
 // bound by reading its weights once, not by MFMA. A block of four waves owns
-// kSmallCols output columns (weight rows) of one such expert; wave w streams
-// the w-th quarter of the K range of those rows with 16x16x32 MFMAs (the
-// expert's rows padded to 16 * MT with zeros, which are never loaded), and
-// the four partial sums are added through LDS in wave order. Splitting K inside the
-// block, rather than giving each wave its own columns, keeps the addresses
-// the whole chip reads at one time close together, which DRAM serves faster.
-constexpr int kSmallNT = 2;                      // 16-column MFMA tiles per block
-constexpr int kSmallCols = 16 * kSmallNT;
-constexpr int kSmallU = 4;                       // K steps of 32 loaded per batch
+// one unit: SmallShape<EPI>::COLS output columns (weight rows) of one such
+// expert, all of its rows; wave w streams the w-th quarter of the K range of
+// those weight rows with 16x16x32 MFMAs (the expert's rows padded to 16 * MT,
+// MT = ceil(rows / 16)), and the four partial sums are added through LDS.
+// Splitting K inside the block, rather than giving each wave its own columns,
+// keeps the addresses the whole chip reads at one time close together, which
+// DRAM serves faster. A unit has four 16-column tiles of weights per K step
+// (gate and up of 32 columns, or 64 columns of the down projection), so the
+// activation fragments a wave loads (again in every unit of the expert, from
+// L2) are MT/4 of its weight loads; those extra load instructions, not the
+// MFMAs, are what slows the unit as MT grows.
 constexpr int kSmallWaves = 4;
+constexpr int kSmallRC = 2;                      // row tiles per LDS reduction pass
 
-// MTMAX = 1: the experts of list1 (at most 16 rows); MTMAX = 2: those of list1
-// and then those of list2 (17 to 32 rows, two row tiles) in one launch, each
-// unit taking the body for its row tiles (the branch is uniform per block).
+template <int EPI>
+struct SmallShape {
+  static constexpr int NB = EPI == 0 ? 2 : 1;    // gate and up, or down
+  static constexpr int NT = 4 / NB;              // 16-column MFMA tiles per unit
+  static constexpr int COLS = 16 * NT;
+};
+// K steps of 32 loaded per batch: four while the rows' fragments are few,
+// two for three or more row tiles (registers)
+template <int MT>
+constexpr int small_unroll() { return MT <= 2 ? 4 : 2; }
+
+// MTMAX: the most row tiles of any listed expert the launch supports; each
+// unit takes the body for its expert's tile count (uniform per block).
 template <int EPI, int MTMAX>
-__global__ void __launch_bounds__(64 * kSmallWaves)
+__global__ void __launch_bounds__(64 * kSmallWaves) __attribute__((amdgpu_waves_per_eu(2)))
 ffn_small_bf16(const uint16_t* __restrict__ A, int64_t K, const uint16_t* __restrict__ B0,
                const uint16_t* __restrict__ B1, int64_t F, int64_t H,
                const int32_t* __restrict__ offsets, const int32_t* __restrict__ slot,
-               int64_t max_rows, const int32_t* __restrict__ list1,
-               const int32_t* __restrict__ list2, uint16_t* __restrict__ C) {
-  constexpr int NB = EPI == 0 ? 2 : 1;           // gate and up, or down
-  __shared__ f32x4_t part[kSmallWaves][MTMAX][kSmallNT][NB][kWave];
-  const int64_t N_out = EPI == 0 ? F : H;        // a multiple of kSmallCols (fast path)
-  const int ncb = (int)(N_out / kSmallCols);
-  const int64_t units1 = (int64_t)list1[0] * ncb;
-  const int64_t units = units1 + (MTMAX == 2 ? (int64_t)list2[0] * ncb : 0);
+               int64_t max_rows, const int32_t* __restrict__ small, uint16_t* __restrict__ C) {
+  using SS = SmallShape<EPI>;
+  constexpr int NB = SS::NB, NT = SS::NT;
+  constexpr int RC = MTMAX < kSmallRC ? MTMAX : kSmallRC;
+  __shared__ f32x4_t part[kSmallWaves][RC][NT][NB][kWave];
+  const int64_t N_out = EPI == 0 ? F : H;        // a multiple of 32 (fast path)
+  const int ncb = (int)((N_out + SS::COLS - 1) / SS::COLS);
+  const int64_t units = (int64_t)small[0] * ncb;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
   const int r = lane & 15;                       // A row / B column of this lane
@@ -320,24 +350,19 @@ ffn_small_bf16(const uint16_t* __restrict__ A, int64_t K, const uint16_t* __rest
   const int64_t ks = K / 32;
   const int64_t per = (ks + kSmallWaves - 1) / kSmallWaves;
   const int64_t kb = min(ks, wave * per), ke = min(ks, kb + per);
-  const int64_t kfull = kb + (ke - kb) / kSmallU * kSmallU;
   // byte offset of this lane's B slice from a weight tile's first row
   const uint32_t b_off = (uint32_t)(((int64_t)r * K + kq) * 2);
-  // units (expert, column block) in order, the grid striding over them: at any
-  // time the blocks work on neighbouring columns
-  auto run_unit = [&](auto mt_c, int e, int cb) {
+  auto run_unit = [&](auto mt_c, int e, int cb, int m, int64_t lo) {
     constexpr int MT = decltype(mt_c)::value;
+    constexpr int U = small_unroll<MT>();
     const int s = slot ? slot[e] : e;
-    int64_t lo = offsets[e], hi = offsets[e + 1];
-    lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
-    hi = hi < lo ? lo : (hi > max_rows ? max_rows : hi);
-    const int m = (int)min(hi - lo, (int64_t)(16 * MT));
-    const int64_t n0 = (int64_t)cb * kSmallCols;
+    const int64_t kfull = kb + (ke - kb) / U * U;
+    const int64_t n0 = (int64_t)cb * SS::COLS;
     // wave-uniform bases plus 32-bit lane offsets. With one row tile, lanes of
     // rows past m load nothing (masked off, so no data comes back) and feed
-    // zeros; with two, every lane loads (rows past m read the expert's last
+    // zeros; with more, every lane loads (rows past m read the expert's last
     // row, whose products land in rows that are never stored): most of those
-    // lanes are live, and the masks would cost registers and occupancy.
+    // lanes are live, and the masks would cost registers.
     const char* const a_base = reinterpret_cast<const char*>(A + lo * K);
     uint32_t a_off[MT];
     bool a_on[MT];
@@ -346,91 +371,108 @@ ffn_small_bf16(const uint16_t* __restrict__ A, int64_t K, const uint16_t* __rest
       a_on[i] = 16 * i + r < m;
       a_off[i] = (uint32_t)(((int64_t)min(16 * i + r, m - 1) * K + kq) * 2);
     }
-    const char* b_base[kSmallNT][NB];
+    // a column tile past N_out (the last unit of a down projection whose
+    // width is an odd multiple of 32) re-reads the unit's first tile and is
+    // not stored
+    const char* b_base[NT][NB];
 #pragma unroll
-    for (int j = 0; j < kSmallNT; ++j) {
-      b_base[j][0] = reinterpret_cast<const char*>(B0 + ((int64_t)s * N_out + n0 + 16 * j) * K);
+    for (int j = 0; j < NT; ++j) {
+      const int64_t n = n0 + 16 * j < N_out ? n0 + 16 * j : n0;
+      b_base[j][0] = reinterpret_cast<const char*>(B0 + ((int64_t)s * N_out + n) * K);
       if constexpr (EPI == 0)
-        b_base[j][1] = reinterpret_cast<const char*>(B1 + ((int64_t)s * N_out + n0 + 16 * j) * K);
+        b_base[j][1] = reinterpret_cast<const char*>(B1 + ((int64_t)s * N_out + n) * K);
     }
-    f32x4_t acc[MT][kSmallNT][NB];
+    f32x4_t acc[MT][NT][NB];
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < kSmallNT; ++j)
+      for (int j = 0; j < NT; ++j)
 #pragma unroll
         for (int b = 0; b < NB; ++b) acc[i][j][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     auto steps = [&](int64_t s0, auto n_c) {
       constexpr int NS = decltype(n_c)::value;
-      uint4 a[NS][MT], w[NS][kSmallNT][NB];
+      uint4 a[NS][MT], w[NS][NT][NB];
 #pragma unroll
       for (int u = 0; u < NS; ++u) {
         const int64_t kbyte = (s0 + u) * 64;
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
-          a[u][i] = (MT == 2 || a_on[i]) ? *reinterpret_cast<const uint4*>(a_base + kbyte + a_off[i])
-                                         : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int j = 0; j < kSmallNT; ++j)
+        for (int j = 0; j < NT; ++j)
 #pragma unroll
           for (int b = 0; b < NB; ++b)
             w[u][j][b] = __builtin_bit_cast(uint4, __builtin_nontemporal_load(
                 reinterpret_cast<const u32x4_t*>(b_base[j][b] + kbyte + b_off)));
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+          a[u][i] = (MT > 1 || a_on[i]) ? *reinterpret_cast<const uint4*>(a_base + kbyte + a_off[i])
+                                        : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
       for (int u = 0; u < NS; ++u)
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
-          for (int j = 0; j < kSmallNT; ++j)
+          for (int j = 0; j < NT; ++j)
 #pragma unroll
             for (int b = 0; b < NB; ++b)
               acc[i][j][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                   __builtin_bit_cast(bf16x8_t, a[u][i]), __builtin_bit_cast(bf16x8_t, w[u][j][b]),
                   acc[i][j][b], 0, 0, 0);
     };
-    for (int64_t s0 = kb; s0 < kfull; s0 += kSmallU) steps(s0, std::integral_constant<int, kSmallU>{});
+    for (int64_t s0 = kb; s0 < kfull; s0 += U) steps(s0, std::integral_constant<int, U>{});
     for (int64_t s0 = kfull; s0 < ke; ++s0) steps(s0, std::integral_constant<int, 1>{});
+    // the four waves' partial sums, RC row tiles at a time: every wave writes
+    // its own, then wave q adds up the (row tile, column tile) groups g with
+    // g % 4 == q and stores them. C layout of the 16x16 MFMA: lane holds
+    // column (lane % 16), rows 4 * (lane / 16) + q of its 16-row tile.
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+    for (int i0 = 0; i0 < MT; i0 += RC) {
 #pragma unroll
-      for (int j = 0; j < kSmallNT; ++j)
+      for (int ii = 0; ii < RC; ++ii)
+        if (i0 + ii < MT)
 #pragma unroll
-        for (int b = 0; b < NB; ++b) part[wave][i][j][b][lane] = acc[i][j][b];
-    __syncthreads();
-    // C layout of the 16x16 MFMA: lane holds column (lane % 16), rows
-    // 4 * (lane / 16) + q of its 16-row tile.
-    if (wave == 0) {
+          for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+            for (int b = 0; b < NB; ++b) part[wave][ii][j][b][lane] = acc[i0 + ii][j][b];
+      __syncthreads();
+      const int groups = (MT - i0 < RC ? MT - i0 : RC) * NT;
+      for (int g = wave; g < groups; g += kSmallWaves) {
+        const int ii = g / NT, j = g % NT;
+        const int64_t col = n0 + 16 * j + r;
+        f32x4_t t[NB];
 #pragma unroll
-        for (int j = 0; j < kSmallNT; ++j) {
-          f32x4_t t[NB];
+        for (int b = 0; b < NB; ++b) {
+          t[b] = part[0][ii][j][b][lane];
 #pragma unroll
-          for (int b = 0; b < NB; ++b) {
-            t[b] = part[0][i][j][b][lane];
-#pragma unroll
-            for (int q = 1; q < kSmallWaves; ++q) t[b] += part[q][i][j][b][lane];
-          }
-          const int64_t col = n0 + 16 * j + r;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int rr = 16 * i + (lane >> 4) * 4 + q;
-            if (rr >= m) continue;
-            const float v = EPI == 0 ? swiglu(t[0][q], t[1][q]) : t[0][q];
-            C[(lo + rr) * N_out + col] = f32_to_bf16(v);
-          }
+          for (int q = 1; q < kSmallWaves; ++q) t[b] += part[q][ii][j][b][lane];
         }
+        if (col >= N_out) continue;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int rr = 16 * (i0 + ii) + (lane >> 4) * 4 + q;
+          if (rr >= m) continue;
+          const float v = EPI == 0 ? swiglu(t[0][q], t[NB - 1][q]) : t[0][q];
+          C[(lo + rr) * N_out + col] = f32_to_bf16(v);
+        }
+      }
+      __syncthreads();                             // part is rewritten next
     }
-    __syncthreads();                               // part is rewritten by the next unit
   };
+  // units (expert, column block) in list order, the grid striding over them:
+  // at any time the blocks work on neighbouring columns
   for (int64_t unit = blockIdx.x; unit < units; unit += gridDim.x) {
-    if (MTMAX == 1 || unit < units1) {
-      run_unit(std::integral_constant<int, 1>{}, list1[1 + (int)(unit / ncb)], (int)(unit % ncb));
-    } else if constexpr (MTMAX == 2) {
-      const int64_t u = unit - units1;
-      run_unit(std::integral_constant<int, 2>{}, list2[1 + (int)(u / ncb)], (int)(u % ncb));
-    }
+    const int e = small[1 + (int)(unit / ncb)];
+    const int cb = (int)(unit % ncb);
+    int64_t lo = offsets[e], hi = offsets[e + 1];
+    lo = lo < 0 ? 0 : (lo > max_rows ? max_rows : lo);
+    hi = hi < lo ? lo : (hi > max_rows ? max_rows : hi);
+    const int m = (int)(hi - lo);                  // 1 .. 16 * MTMAX (the list's rule)
+    const int mt = (m + 15) / 16;
+    if (mt <= 1) run_unit(std::integral_constant<int, 1>{}, e, cb, m, lo);
+    else if (mt == 2) { if constexpr (MTMAX >= 2) run_unit(std::integral_constant<int, 2>{}, e, cb, m, lo); }
+    else if (mt == 3) { if constexpr (MTMAX >= 3) run_unit(std::integral_constant<int, 3>{}, e, cb, m, lo); }
+    else if (mt == 4) { if constexpr (MTMAX >= 4) run_unit(std::integral_constant<int, 4>{}, e, cb, m, lo); }
+    else if (mt == 5) { if constexpr (MTMAX >= 5) run_unit(std::integral_constant<int, 5>{}, e, cb, m, lo); }
+    else { if constexpr (MTMAX >= 6) run_unit(std::integral_constant<int, 6>{}, e, cb, m, lo); }
   }
 }
 
@@ -1047,7 +1089,7 @@ extern "C" size_t moe_expert_ffn_workspace(int64_t max_rows, int64_t H, int64_t 
   if (max_rows < 1 || H < 1 || F < 1 || E < 1 || !valid_dtype(dtype)) return 0;
   const size_t elt = dtype == MOE_BF16 ? 2 : 4;
   size_t bytes = align_up((size_t)max_rows * (size_t)F * elt, 256);
-  bytes += align_up((size_t)(E + 1 + kCounterWords + 3 * (E + 1)) * sizeof(int32_t), 256);
+  bytes += align_up((size_t)(E + 1 + kCounterWords + 2 * (E + 1)) * sizeof(int32_t), 256);
   if (dtype == MOE_BF16 && fast_path(H, F))
     bytes += (size_t)max_split_pieces(max_rows, H, F, E) * fast::kPieceBytes;
   return bytes;
@@ -1092,22 +1134,23 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
 
   const bool fast = fast_path(H, F);
   const int bm = fast ? fast::BM : BM;
-  // Experts with at most 32 rows go to the weight-streaming kernels when the
-  // batch is decode-sized (at most 32 rows per expert on average): bf16, H and
-  // F multiples of 32 (the fast-path shapes), 32-bit lane offsets within 32
-  // rows of K. Larger batches leave the rare small expert to the large tiles
-  // and launch no few-row kernel at all.
+  // Experts with at most 16 * kSmallMaxTiles rows go to the weight-streaming
+  // kernel when the batch is decode-sized (at most 64 rows per expert on
+  // average): bf16, H and F multiples of 32 (the fast-path shapes), 32-bit lane
+  // offsets within 96 rows of K. Larger batches leave the rare small expert to
+  // the large tiles and launch no few-row kernel at all.
   const int small_tiles =
-      fast && std::max(H, F) < ((int64_t)1 << 25) && max_rows <= 32 * (int64_t)E ? 2 : 0;
+      fast && std::max(H, F) < ((int64_t)1 << 24) && max_rows <= 64 * (int64_t)E ? kSmallMaxTiles : 0;
   ffn_tiles_kernel<<<dim3(1), dim3(64), 0, st>>>(expert_offsets, slot_of_expert, E, S, max_rows,
                                                  bm, small_tiles, fast ? 1 : 0, prefix);
   MOE_CHECK_LAUNCH();
-  const int32_t* const list1 = prefix + E + 1 + kCounterWords;
-  const int32_t* const list2 = list1 + E + 1;
-  const int32_t* const prefix2 = list2 + E + 1;
+  const int32_t* const small = prefix + E + 1 + kCounterWords;
+  const int32_t* const prefix2 = small + E + 1;
   const bool few = small_tiles > 0;
   const bool big = max_rows > 16 * small_tiles;  // else every expert has few rows
-  const bool mid = few && max_rows > 16;          // else none has 17 to 32
+  // the most row tiles a listed expert can have, rounded up to a compiled bound
+  const int64_t few_tiles = std::min<int64_t>(ceil_div(max_rows, 16), small_tiles);
+  const int mtmax = few_tiles <= 1 ? 1 : few_tiles <= 2 ? 2 : few_tiles <= 4 ? 4 : 6;
   int grid = device_cu_count();
   grid = std::min((grid + 7) / 8 * 8, kMaxTailTiles);     // a tail round has < grid tiles
   const auto* xb = static_cast<const uint16_t*>(x_perm);
@@ -1120,27 +1163,41 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
     int32_t* const claim = prefix + E + 1;
     int32_t* const tail = claim + kClaimWords;
     float* const partial = reinterpret_cast<float*>(
-        reinterpret_cast<char*>(prefix) + align_up((size_t)(E + 1 + kCounterWords + 3 * (E + 1)) * 4, 256));
+        reinterpret_cast<char*>(prefix) + align_up((size_t)(E + 1 + kCounterWords + 2 * (E + 1)) * 4, 256));
     const int pieces = (int)max_split_pieces(max_rows, H, F, E);
     // two blocks per compute unit, striding over the few-row experts' units
     // (more blocks in flight spread the reads over more DRAM rows at once and
-    // measured slower; fewer leave bandwidth unused); with no such expert each
-    // block does one load
-    const int64_t small_units = (int64_t)E * ceil_div(std::max(F, H), kSmallCols);
-    const unsigned small_grid = (unsigned)std::min<int64_t>(2 * (int64_t)device_cu_count(), small_units);
+    // measured slower; fewer leave bandwidth unused); with few units each
+    // block does one
+    auto small_grid = [&](int64_t n_out, int cols) {
+      return (unsigned)std::min<int64_t>(2 * (int64_t)device_cu_count(), (int64_t)E * ceil_div(n_out, cols));
+    };
+    auto launch_small = [&](auto epi_c, const uint16_t* a, int64_t K, const uint16_t* b0,
+                            const uint16_t* b1, uint16_t* c) {
+      constexpr int EPI = decltype(epi_c)::value;
+      const unsigned g = small_grid(EPI == 0 ? F : H, SmallShape<EPI>::COLS);
+      const dim3 blk(64 * kSmallWaves);
+      if (mtmax == 1)
+        ffn_small_bf16<EPI, 1><<<dim3(g), blk, 0, st>>>(a, K, b0, b1, F, H, expert_offsets,
+                                                        slot_of_expert, max_rows, small, c);
+      else if (mtmax == 2)
+        ffn_small_bf16<EPI, 2><<<dim3(g), blk, 0, st>>>(a, K, b0, b1, F, H, expert_offsets,
+                                                        slot_of_expert, max_rows, small, c);
+      else if (mtmax == 4)
+        ffn_small_bf16<EPI, 4><<<dim3(g), blk, 0, st>>>(a, K, b0, b1, F, H, expert_offsets,
+                                                        slot_of_expert, max_rows, small, c);
+      else
+        ffn_small_bf16<EPI, 6><<<dim3(g), blk, 0, st>>>(a, K, b0, b1, F, H, expert_offsets,
+                                                        slot_of_expert, max_rows, small, c);
+    };
     if (big) {
       ffn_gemm_bf16_fast<0><<<dim3(grid), dim3(fast::kThreads), 0, st>>>(
           xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, E, max_rows, prefix,
           prefix2, claim, tail, partial, pieces, ab);
       MOE_CHECK_LAUNCH();
     }
-    if (few && !mid) {
-      ffn_small_bf16<0, 1><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, ab);
-      MOE_CHECK_LAUNCH();
-    } else if (mid) {
-      ffn_small_bf16<0, 2><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          xb, H, wgb, wub, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, ab);
+    if (few) {
+      launch_small(std::integral_constant<int, 0>{}, xb, H, wgb, wub, ab);
       MOE_CHECK_LAUNCH();
     }
     if (big) {
@@ -1149,13 +1206,8 @@ extern "C" int moe_expert_ffn(const void* x_perm, int32_t dtype, int64_t max_row
           prefix2, claim + 8, tail + kTailWords, partial, pieces, yb);
       MOE_CHECK_LAUNCH();
     }
-    if (few && !mid) {
-      ffn_small_bf16<1, 1><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, yb);
-      MOE_CHECK_LAUNCH();
-    } else if (mid) {
-      ffn_small_bf16<1, 2><<<dim3(small_grid), dim3(64 * kSmallWaves), 0, st>>>(
-          ab, F, wdb, nullptr, F, H, expert_offsets, slot_of_expert, max_rows, list1, list2, yb);
+    if (few) {
+      launch_small(std::integral_constant<int, 1>{}, ab, F, wdb, nullptr, yb);
       MOE_CHECK_LAUNCH();
     }
     return MOE_OK;

@@ -140,31 +140,38 @@ def test_full_shape_every_row(name):
     ([2, 7, 0, 5], 192, 320),               # K = 6 and 10 steps of 32: partial batches
     ([17, 32, 16, 33, 24], 256, 416),       # two-tile experts (17..32 rows) beside the others
     ([31, 1, 29], 160, 96),                 # K = 5 and 3 steps: every wave's range is short
+    ([33, 48, 49, 64, 1, 17], 256, 416),    # three and four row tiles beside one and two
+    ([65, 80, 96, 40, 3], 192, 320),        # five and six row tiles; K = 6 and 10 steps
+    ([70, 2, 50], 160, 96),                 # down projection 160 wide: a half-empty last unit
+    ([96, 96], 512, 1408),                  # every expert at the few-row limit (96 rows)
+    ([81, 0, 0, 35], 128, 64),              # K = 4 and 2 steps with six and three row tiles
 ])
 def test_bf16_few_rows_per_expert(counts, H, F):
-    # in decode-sized batches experts with at most 32 rows take the
-    # weight-streaming kernels
+    # in decode-sized batches experts with at most 96 rows take the
+    # weight-streaming kernel
     _run(counts, H, F, None, len(counts), seed=sum(counts) + H + F)
 
 
-def test_bf16_few_rows_resident_subset():
-    # decode-sized batch (at most 32 rows per expert on average) with one
+@pytest.mark.parametrize("counts,slot,S,extra", [
+    ([3, 0, 16, 1, 120, 9], [1, 0, -1, 3, 2, -1], 4, 5),
+    ([97, 5, 60, 33], [2, 0, 1, -1], 3, 0),     # 97 rows: one row past the few-row limit
+])
+def test_bf16_few_rows_resident_subset(counts, slot, S, extra):
+    # decode-sized batch (at most 64 rows per expert on average) with one
     # expert large enough for the large tiles
-    counts = [3, 0, 16, 1, 120, 9]
-    slot = [1, 0, -1, 3, 2, -1]
-    _run(counts, 256, 384, slot, 4, seed=23, extra_rows=5)
+    _run(counts, 256, 384, slot, S, seed=23 + sum(counts), extra_rows=extra)
 
 
-@pytest.mark.parametrize("T", [24, 100])
-def test_full_shape_decode_batch(T):
-    """Decode-sized batch at the full 8-expert shape (H 4096, F 14336): 24 or
-    100 tokens with top-2 give up to 16, or 17 to 32, rows per expert; every
-    row is checked."""
+@pytest.mark.parametrize("T,lo,hi", [(24, 1, 16), (100, 17, 32), (160, 33, 64), (256, 49, 96)])
+def test_full_shape_decode_batch(T, lo, hi):
+    """Decode-sized batch at the full 8-expert shape (H 4096, F 14336): 24,
+    100, 160 or 256 tokens with top-2 give at most one, two, four or six
+    16-row tiles per expert; every row is checked."""
     cfg = synth.workload("mixtral8x7b_layer")
     E, H, F, k = cfg["E"], cfg["H"], cfg["F"], cfg["k"]
     idx = synth.random_topk_idx(T, E, k, seed=77)
     counts = np.bincount(idx.ravel(), minlength=E)
-    assert counts.max() <= (16 if T == 24 else 32)
+    assert lo <= counts.max() <= hi
     offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
     R = int(offsets[-1])
     inp = synth.layer_inputs(cfg, 2, T=R, parts=("x", "experts"))
