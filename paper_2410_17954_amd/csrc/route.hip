@@ -180,14 +180,15 @@ __device__ __forceinline__ uint4 abs_bf16x8(uint4 v) {
 }
 
 // K-steps (of 32) accumulated in one float32 chain before it is added to the
-// float64 accumulator.
+// float64 accumulator (the kernel for up to 32 or more than 64 experts; the
+// one for 33-64 experts closes chains of one or four K-steps).
 constexpr int kChainSteps = 8;
 
 // Exactness of the decision. A logit is an exact sum of exact bf16 products
 // (8-bit significands: every product is exact in float32). Each product passes
-// through at most 32 * kChainSteps float32 additions (one chain, whatever the
-// order inside the matrix core) before the chain is added in float64, so
-// |z_f32 - z| <= 2 gamma_n S + tiny with n = 32 * kChainSteps + 1 and
+// through at most 32 * CH float32 additions (one chain of CH K-steps, whatever
+// the order inside the matrix core) before the chain is added in float64, so
+// |z_f32 - z| <= 2 gamma_n S + tiny with n = 32 * CH + 1 and
 // S = sum_h |x_h w_eh| (the factor 2 covers directed rounding inside the
 // matrix core; the float64 additions and the final rounding to float32 are the
 // rest). The float32 top-k is exact, set and order, when the intervals
@@ -209,7 +210,7 @@ struct DecideLds {
   int* npairs;
 };
 
-template <int EP, int TB, int NW>
+template <int EP, int TB, int NW, int CH>
 __device__ __forceinline__ void route_decide(const DecideLds<EP>& s, const uint16_t* __restrict__ x,
                                              const uint16_t* __restrict__ wg, int64_t T, int64_t H,
                                              int E, int k, const float* __restrict__ bias,
@@ -224,9 +225,9 @@ __device__ __forceinline__ void route_decide(const DecideLds<EP>& s, const uint1
   const int wave = threadIdx.x / kWave;
   const int grp = lane / kRowLanes, gl = lane % kRowLanes;
   const float u = 5.9604645e-8f;                  // 2^-24
-  const float nacc = (float)(32 * kChainSteps + 1);
+  const float nacc = (float)(32 * CH + 1);
   const float gam = nacc * u / (1.f - nacc * u);
-  const float f64_part = (float)((H / (32 * kChainSteps) + NW + 4) * 2.3e-16);
+  const float f64_part = (float)((H / (32 * CH) + NW + 4) * 2.3e-16);
   const float cb = 1.01f * (2.f * gam / (1.f - 2.f * gam) + f64_part);
   auto bound = [&](float z, float sabs) { return cb * sabs + 2.02f * u * fabsf(z); };
 
@@ -573,8 +574,8 @@ route_ksplit_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__
   if (threadIdx.x == 0) npairs = 0;
   __syncthreads();
   const DecideLds<EP> s{zf, sacc, zacc, sel, lk, need, pairs, &npairs};
-  route_decide<EP, TB, KS>(s, x, wg, T, H, E, k, bias, bias_mode, renorm, tok0, logits, topk_idx,
-                           topk_w);
+  route_decide<EP, TB, KS, kChainSteps>(s, x, wg, T, H, E, k, bias, bias_mode, renorm, tok0,
+                                        logits, topk_idx, topk_w);
 }
 
 // 33..64 experts: 64 tokens per block, one wave per 16-token tile over the
@@ -587,6 +588,10 @@ constexpr int kWPitch = kWChunk + 8;              // padded row (bank spread)
 // used (measured at 8192 Qwen-shaped tokens: 64-token tiles, 128 blocks, 59 us;
 // 32, 256 blocks, 46 us; 16, 512 blocks, 41 us)
 constexpr int kRouteTileBlocks = 2;
+// float32 chain of the 33-64-expert kernel: one K-step while a wave holds one
+// or two 16-expert blocks, four for four blocks (one K-step there needs more
+// registers than the wave has)
+constexpr int route_tile_chain(int tb) { return tb <= 32 ? 1 : 4; }
 
 // TB tokens per block (64, 32 or 16): TB / 16 tiles of 16 tokens, the waves
 // of a tile splitting the 64 expert columns between them.
@@ -601,8 +606,9 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
   constexpr int WPT = NW / TT;                    // waves per tile
   constexpr int NEBW = NEB / WPT;                 // 16-expert blocks per wave
   static_assert(TT * WPT == NW && NEBW * WPT == NEB, "tile split");
-  constexpr int SS = kWChunk / 32;                // K-steps per chunk (= kChainSteps)
-  static_assert(SS == kChainSteps, "one float32 chain per chunk");
+  constexpr int SS = kWChunk / 32;                // K-steps per chunk
+  constexpr int CH = route_tile_chain(TB);        // K-steps per float32 chain
+  static_assert(SS % CH == 0, "whole chains per chunk");
   constexpr int WV = EP * kWChunk / 8 / (NW * kWave);   // 16-byte W pieces per thread
   __shared__ __attribute__((aligned(16))) uint16_t wsh[EP * kWPitch];   // later: z64
   __shared__ float zf[TB][EP];
@@ -669,8 +675,10 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
       load_x(c + 1, xn);
       load_w(c + 1, wr);
     }
-#pragma unroll
-    for (int nb = 0; nb < NEBW; ++nb) acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // float32 chains of CH K-steps (CH MFMAs, 32 CH products) added into
+    // float64: the decision's bounds are those of 32 CH + 1 float32
+    // additions (8 / CH times tighter than for 8-step chains), so far fewer
+    // tokens need the float64 recomputation
 #pragma unroll
     for (int u = 0; u < SS; ++u) {
       const bf16x8_t av = __builtin_bit_cast(bf16x8_t, xc[u]);
@@ -679,16 +687,19 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
       for (int nb = 0; nb < NEBW; ++nb) {
         const int eb = eg * NEBW + nb;
         const uint4 bv = *reinterpret_cast<const uint4*>(&wsh[(eb * 16 + row) * kWPitch + u * 32 + kq]);
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8_t, bv),
-                                                          acc[nb], 0, 0, 0);
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            av, __builtin_bit_cast(bf16x8_t, bv),
+            u % CH == 0 ? f32x4_t{0.f, 0.f, 0.f, 0.f} : acc[nb], 0, 0, 0);
         acs[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             aa, __builtin_bit_cast(bf16x8_t, abs_bf16x8(bv)), acs[nb], 0, 0, 0);
       }
+      if ((u + 1) % CH == 0) {
+#pragma unroll
+        for (int nb = 0; nb < NEBW; ++nb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) a64[nb][i] += (double)acc[nb][i];
+      }
     }
-#pragma unroll
-    for (int nb = 0; nb < NEBW; ++nb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a64[nb][i] += (double)acc[nb][i];
     __syncthreads();                              // every wave is done with this chunk
     if (more) {
       store_w(wr);
@@ -715,8 +726,8 @@ route_tiles_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ 
   __syncthreads();
   const DecideLds<EP> s{zf, sf, reinterpret_cast<double(*)[EP]>(wsh), sel, lk, need, pairs,
                         &npairs};
-  route_decide<EP, TB, NW>(s, x, wg, T, H, E, k, bias, bias_mode, renorm, tok0, logits, topk_idx,
-                           topk_w);
+  route_decide<EP, TB, NW, CH>(s, x, wg, T, H, E, k, bias, bias_mode, renorm, tok0, logits,
+                               topk_idx, topk_w);
 }
 
 // float32 inputs: logits in float64 (products of two floats are exact in
