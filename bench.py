@@ -44,6 +44,10 @@ def parse():
                         "a Qwen-shaped layer with 32 of 60 experts resident, misses loaded "
                         "from pinned host memory while the resident experts compute, and "
                         "PLEC against per-layer LRU hit ratios on synthetic predicted routes")
+    p.add_argument("--decode-ts", action="store_true",
+                   help="instead of the layer throughput, run decode-sized two-batch units "
+                        "through the Qwen-shaped layer in input order and as the token "
+                        "scheduler splits them")
     p.add_argument("--decode", action="store_true",
                    help="instead of the layer throughput, measure decode-sized batches of the "
                         "Mixtral-shaped layer (4 to 256 tokens, all 8 experts resident): "
@@ -338,6 +342,129 @@ def decode_report(args):
            "config": {"workload": f"Mixtral-8x7B-shaped layer: H={H}, E={E}, F={F}, top-{k}, "
                                   "all experts resident, weights read from HBM every step"},
            "steps": out, "data": "synthetic"}
+    print(json.dumps(rec))
+
+
+def decode_ts_report(args):
+    """The token scheduler on decode-sized scheduling units (Sec. 3.3): two
+    batches of B tokens whose predicted routes over L = 24 Qwen-shaped layers
+    carry topic structure (two topics, each token on its own topic's Markov
+    chain), run through all 24 layers (60 experts, top-4, every expert
+    resident; shared experts and attention left out: their cost does not
+    depend on the batching), once in input order and once as the scheduler
+    splits the unit. Layer l has its own router, and its gating is boosted by
+    4 towards the token's predicted layer-l route, so the experts a batch
+    activates at each layer are the ones Eq. 2 counts. Expert weights cycle
+    through 8 distinct sets (8.3 GB), so every layer reads its experts from
+    HBM. Per order: Eq. 2 (active (layer, expert) pairs summed over the
+    batches), the expert-weight bytes read, and the time of the two batches
+    through the layers (moe_permute + moe_expert_ffn + moe_combine per layer
+    and batch; routing is the same per token in both orders and is done
+    beforehand), HIP events, median of 5 after warm-up, a 512 MB fill before
+    each run; for the scheduled order also moe_schedule. One JSON line."""
+    import torch
+    from paper_2410_17954_amd import ops, synth
+
+    dev = torch.device("cuda:0")
+    cfg = synth.workload("qwen15_moe_layer")
+    H, E, F, k, L = cfg["H"], cfg["E"], cfg["F"], cfg["k"], cfg["L"]
+    topics, boost, n_sets = 2, 4.0, 8
+    Bmax = 64
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed)
+
+    def normal(shape, std):
+        return (torch.randn(shape, generator=g, device=dev) * std).to(torch.bfloat16)
+
+    sets = [(normal((E, F, H), 0.02), normal((E, F, H), 0.02), normal((E, H, F), 0.02))
+            for _ in range(n_sets)]
+    routers = [normal((E, H), 0.02) for _ in range(L)]
+    x_all = normal((2 * Bmax, H), 1.0)
+    flush = torch.empty(512 * 2 ** 20 // 4, dtype=torch.float32, device=dev)
+    wbytes_expert = 3 * H * F * 2
+    out = []
+    for B in (8, 16, 32, 64):
+        N = 2 * B
+        routes = synth.topic_routes(N, L, E, k, cfg["keep"], cfg["zipf"], topics, args.seed + B)
+        x = x_all[:N].contiguous()
+        rt = torch.from_numpy(np.ascontiguousarray(routes, dtype=np.uint8)).to(dev)
+        idx_l, gw_l = [], []
+        for l in range(L):
+            bias = torch.from_numpy(synth.route_boost_bias(routes, l, E, boost)).to(dev)
+            i_, w_, _ = ops.route(x, routers[l], k, bias=bias)
+            idx_l.append(i_)
+            gw_l.append(w_)
+        idx_host = [i_.cpu().numpy() for i_ in idx_l]
+        ws_s = ops.workspace_tensor(ops.schedule_workspace(N, L, E, k), dev)
+        perm = torch.empty(N, dtype=torch.int32, device=dev)
+        demand = torch.empty((2, L, E), dtype=torch.int32, device=dev)
+        info = torch.empty(8, dtype=torch.int64, device=dev)
+        ws_p = ops.workspace_tensor(ops.permute_workspace(B, k, E), dev)
+        ws_f = ops.workspace_tensor(ops.expert_ffn_workspace(B * k, H, F, E), dev)
+        offs = torch.empty(E + 1, dtype=torch.int32, device=dev)
+        rop = torch.empty(B * k, dtype=torch.int32, device=dev)
+        por = torch.empty(B * k, dtype=torch.int32, device=dev)
+        xp = torch.empty((B * k, H), dtype=torch.bfloat16, device=dev)
+        yp = torch.empty_like(xp)
+        y = torch.empty((N, H), dtype=torch.bfloat16, device=dev)
+        inc = torch.empty(B, dtype=torch.int32, device=dev)
+        natural = torch.arange(N, dtype=torch.int32, device=dev)
+
+        def through_layers(tids):
+            for l in range(L):
+                wg, wu, wd = sets[l % n_sets]
+                ops.permute(x, idx_l[l], E, token_ids=tids, expert_offsets=offs, row_of_pair=rop,
+                            pair_of_row=por, x_perm=xp, workspace=ws_p)
+                ops.expert_ffn(xp, offs, wg, wu, wd, y_perm=yp, workspace=ws_f)
+                ops.combine(yp, idx_l[l], gw_l[l], rop, token_ids=tids, y=y, incomplete=inc)
+
+        rec = {"tokens_per_batch": B}
+        for name in ("input_order", "scheduled"):
+            t_sched, t_layers = [], []
+            for rep in range(args.warmup + 5):
+                flush.fill_(float(rep))
+                torch.cuda._sleep(1000000)
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                ev[0].record()
+                if name == "scheduled":
+                    ops.schedule(rt, E, perm=perm, demand=demand, info=info, workspace=ws_s)
+                    order = perm
+                else:
+                    order = natural
+                ev[1].record()
+                for b in range(2):
+                    through_layers(order[b * B:(b + 1) * B])
+                ev[2].record()
+                torch.cuda.synchronize()
+                if rep >= args.warmup:
+                    t_sched.append(ev[0].elapsed_time(ev[1]))
+                    t_layers.append(ev[1].elapsed_time(ev[2]))
+            o = order.cpu().numpy()
+            pairs = 0
+            for b in range(2):
+                rows = o[b * B:(b + 1) * B]
+                pairs += sum(int(np.unique(idx_host[l][rows]).size) for l in range(L))
+            layers_ms = float(np.median(t_layers))
+            wgb = pairs * wbytes_expert / 1e9
+            rec[name] = {"active_layer_expert_pairs": pairs,
+                         "expert_weight_GB": round(wgb, 2),
+                         "layers_ms": round(layers_ms, 3),
+                         "weight_GBps": round(wgb / (layers_ms * 1e-3), 1)}
+            if name == "scheduled":
+                rec[name]["schedule_ms"] = round(float(np.median(t_sched)), 4)
+                rec[name]["eq2_predicted_before_after"] = [int(info[4].item()), int(info[5].item())]
+        a_, s_ = rec["input_order"], rec["scheduled"]
+        rec["speedup_with_schedule"] = round(a_["layers_ms"] / (s_["layers_ms"] + s_["schedule_ms"]), 3)
+        out.append(rec)
+    rec = {"metric": "token scheduling on decode-sized units: active (layer, expert) pairs, "
+                     "expert-weight bytes and time through 24 layers, input order against "
+                     "scheduled",
+           "config": {"workload": f"Qwen1.5-MoE-shaped layers: L={L}, H={H}, E={E}, F={F}, "
+                                  f"top-{k}, every expert resident, no shared experts or "
+                                  f"attention; units of two batches; predicted routes with "
+                                  f"{topics} topics (keep {cfg['keep']}, zipf {cfg['zipf']}), "
+                                  f"gating boosted {boost} towards each layer's predicted route"},
+           "units": out, "data": "synthetic"}
     print(json.dumps(rec))
 
 
@@ -1091,6 +1218,9 @@ def main():
         sys.exit(2)
     if args.ece:
         ece_report(args)
+        return
+    if args.decode_ts:
+        decode_ts_report(args)
         return
     if args.decode:
         decode_report(args)
