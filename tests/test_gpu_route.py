@@ -130,3 +130,32 @@ def test_x_mode_crafted_exact_and_near_ties():
     idx, _, _ = ops.route(to_dev(x), to_dev(w), k)
     z_ref = oracle.router_logits(synth.values(x), synth.values(w))
     assert np.array_equal(to_host(idx), oracle.topk_select(z_ref, k))
+
+
+@pytest.mark.parametrize("T", [64, 40000])
+def test_x_mode_crafted_ties_60_experts(T):
+    """The 33-64-expert kernel (float32 chains of one K-step in 16-token
+    tiles, of four in 64-token tiles): strong router rows that tie exactly or
+    differ by one bf16 ulp in one element sit in most tokens' top-4, so the
+    certificate fails and the float64 recomputation decides; the result must
+    match the float64 oracle, exact ties going to the lower expert id."""
+    g = np.random.default_rng(23)
+    H, E, k = 512, 60, 4
+    wf = (g.standard_normal((E, H)) * 0.02).astype(np.float32)
+    wf[[1, 9, 33], 7] = 0.5                   # with x[:, 7] = 3: usually selected
+    w = synth.bf16_bits(wf)
+    w[12] = w[1]                              # exact tie with expert 1
+    w[40] = w[9]
+    w[40, 3] ^= 1                             # one ulp from expert 9 in one element
+    w[59] = w[33]                             # exact tie, the higher id last
+    w[20] = w[33]
+    w[20, 200] += 1
+    x = synth.bf16_bits(g.standard_normal((T, H)).astype(np.float32))
+    x[:, 7] = synth.bf16_bits(np.full(T, 3.0, np.float32))
+    idx, _, _ = ops.route(to_dev(x), to_dev(w), k)
+    z_ref = oracle.router_logits(synth.values(x), synth.values(w))
+    got = to_host(idx)
+    assert np.array_equal(got, oracle.topk_select(z_ref, k))
+    # seven strong experts compete for four places: the crafted pairs are
+    # decided in a large share of the tokens
+    assert (got == 12).any(axis=1).mean() > 0.4 and (got == 59).any(axis=1).mean() > 0.4
