@@ -1415,6 +1415,10 @@ def main():
     # and combine also write, and read data written just before)
     stages["route"]["frac_of_dirty_cache_read"] = (stages["route"]["GB/s"] /
                                                    ceilings["read_64MiB_dirty_GBps"])
+    # permute and combine read and write: against the plain copy in that state
+    for name in ("permute", "combine"):
+        stages[name]["frac_of_dirty_cache_copy"] = (stages[name]["GB/s"] /
+                                                    ceilings["copy_64MiB_dirty_GBps"])
     stages["expert_ffn"]["mfma_frac_measured"] = achieved / ceilings["mfma_bf16_TFLOPs"]
 
     out = {
@@ -1517,13 +1521,31 @@ def measured_ceilings(torch, ops, dev):
     warm = state(lambda rep: read(a))
     clean = state(lambda rep: read(big))
     dirty = state(lambda rep: big.fill_(rep))
+    # a plain copy of 64 MiB into a second buffer after a 512 MiB write (the
+    # state permute and combine run in: reads and writes, dirty lines to
+    # write back); bytes counted read plus written
+    dst = torch.empty_like(a)
+    cts = []
+    for rep in range(6):
+        big.fill_(rep)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        if lib.moe_probe_copy(ops._ptr(a), ops._ptr(dst), a.numel(), st) != 0:
+            raise RuntimeError("moe_probe_copy failed")
+        e1.record()
+        torch.cuda.synchronize()
+        if rep:
+            cts.append(e0.elapsed_time(e1))
+    copy = 2 * a.numel() / (float(np.median(cts)) * 1e-3) / 1e9
     return {"mfma_bf16_TFLOPs": flops / (ms * 1e-3) / 1e12,
             "hbm_read_GBps": buf.numel() / (rms * 1e-3) / 1e9,
             "read_64MiB_warm_GBps": warm, "read_64MiB_clean_GBps": clean,
-            "read_64MiB_dirty_GBps": dirty,
+            "read_64MiB_dirty_GBps": dirty, "copy_64MiB_dirty_GBps": copy,
             "probes": "moe_probe_mfma_bf16 (4 waves per SIMD, 8 MFMA chains, "
                       f"{iters} rounds), moe_probe_read (1 GiB, one pass; 64 MiB after a "
-                      "read of it, after a 512 MiB read, after a 512 MiB write)"}
+                      "read of it, after a 512 MiB read, after a 512 MiB write), "
+                      "moe_probe_copy (64 MiB to a second buffer after a 512 MiB write, "
+                      "read + written bytes)"}
 
 
 def measured_traffic():

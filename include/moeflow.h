@@ -309,11 +309,15 @@ int moe_rpp_forward(const int32_t* ids, int32_t B, int32_t S, const moe_rpp_dims
  * moe_probe_read reads `bytes` (a multiple of 16, 16-byte aligned DEVICE
  * memory) once with one 16-byte load per lane, grid-stride, and writes one
  * word per thread to out (out_len >= 2048 x compute units).
+ * moe_probe_copy copies `bytes` (a multiple of 16) from src to dst (16-byte
+ * aligned DEVICE buffers that do not overlap) with one 16-byte load and store
+ * per lane, grid-stride.
  * ---------------------------------------------------------------------- */
 int64_t moe_probe_mfma_bf16(const void* src, int64_t iters, float* out, int32_t out_len,
                             void* stream);
 int moe_probe_read(const void* src, int64_t bytes, uint32_t* out, int32_t out_len,
                    void* stream);
+int moe_probe_copy(const void* src, void* dst, int64_t bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * moe_permute -- group the (token, choice) pairs of one batch by expert so

@@ -56,6 +56,13 @@ probe_read_kernel(const uint4* __restrict__ p, int64_t n, uint32_t* __restrict__
   out[blockIdx.x * blockDim.x + threadIdx.x] = acc;
 }
 
+__global__ void __launch_bounds__(256)
+probe_copy_kernel(const uint4* __restrict__ p, int64_t n, uint4* __restrict__ q) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    q[i] = p[i];
+}
+
 }  // namespace
 }  // namespace moe
 
@@ -81,6 +88,18 @@ extern "C" int moe_probe_read(const void* src, int64_t bytes, uint32_t* out, int
   MOE_CHECK_ARG(out_len >= blocks * 256);
   probe_read_kernel<<<dim3((unsigned)blocks), dim3(256), 0, as_stream(stream)>>>(
       static_cast<const uint4*>(src), bytes / 16, out);
+  MOE_CHECK_LAUNCH();
+  return MOE_OK;
+}
+
+extern "C" int moe_probe_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+  using namespace moe;
+  MOE_CHECK_ARG(src && dst && bytes >= 16 && bytes % 16 == 0 &&
+                (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
+                (reinterpret_cast<uintptr_t>(dst) & 15) == 0);
+  const int64_t blocks = 8 * (int64_t)device_cu_count();
+  probe_copy_kernel<<<dim3((unsigned)blocks), dim3(256), 0, as_stream(stream)>>>(
+      static_cast<const uint4*>(src), bytes / 16, static_cast<uint4*>(dst));
   MOE_CHECK_LAUNCH();
   return MOE_OK;
 }

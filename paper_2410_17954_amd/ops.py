@@ -55,6 +55,7 @@ def load_library(path=None):
                                     I32, I32, I32, P, ctypes.c_float, P, P, P, P, SZ, P]),
         "moe_probe_mfma_bf16": (I64, [P, I64, P, I32, P]),
         "moe_probe_read": (I32, [P, I64, P, I32, P]),
+        "moe_probe_copy": (I32, [P, P, I64, P]),
         "moe_rpp_weights_count": (SZ, [P]),
         "moe_rpp_workspace": (SZ, [I32, I32, P]),
         "moe_rpp_forward": (I32, [P, I32, I32, P, P, P, P, P, P, SZ, P]),
@@ -94,7 +95,7 @@ def exported_symbols():
             "moe_expert_ffn_workspace", "moe_expert_ffn", "moe_combine", "moe_kv_gather",
             "moe_kv_reindex", "moe_stack_workspace", "moe_stack_forward",
             "moe_rpp_weights_count", "moe_rpp_workspace", "moe_rpp_forward",
-            "moe_probe_mfma_bf16", "moe_probe_read", "moe_plan_slots", "moe_plec_order",
+            "moe_probe_mfma_bf16", "moe_probe_read", "moe_probe_copy", "moe_plan_slots", "moe_plec_order",
             "moe_plec_run", "moe_lru_run", "moe_load_experts", "moe_plec_state_bytes",
             "moe_plec_begin", "moe_plec_layer", "moe_plec_advance"]
 

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported(lib):
     names = declared_functions()
-    assert len(names) == 32, names
+    assert len(names) == 33, names
     assert sorted(ops.exported_symbols()) == names
     for n in names:
         assert hasattr(lib, n)
@@ -219,3 +219,13 @@ def test_route_binarize_rejects_on_the_host(lib):
     assert lib.moe_route_binarize(FAKE, 0, 8, 2, FAKE, S) == ops.MOE_ERR_ARG
     assert lib.moe_route_binarize(FAKE, 10, 8, 9, FAKE, S) == ops.MOE_ERR_ARG
     assert lib.moe_route_binarize(FAKE, 10, 257, 2, FAKE, S) == ops.MOE_ERR_ARG
+
+
+def test_probe_copy_rejects_on_the_host(lib):
+    # validated before any launch: null buffers, a size that is not a
+    # multiple of 16, a misaligned buffer (the pointers are never touched)
+    fake = ctypes.c_void_p(4096)
+    assert lib.moe_probe_copy(None, fake, 16, None) != 0
+    assert lib.moe_probe_copy(fake, fake, 24, None) != 0
+    assert lib.moe_probe_copy(ctypes.c_void_p(4104), fake, 16, None) != 0
+    assert lib.moe_probe_copy(fake, fake, 0, None) != 0
