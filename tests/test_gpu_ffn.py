@@ -162,6 +162,27 @@ def test_bf16_few_rows_resident_subset(counts, slot, S, extra):
     _run(counts, 256, 384, slot, S, seed=23 + sum(counts), extra_rows=extra)
 
 
+def test_bf16_few_rows_many_experts_subset():
+    # decode-sized batch over 256 experts (the few-row list built from all of
+    # them, ids sorted by row tiles), a fifth of them not resident, many empty,
+    # one row past the few-row limit
+    g = np.random.default_rng(5)
+    E = 256
+    counts = np.where(g.random(E) < 0.4, 0, g.integers(1, 80, size=E))
+    counts[17] = 97
+    slot = np.full(E, -1, np.int32)
+    res = np.flatnonzero(g.random(E) < 0.8)
+    slot[res] = np.arange(len(res), dtype=np.int32)
+    assert counts.sum() <= 64 * E
+    _run(counts, 64, 96, slot, len(res), seed=5, extra_rows=3)
+
+
+def test_bf16_few_rows_nothing_to_do():
+    # decode-sized batch whose experts are all empty or not resident: the
+    # launches find no work and the output keeps its sentinel
+    _run([0, 5, 0, 9], 128, 256, [0, -1, 1, -1], 2, seed=8, extra_rows=4)
+
+
 @pytest.mark.parametrize("T,lo,hi", [(24, 1, 16), (100, 17, 32), (160, 33, 64), (256, 49, 96)])
 def test_full_shape_decode_batch(T, lo, hi):
     """Decode-sized batch at the full 8-expert shape (H 4096, F 14336): 24,
