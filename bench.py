@@ -1584,18 +1584,33 @@ def cpu_baseline(inp, routes, cfg, budget_s):
     t_sched = time.perf_counter() - t0
     chunk = 128
     done = 0
-    t_layer = 0.0
-    while done < N and (t_layer + t_sched) < budget_s:
+    t_stage = {"route": 0.0, "permute": 0.0, "expert_ffn": 0.0, "combine": 0.0}
+    slots = np.arange(E)
+    while done < N and (sum(t_stage.values()) + t_sched) < budget_s:
         tok = perm[done:done + chunk]
+        xb = np.asarray(x[tok], dtype=np.float64)
+        # the composition of oracle.moe_layer, one stage at a time
         t1 = time.perf_counter()
-        oracle.moe_layer(x[tok], wr, k, wg, wu, wd)
-        t_layer += time.perf_counter() - t1
+        _, idx, w = oracle.route(xb, wr, k)
+        t2 = time.perf_counter()
+        offs, rop, _, xp = oracle.permute(xb, idx, E)
+        t3 = time.perf_counter()
+        yp, _ = oracle.expert_ffn(xp, offs, slots, wg, wu, wd)
+        t4 = time.perf_counter()
+        oracle.combine(np.nan_to_num(yp), idx, w, rop, None, slots, None, n_out=xb.shape[0])
+        t5 = time.perf_counter()
+        for name, dt in zip(t_stage, (t2 - t1, t3 - t2, t4 - t3, t5 - t4)):
+            t_stage[name] += dt
         done += len(tok)
+    t_layer = sum(t_stage.values())
     per_token = t_sched / N + t_layer / max(done, 1)
+    rates = {"schedule": N / t_sched if t_sched > 0 else None}
+    rates.update({n: (done / t if t > 0 else None) for n, t in t_stage.items()})
     return {"value": 1.0 / per_token, "unit": "tokens/s", "cores": blas_threads,
             "kind": "oracle",
             "sample": (f"scheduler over all {N} tokens ({t_sched:.2f} s) + MoE layer on "
                        f"{done} tokens in {chunk}-token chunks ({t_layer:.2f} s), float64"),
+            "stage_tokens_per_s": rates,
             "affinity_cores": len(os.sched_getaffinity(0))}
 
 
