@@ -39,6 +39,11 @@ def load_library(path=None):
         raise RuntimeError(
             f"{path} is missing: build the HIP library first "
             "(python -c 'import __graft_entry__ as g; g.build()')")
+    # torch's HIP runtime first: the library's libamdhip64.so.7 then resolves
+    # to it, whereas loaded the other way round torch (which names the
+    # runtime without its version) brings a second runtime into the process
+    # and kernel launches from one fail on the other's device state
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     sig = {

@@ -229,3 +229,21 @@ def test_probe_copy_rejects_on_the_host(lib):
     assert lib.moe_probe_copy(fake, fake, 24, None) != 0
     assert lib.moe_probe_copy(ctypes.c_void_p(4104), fake, 16, None) != 0
     assert lib.moe_probe_copy(fake, fake, 0, None) != 0
+
+
+def test_one_hip_runtime_whatever_the_import_order(lib):
+    """Loading the library before torch must not bring a second HIP runtime
+    into the process (torch names the runtime without its version, the
+    library with it): the binding loads torch's first."""
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2410_17954_amd import ops\n"
+            "ops.load_library()\n"
+            "import torch\n"
+            "maps = open('/proc/self/maps').read().splitlines()\n"
+            "print(len({l.split()[-1] for l in maps if 'libamdhip64' in l}))\n") % ROOT
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.strip().splitlines()[-1] == "1"
