@@ -633,7 +633,15 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
 
   bool in_tail = false;                        // thread 0 only
   // thread 0: the next whole-round claim, issued while the current tile runs
-  int32_t j_next = tid == 0 ? atomicAdd(&claim[xcd], 1) : 0;
+  // The counter's address is made opaque so the compiler does not rewrite the
+  // one-lane atomic into its wave-aggregated form, which reads the result at
+  // once; this way the round trip overlaps the tile and only the next claim
+  // waits for it.
+  __attribute__((address_space(1))) int32_t* claim_x =
+      (__attribute__((address_space(1))) int32_t*)(claim + xcd);
+  asm volatile("" : "+v"(claim_x));
+  int32_t j_next =
+      tid == 0 ? __hip_atomic_fetch_add(claim_x, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
   for (;;) {
     if (tid == 0) {
       int64_t tt = -1;
@@ -661,7 +669,8 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
     const int64_t t = s_claim;
     const int piece = s_piece;
     if (t < 0) break;
-    if (tid == 0 && !in_tail) j_next = atomicAdd(&claim[xcd], 1);
+    if (tid == 0 && !in_tail)
+      j_next = __hip_atomic_fetch_add(claim_x, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const bool split_tile = t >= full && split > 1;
     const int64_t kbeg = split_tile ? piece * ksteps / split : 0;
     const int64_t nks = split_tile ? (piece + 1) * ksteps / split - kbeg : ksteps;
@@ -702,7 +711,10 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
     // DMA sources: a wave-uniform base per piece plus a 32-bit byte offset
     // per lane (the K offset is added to the base per step). Rows past the
     // end of the expert or of the weight read a valid row; their results are
-    // never stored.
+    // never stored. Inside the K loop the stepped base and the lane offset
+    // pass through empty asm, so the load takes the scalar-base form (SGPR
+    // pair + 32-bit VGPR offset) and the K step costs scalar adds, rather than
+    // 64-bit per-lane pointers stepped with vector adds.
     const char* const a_base = reinterpret_cast<const char*>(A + row0 * K);
     const char* b_base[PPW];
     uint32_t a_off[PPW], b_off[PPW];
@@ -732,21 +744,36 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
       const int64_t kb = (kbeg + step) * BK * 2;
 #pragma unroll
       for (int i = 0; i < PPW; ++i) {
-        lds_dma16(a_base + kb + a_off[i], As[stage] + (wave * PPW + i) * 512);
-        lds_dma16(b_base[i] + kb + b_off[i], Bs[stage] + (wave * PPW + i) * 512);
+        const char* ab = a_base + kb;
+        const char* bb = b_base[i] + kb;
+        uint32_t ao = a_off[i], bo = b_off[i];
+        asm("" : "+s"(ab), "+s"(bb), "+v"(ao), "+v"(bo));
+        lds_dma16(ab + ao, As[stage] + (wave * PPW + i) * 512);
+        lds_dma16(bb + bo, Bs[stage] + (wave * PPW + i) * 512);
       }
     };
     auto issue_a = [&](auto stage_c, int64_t step) {
       constexpr int stage = decltype(stage_c)::value;
       const int64_t kb = (kbeg + step) * BK * 2;
+      const char* ab = a_base + kb;
+      asm("" : "+s"(ab));
 #pragma unroll
-      for (int i = 0; i < PPW; ++i) lds_dma16(a_base + kb + a_off[i], As[stage] + (wave * PPW + i) * 512);
+      for (int i = 0; i < PPW; ++i) {
+        uint32_t ao = a_off[i];
+        asm("" : "+v"(ao));
+        lds_dma16(ab + ao, As[stage] + (wave * PPW + i) * 512);
+      }
     };
     auto issue_b = [&](auto stage_c, int64_t step) {
       constexpr int stage = decltype(stage_c)::value;
       const int64_t kb = (kbeg + step) * BK * 2;
 #pragma unroll
-      for (int i = 0; i < PPW; ++i) lds_dma16(b_base[i] + kb + b_off[i], Bs[stage] + (wave * PPW + i) * 512);
+      for (int i = 0; i < PPW; ++i) {
+        const char* bb = b_base[i] + kb;
+        uint32_t bo = b_off[i];
+        asm("" : "+s"(bb), "+v"(bo));
+        lds_dma16(bb + bo, Bs[stage] + (wave * PPW + i) * 512);
+      }
     };
 
     // MODE 0: 2 x 2 waves of 128 x 128; MODE m in {1, 2, 4}: 4 waves side by
