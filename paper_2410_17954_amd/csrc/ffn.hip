@@ -526,8 +526,11 @@ constexpr int PPW = PIECES / kWaves;        // pieces per wave per operand
 constexpr int kStage = BM * BK;             // elements per operand stage
 // Split-K of the last, partial round of tiles: at most kMaxSplit pieces per
 // tile, each at least kMinSplitSteps K-steps; a piece's fp32 partial tile is
-// 256 threads x 64 float4 (256 KB) in the workspace.
-constexpr int kMaxSplit = 8, kMinSplitSteps = 16;
+// 256 threads x 64 float4 (256 KB) in the workspace. A piece pays a prologue,
+// its partial tile's stores and a share of the final sum whatever its length,
+// which shorter pieces do not earn back: with K = 2048 (64 steps) four
+// 16-step pieces made the launch slower than no split at all.
+constexpr int kMaxSplit = 8, kMinSplitSteps = 64;
 constexpr int kMaxPieces = 512;
 constexpr size_t kPieceBytes = 256 * 64 * 16;
 static_assert(BM == BN, "A and B stages share the piece layout");

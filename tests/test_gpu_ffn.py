@@ -69,9 +69,10 @@ def test_bf16_ragged_groups(counts, H, F):
 
 
 @pytest.mark.parametrize("counts,H,F", [
-    ([300, 40, 200], 1024, 4096),      # both GEMMs split their only, partial round along K
-    ([9, 1100, 257, 31], 512, 2048),   # split down projection over ragged tiles of every size
-    ([280, 530], 1024, 4096),          # the split round holds small last row tiles (24, 18 rows)
+    ([300, 40, 200], 4096, 4096),      # both GEMMs split their only, partial round along K (2 pieces)
+    ([300, 40, 200], 1024, 8192),      # the down projection in 4 pieces
+    ([9, 1100, 257, 31], 512, 4096),   # split down projection over ragged tiles of every size
+    ([280, 530], 1024, 4096),          # the down projection's split round holds small last row tiles (24, 18 rows)
 ])
 def test_bf16_split_k_tail(counts, H, F):
     # Fewer tiles than compute units: the last round is split into K-pieces
