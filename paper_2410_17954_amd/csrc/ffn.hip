@@ -50,13 +50,13 @@ constexpr int kCounterWords = kClaimWords + 2 * kTailWords;
 // kSmallMaxTiles) get no row tiles here: they are listed for the few-row
 // kernel instead (small[0] = their number, small[1..] = their ids, those with
 // the most 16-row tiles first, ascending ids within a tile count).
-// With split_small an expert's last row tile, when it holds at most bm / 4
+// With split_small an expert's last row tile, when it holds at most bm / 8
 // rows, is counted apart (prefix2: 0 or 1 per expert), so that the GEMMs can
 // run every expert's full-cost row tiles first and these small ones last: a
 // tile that short runs its K loop several times faster than the full tiles
 // beside it, so kept in its column group it runs ahead of the tiles that share
 // its weights in L2 and streams them from HBM alone. A last tile of more than
-// bm / 4 rows keeps close enough pace to stay in place.
+// bm / 8 rows keeps close enough pace to stay in place.
 constexpr int kSmallMaxTiles = 6;              // few-row experts: at most 96 rows
 
 __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
@@ -86,7 +86,7 @@ __global__ void ffn_tiles_kernel(const int32_t* __restrict__ offsets,
       ++n_of[(m + 15) / 16];
     } else {
       const int64_t nt = (m + bm - 1) / bm;
-      if (split_small && m - (nt - 1) * bm <= bm / 4) {
+      if (split_small && m - (nt - 1) * bm <= bm / 8) {
         run += (int32_t)(nt - 1);
         ++run2;
       } else {
