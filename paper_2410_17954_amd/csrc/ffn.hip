@@ -612,12 +612,16 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   if (total == 0) return;                      // every expert went to the few-row kernels
   const int64_t G = gridDim.x;                 // persistent grid, a multiple of 8
   const int64_t per_xcd = G / 8;
+  // claim chunk: 16 consecutive tiles when that divides an XCD's share of a
+  // round (so the chunks of the 8 XCDs still cover each round exactly once),
+  // else the whole share
+  const int64_t chunk = per_xcd % 16 == 0 ? 16 : per_xcd;
   const int xcd = blockIdx.x % 8;
   const int64_t ksteps = K / BK;
 
   // Whole rounds of G tiles are claimed per XCD (each XCD walks its own
-  // chunks of per_xcd consecutive tiles, so the row tiles that share a weight
-  // tile run together on one L2). The last, partial round of rem tiles is
+  // chunks of consecutive tiles, so the row tiles that share a weight tile
+  // run together on one L2). The last, partial round of rem tiles is
   // split along K into `split` pieces claimed from one global counter,
   // chosen to minimise ceil(rem * split / G) / split rounds.
   const int64_t full = total / G * G;
@@ -651,7 +655,7 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
       int pc = 0;
       if (!in_tail) {
         const int64_t j = j_next;
-        const int64_t c = ((j / per_xcd) * 8 + xcd) * per_xcd + (j % per_xcd);
+        const int64_t c = ((j / chunk) * 8 + xcd) * chunk + (j % chunk);
         if (c < full) tt = c;
         else in_tail = true;
       }
