@@ -63,6 +63,7 @@ def test_tiny_fp32_config():
     ([263, 544, 300, 1025, 0, 287], 256, 512),   # small last row tiles (7, 32, 44, 1, 31 rows)
     ([257, 7, 288], 512, 1408),            # small last row tiles next to a lone 7-row expert
     ([356, 326, 320, 321, 128, 96, 288], 256, 512),  # last tiles of 100, 70, 64, 65 rows stay in place, 32 goes last
+    ([1400, 300, 2100], 256, 512),         # experts of 6 and 9 full-cost row tiles
 ])
 def test_bf16_ragged_groups(counts, H, F):
     _run(counts, H, F, None, len(counts), seed=sum(counts) + H)
