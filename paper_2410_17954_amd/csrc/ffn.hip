@@ -612,10 +612,15 @@ ffn_gemm_bf16_fast(const uint16_t* __restrict__ A, int64_t K,
   if (total == 0) return;                      // every expert went to the few-row kernels
   const int64_t G = gridDim.x;                 // persistent grid, a multiple of 8
   const int64_t per_xcd = G / 8;
-  // claim chunk: 16 consecutive tiles when that divides an XCD's share of a
-  // round (so the chunks of the 8 XCDs still cover each round exactly once),
-  // else the whole share
-  const int64_t chunk = per_xcd % 16 == 0 ? 16 : per_xcd;
+  // Claim chunk: an XCD's whole share of a round, or 16 consecutive tiles
+  // when some expert has 8 or more full-cost row tiles (a column's row tiles
+  // then fill a 32-tile chunk by themselves, one weight tile against 32
+  // activation panels; 16 divides the share, so the chunks of the 8 XCDs
+  // still cover each round exactly once). With at most 7 row tiles per expert
+  // the larger chunk cuts fewer column groups across two XCDs' L2s.
+  int64_t me_max = 0;
+  for (int ee = 0; ee < E; ++ee) me_max = max(me_max, (int64_t)(prefix[ee + 1] - prefix[ee]));
+  const int64_t chunk = me_max >= 8 && per_xcd % 16 == 0 ? 16 : per_xcd;
   const int xcd = blockIdx.x % 8;
   const int64_t ksteps = K / BK;
 
